@@ -1,0 +1,17 @@
+"""CPU oracle for grid EventProp with learnable delays.
+
+TEST INFRASTRUCTURE ONLY: the checker, not the product.  Only ``tests/``,
+``__graft_entry__.smoke()`` and the CPU-baseline leg of ``bench.py`` may import
+it.  It shares no code with the HIP library (``paper_2501_07331_amd``), and the
+library never imports it.
+
+* ``snn_oracle.c`` (built into ``liboracle.so`` by ``oracle/build.py``): the
+  plain single-threaded grid forward (fp32), CE loss (fp64) and backward
+  (fp64 definition, or the fp32 kernel-precision model).
+* ``continuous.py``: an fp64 event-driven simulator of the continuous-time
+  system of Table 1 for tiny networks, with the exact EventProp backward and
+  a finite-difference check; it pins the grid oracle.
+"""
+from .grid import (OracleNet, constants, forward, loss, backward, lib_path, ForwardResult)
+
+__all__ = ["OracleNet", "constants", "forward", "loss", "backward", "lib_path", "ForwardResult"]

@@ -1,0 +1,133 @@
+"""The five benchmark network configurations and their generator settings.
+
+Each configuration names a topology (input layer, LIF hidden layers that may be
+recurrent, one leaky-integrator readout layer), the integration grid (dt, T),
+the batch size, the per-projection delay ranges in steps, the readout loss and
+the input spike generator.  The neuron constants follow the LIF model of Table 1
+(tau_m = 20 ms, tau_s = 5 ms, threshold 1, reset to 0); the paper defers the time
+constants to earlier EventProp work, so these values are the stated config-1
+ones, used for every configuration.
+
+Weights are N(mean, std) per projection.  Config 1 states N(0, 1/sqrt(fan_in)).
+Configs 2-5 state no initialisation, so they take the paper's hyper-parameter
+tables for the task each stands in for (Yin-Yang for config 2, Braille for
+config 3, SHD for configs 4 and 5: recurrent N(0, 0.02), hidden-to-output
+N(0.02, 0.03), feed-forward hidden-to-hidden N(0.02, 0.03), input std 0.01).
+The means of the feed-forward projections into LIF layers are then calibrated
+once (bisection on the oracle forward over the first 8 samples, see
+``oracle/calibrate.py``) to a mean hidden activity of about 14 spikes per neuron
+per sample (the SHD spike-count target of the Results section) or about 1
+(latency-coded config 2); the values live in ``calibration.json``.
+"""
+from __future__ import annotations
+
+import json
+import os
+from dataclasses import dataclass, field
+from typing import Dict, List, Tuple
+
+INPUT, LIF, LI = 0, 1, 2
+LOSS_CE_SUM, LOSS_CE_MAX = 0, 1
+
+
+@dataclass(frozen=True)
+class Config:
+    cid: int
+    name: str
+    B: int
+    T: int
+    dt: float
+    layers: Tuple[Tuple[int, int, int], ...]      # (n, kind, recurrent)
+    delay_range: Tuple[int, ...]                   # one per projection, in steps
+    loss: int
+    generator: str
+    gen_params: Dict = field(default_factory=dict)
+    tau_m: float = 20.0
+    tau_s: float = 5.0
+    theta: float = 1.0
+    target_rate: float = 0.0                       # spikes / hidden neuron / sample for mu calibration
+    w_init: Tuple[Tuple[float, float], ...] = ()   # (mean, std) per projection; std 0 -> 1/sqrt(fan_in)
+    calibrate: Tuple[int, ...] = ()                # projections whose mean is calibrated
+
+    @property
+    def max_delay(self) -> int:
+        return max(self.delay_range)
+
+    @property
+    def S(self) -> int:
+        return self.max_delay + 1
+
+    @property
+    def n_classes(self) -> int:
+        return self.layers[-1][0]
+
+    @property
+    def readout_scale(self) -> float:
+        # time-average readout (a literal sum saturates the softmax at T = 1000)
+        return 1.0 / self.T
+
+
+def projections(layers) -> List[Tuple[int, int]]:
+    """Fixed projection order: for each non-input layer l, the feed-forward
+    projection (l-1 -> l), then the recurrent one (l -> l) if l is recurrent."""
+    out = []
+    for l in range(1, len(layers)):
+        out.append((l - 1, l))
+        if layers[l][2]:
+            out.append((l, l))
+    return out
+
+
+CONFIGS: Dict[int, Config] = {
+    1: Config(1, "seqdet-10-20-2", B=32, T=100, dt=1.0,
+              layers=((10, INPUT, 0), (20, LIF, 0), (2, LI, 0)),
+              delay_range=(10, 10), loss=LOSS_CE_SUM,
+              generator="bernoulli", gen_params={"rate_hz": 20.0},
+              w_init=((0.0, 0.0), (0.0, 0.0))),
+    2: Config(2, "latency-4-200-3", B=64, T=600, dt=0.1,
+              layers=((4, INPUT, 0), (200, LIF, 0), (3, LI, 0)),
+              delay_range=(50, 50), loss=LOSS_CE_MAX,
+              generator="latency", gen_params={"t_max_ms": 30.0}, target_rate=1.0,
+              w_init=((2.0, 0.78), (0.93, 0.1)), calibrate=(0,)),
+    3: Config(3, "tactile-12-128rec-27", B=128, T=300, dt=1.0,
+              layers=((12, INPUT, 0), (128, LIF, 1), (27, LI, 0)),
+              delay_range=(25, 25, 25), loss=LOSS_CE_SUM,
+              generator="bumps", gen_params={"n_bumps": 3, "peak_hz": 50.0}, target_rate=14.0,
+              w_init=((0.03, 0.01), (0.0, 0.02), (0.02, 0.03)), calibrate=(0,)),
+    4: Config(4, "audio-700-256rec-20", B=256, T=1000, dt=1.0,
+              layers=((700, INPUT, 0), (256, LIF, 1), (20, LI, 0)),
+              delay_range=(150, 50, 150), loss=LOSS_CE_SUM,
+              generator="audio", gen_params={"mean_spikes": 8000.0}, target_rate=14.0,
+              w_init=((0.03, 0.01), (0.0, 0.02), (0.02, 0.03)), calibrate=(0,)),
+    5: Config(5, "audio-700-1024rec-1024rec-35", B=256, T=1000, dt=1.0,
+              layers=((700, INPUT, 0), (1024, LIF, 1), (1024, LIF, 1), (35, LI, 0)),
+              delay_range=(150, 150, 150, 150, 150), loss=LOSS_CE_SUM,
+              generator="audio", gen_params={"mean_spikes": 8000.0}, target_rate=14.0,
+              w_init=((0.03, 0.01), (0.0, 0.02), (0.02, 0.03), (0.0, 0.02), (0.02, 0.03)),
+              calibrate=(0, 2)),
+}
+
+_CAL_PATH = os.path.join(os.path.dirname(__file__), "calibration.json")
+
+
+def weight_stds(cfg: Config) -> List[float]:
+    out = []
+    for p, (a, q) in enumerate(projections(cfg.layers)):
+        sd = cfg.w_init[p][1]
+        out.append(sd if sd > 0 else 1.0 / float(cfg.layers[a][0]) ** 0.5)
+    return out
+
+
+def weight_means(cfg: Config) -> List[float]:
+    """Per-projection weight means: the table value, replaced by the calibrated
+    one for the projections listed in ``calibrate``."""
+    mus = [m for m, _ in cfg.w_init]
+    try:
+        with open(_CAL_PATH) as f:
+            cal = json.load(f)
+    except FileNotFoundError:
+        cal = {}
+    entry = cal.get(str(cfg.cid), {})
+    for p, v in entry.get("mu", {}).items():
+        mus[int(p)] = float(v)
+    return mus
