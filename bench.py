@@ -1,0 +1,169 @@
+"""Benchmark: one EventProp training step (forward + loss + backward) of the
+700-256rec-20 audio-sized network (batch 256, T = 1000 steps of 1 ms, delays
+U[0,150] feed-forward / U[0,50] recurrent) on one MI355X, on seeded synthetic
+SHD-shaped input spikes.  Prints one JSON line.
+
+The metric is synaptic events per second for forward + backward, where one
+event is one (presynaptic spike, postsynaptic target) pair of the step, counted
+once per training step, with the spike counts the step actually produced.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+
+# Algorithmic bytes per unit of work (fp32 values, uint8 delay slots; V, I and
+# the adjoints held on chip), split over the three kernels of a step:
+#  forward:     event 13 (w 4, slot 1, ring read-modify-write 8); neuron-step 8
+#               (ring read + clear); LIF spike 8 (record write); input spike 4
+#  backward A:  event 13 (w 4, slot 1, lambda_I - lambda_V at arrival 4, dD 4);
+#               neuron-step 4 (history write); LIF spike 8 (record read);
+#               input spike 4
+#  backward B:  event 8 (lambda_I at arrival 4, dW 4); neuron-step 4
+BYTES = {
+    "forward": {"event": 13, "neuron_step": 8, "lif_spike": 8, "input_spike": 4},
+    "backward_a": {"event": 13, "neuron_step": 4, "lif_spike": 8, "input_spike": 4},
+    "backward_b": {"event": 8, "neuron_step": 4, "lif_spike": 0, "input_spike": 0},
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_bytes(kind, units):
+    c = BYTES[kind]
+    return sum(c[k] * units[k] for k in c)
+
+
+def cpu_baseline(wl, n_samples):
+    """The oracle as it stands (single thread, fp64 backward) on the first
+    n_samples samples of the same workload."""
+    import oracle
+    from workloads.generators import Workload
+    B = min(n_samples, wl.B)
+    off = wl.in_off[:B + 1]
+    sub = Workload(wl.cfg, B, wl.T, off, wl.in_step[:off[-1]], wl.in_neuron[:off[-1]], wl.W, wl.D,
+                   wl.labels[:B])
+    c = wl.cfg
+    net = oracle.OracleNet(c.layers, c.tau_m, c.tau_s, c.theta, c.dt, c.max_delay, sub.T, c.loss,
+                           c.readout_scale)
+    cap = 64 * 256
+    t0 = time.perf_counter()
+    f = oracle.forward(net, sub.in_off, sub.in_step, sub.in_neuron, sub.W, sub.D, cap=cap)
+    lo, g = oracle.loss(f.z, sub.labels)
+    oracle.backward(net, sub.in_off, sub.in_step, sub.in_neuron, sub.W, sub.D, f, g, mode="f64")
+    dt = time.perf_counter() - t0
+    E = 0
+    for (a, q) in [(0, 1), (1, 1), (1, 2)]:
+        spikes = int(off[-1]) if a == 0 else int(f.count[0].sum())
+        E += spikes * c.layers[q][0]
+    return {"value": E / dt, "unit": "events/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {B} of the {wl.B} samples, forward + loss + fp64 backward, "
+                      f"{dt:.2f} s wall on one host core, {E} events"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cpu-samples", type=int, default=256,
+                    help="samples of the batch the oracle baseline runs (0: skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (--gpus {args.gpus} requested): the data-parallel "
+              "split over GPUs (an all-reduce of dW/dD per step) is designed, not built.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2501_07331_amd as snn
+    from workloads import make_workload
+
+    assert torch.cuda.is_available(), "bench needs a GPU"
+    wl = make_workload(4)
+    c = wl.cfg
+    cap = 64 * 256
+    dev = torch.device("cuda")
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        t = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dev, dt)
+        off, st, ne = t(wl.in_off, torch.int32), t(wl.in_step, torch.int32), t(wl.in_neuron, torch.int32)
+        W = [t(w, torch.float32) for w in wl.W]
+        D = [t(d, torch.float32) for d in wl.D]
+        labels = t(wl.labels, torch.int32)
+        recs = [(torch.zeros(wl.B, dtype=torch.int32, device=dev),
+                 torch.zeros(wl.B, cap, dtype=torch.int32, device=dev),
+                 torch.zeros(wl.B, cap, dtype=torch.int32, device=dev))]
+        loss = torch.zeros(wl.B + 1, device=dev)
+        z = torch.zeros(wl.B, c.n_classes, device=dev)
+        dW = [torch.zeros_like(w) for w in W]
+        dD = [torch.zeros_like(w) for w in W]
+        net = snn.Network(c.layers, c.tau_m, c.tau_s, c.theta, c.dt, c.max_delay, wl.B, wl.T, c.loss,
+                          c.readout_scale, cap, flags=snn.SNN_FLAG_TIMING, stream=stream)
+
+        def step():
+            net.forward(off, st, ne, W, D, labels, recs, loss, z)
+            net.backward(dW, dD)
+
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        kt = {"forward": [], "backward_a": [], "backward_b": []}
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            step()
+            s = net.stats()
+            kt["forward"].append(s["forward_kernel_ms"])
+            kt["backward_a"].append(s["backward_a_ms"])
+            kt["backward_b"].append(s["backward_b_ms"])
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+    s = net.stats()
+    E = s["events"]
+    ms = 1e3 * elapsed / args.steps
+    units = {"event": E, "neuron_step": wl.B * wl.T * sum(l[0] for l in c.layers[1:]),
+             "lif_spike": s["lif_spikes"], "input_spike": s["input_spikes"]}
+    avg = {k: float(np.mean(v)) for k, v in kt.items()}
+    dom = max(avg, key=avg.get)
+    ach = kernel_bytes(dom, units) / (avg[dom] * 1e-3) / 1e9
+    log(f"kernel ms: {avg}  step ms {ms:.3f}  events {E}  lif spikes/neuron/sample "
+        f"{s['lif_spikes'] / wl.B / 256:.2f}")
+    out = {
+        "metric": "synaptic events/sec fwd+bwd, 700-256rec-20, B=256",
+        "value": E / (elapsed / args.steps),
+        "unit": "events/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "audio-700-256rec-20 (config 4): 700 inputs, 256 recurrent LIF, "
+                               "20 LI, B=256, T=1000, dt=1ms, delays ff U[0,150] rec U[0,50]",
+                   "events_per_step": E, "input_spikes": s["input_spikes"],
+                   "lif_spikes": s["lif_spikes"],
+                   "kernel_ms": {k: round(v, 4) for k, v in avg.items()}},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": ach, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": ach / HBM_PEAK_GBS, "traffic": None},
+    }
+    if args.cpu_samples > 0:
+        log("timing the oracle on the host ...")
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_samples)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,215 @@
+/*
+ * snn.h -- C ABI of libsnn: batched, time-stepped EventProp training step for
+ * leaky integrate-and-fire networks with learnable synaptic delays, on AMD
+ * Instinct MI355X (gfx950).
+ *
+ * Method: "Efficient Event-based Delay Learning in Spiking Neural Networks"
+ * (Mészáros, Knight, Nowotny, arXiv 2501.07331), Table 1 and the Methods
+ * ("Learning Weights in networks with delay", "Learning Delays").
+ *
+ * Model.  Layer 0 is an input layer of spike sources, layers 1 .. L-2 are LIF
+ * layers (optionally recurrent), layer L-1 is a leaky-integrator (LI) readout,
+ * i.e. a LIF layer with an infinite threshold (Table 1 caption).  Between
+ * events tau_m V' = -V + I and tau_s I' = -I; a LIF neuron spikes when V
+ * reaches theta and is reset to 0; a spike of neuron i at step n makes the
+ * current of post neuron j jump by w_ij at step n + d_ij (Table 1, forward).
+ * The backward pass runs the adjoints lambda_V, lambda_I in reverse time,
+ * applies the lambda_V jump at every saved spike using the postsynaptic
+ * adjoints at the delayed arrival time, and accumulates
+ *   dL/dw_ij = -tau_s sum_spikes lambda_I,j(t + d_ij),
+ *   dL/dd_ij = -w_ij  sum_spikes (lambda_I - lambda_V)_j(t + d_ij)
+ * (Table 1, gradient updates; Methods equations for the weight and delay
+ * gradients and the lambda_V jump).
+ *
+ * Discretisation (the paper gives continuous equations only): a fixed grid of
+ * T steps of dt.  Per step n: exact one-step propagation V- = fma(alpha, V,
+ * gamma*I), I- = beta*I with alpha = e^{-dt/tau_m}, beta = e^{-dt/tau_s},
+ * gamma = tau_s/(tau_s - tau_m) (beta - alpha) (constants computed in fp64 on
+ * the host, rounded to fp32); threshold V- >= theta, reset, record (n, i, I-);
+ * emit every presynaptic spike into a per-(sample, post layer) delay ring at
+ * slot (n + d) mod S, S = max_delay + 1, dropping arrivals at or after T;
+ * then I = I- + ring[n mod S].  Delays are integer multiples of dt: the slot
+ * is rint(D) (round half to even) clamped to [0, max_delay], NaN -> 0.
+ * All forward arithmetic is IEEE fp32 with no contraction, in the fixed order
+ * (emission step, projection, presynaptic index) per ring cell, so spike
+ * records are bit-reproducible.
+ *
+ * Projections.  Fixed order: for l = 1 .. L-1, the feed-forward projection
+ * (l-1 -> l), then the recurrent one (l -> l) if layer l is recurrent.  Weight
+ * and delay tensors of projection p are dense, row-major [n_pre][n_post]
+ * (element (i, j) is the synapse from pre neuron i to post neuron j).  Delays
+ * and delay gradients are in units of steps.
+ *
+ * Memory.  Every pointer argument marked (dev) is device memory owned by the
+ * caller.  Inputs are read-only; outputs are fully overwritten.  The library
+ * owns its scratch (delay rings, adjoint rings, internal spike records,
+ * per-step indices, fp64 gradient accumulators, a status word), allocated
+ * in snn_create and released in snn_destroy.  Work is enqueued on
+ * opts.hip_stream (NULL = the default stream); each snn_forward and
+ * snn_backward ends with one small status read-back, so counts and error
+ * codes are final when the call returns.  A handle is not thread-safe;
+ * distinct handles are independent.
+ */
+#ifndef SNN_H
+#define SNN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    SNN_OK = 0,
+    SNN_EINVAL = -1,     /* bad topology, shape, argument or input spike list */
+    SNN_ENOMEM = -2,     /* device allocation failed */
+    SNN_ESTATE = -3,     /* snn_backward without a successful snn_forward */
+    SNN_EOVERFLOW = -4,  /* a sample produced more spikes than record_capacity */
+    SNN_EDEVICE = -5     /* a HIP runtime error */
+};
+
+enum { SNN_INPUT = 0, SNN_LIF = 1, SNN_LI = 2 };                /* layer kinds */
+enum { SNN_LOSS_CE_SUM = 0, SNN_LOSS_CE_MAX = 1 };               /* readout losses */
+
+#define SNN_MAX_LAYERS 6
+#define SNN_MAX_NEURONS 1024   /* per non-input layer */
+#define SNN_MAX_DELAY 255
+
+typedef struct snn_net snn_net;
+
+/* One layer: n neurons, kind SNN_INPUT / SNN_LIF / SNN_LI, recurrent flag
+ * (LIF layers only). */
+typedef struct {
+    int32_t n, kind, recurrent;
+} snn_layer;
+
+/*
+ * batch:            samples per call (>= 1)
+ * T:                steps per sample (>= 1)
+ * loss:             SNN_LOSS_CE_SUM: z_k = readout_scale * sum_n V_k,n;
+ *                   SNN_LOSS_CE_MAX: z_k = max_n V_k,n (first maximiser);
+ *                   softmax cross-entropy on z, mean over the batch
+ *                   (voltage-based readouts of Fig. 1 and the Results)
+ * readout_scale:    s above (sum readout only)
+ * record_capacity:  spike records kept per sample and LIF layer
+ * flags:            bitwise OR of
+ *                   SNN_FLAG_HBM_RINGS: keep every delay and adjoint ring in
+ *                   device memory even where it would fit in LDS (same
+ *                   results; exercises the HBM ring path);
+ *                   SNN_FLAG_TIMING: time the forward kernel and the two
+ *                   backward kernels with HIP events on hip_stream (reported
+ *                   by snn_get_stats)
+ * hip_stream:       hipStream_t to enqueue on (NULL: default stream)
+ */
+#define SNN_FLAG_HBM_RINGS 1
+#define SNN_FLAG_TIMING 2
+
+typedef struct {
+    int32_t batch, T, loss;
+    float readout_scale;
+    int32_t record_capacity;
+    int32_t flags;
+    void* hip_stream;
+} snn_opts;
+
+/* Input spikes, CSR over samples (dev): offsets [batch+1] with offsets[0] = 0
+ * and offsets[batch] = nnz; step and neuron [nnz]; within a sample sorted by
+ * (step, neuron) without duplicates, 0 <= step < T, 0 <= neuron < n_input.
+ * Checked on the device before any other kernel reads them (SNN_EINVAL). */
+typedef struct {
+    const int32_t* offsets;
+    const int32_t* step;
+    const int32_t* neuron;
+    int32_t nnz;
+} snn_spikes_in;
+
+/* Spike records of one LIF layer (dev): count [batch]; step, neuron
+ * [batch][record_capacity], each sample sorted by (step, neuron).  count is
+ * exact even when it exceeds the capacity (then only the first
+ * record_capacity records are stored and the call returns SNN_EOVERFLOW). */
+typedef struct {
+    int32_t* count;
+    int32_t* step;
+    int32_t* neuron;
+} snn_spikes_out;
+
+/* Per-call statistics of the last forward / backward (host copy). */
+typedef struct {
+    int64_t input_spikes;      /* nnz of the last forward */
+    int64_t lif_spikes;        /* all LIF layers, all samples */
+    int64_t events;            /* sum over projections of presynaptic spikes x n_post */
+    int64_t clamped_delays;    /* delays rounded outside [0, max_delay] or NaN */
+    int64_t degenerate_jumps;  /* spikes with I- <= theta whose jump was skipped */
+    int32_t overflow;          /* 1 if any record count exceeded the capacity */
+    int32_t lds_rings;         /* bit l set: layer l's rings live in LDS */
+    float forward_kernel_ms;   /* with SNN_FLAG_TIMING: last forward kernel */
+    float backward_a_ms;       /* last backward pass A kernel (adjoints, jumps, dD) */
+    float backward_b_ms;       /* last backward pass B kernel (replay, dW) */
+    float reserved;
+} snn_stats;
+
+/*
+ * Build a network handle: validates the topology (layer 0 SNN_INPUT, layers
+ * 1 .. L-2 SNN_LIF, last layer SNN_LI, 2 <= L <= SNN_MAX_LAYERS, non-input
+ * layers of 1 .. SNN_MAX_NEURONS neurons, only LIF layers recurrent),
+ * computes the fp32 constants on the host in fp64, and allocates the device
+ * scratch for opts->batch samples.  dt > 0, tau_m != tau_s, both > 0,
+ * 0 <= max_delay <= SNN_MAX_DELAY.  No device compute.  *out receives the
+ * handle (NULL on error); errors: SNN_EINVAL, SNN_ENOMEM, SNN_EDEVICE.
+ */
+int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m, float tau_s, float theta,
+               float dt, int32_t max_delay, const snn_opts* opts, snn_net** out);
+
+/* Number of projections, and the layers / sizes of projection p. */
+int snn_num_projections(const snn_net* net, int32_t* n);
+int snn_projection_info(const snn_net* net, int32_t p, int32_t* pre_layer, int32_t* post_layer,
+                        int32_t* n_pre, int32_t* n_post);
+
+/*
+ * Forward pass and loss (Table 1 forward dynamics; voltage readout loss).
+ *   in:       input spikes (dev)
+ *   W, D:     host arrays of P device pointers, projection p [n_pre][n_post]
+ *             fp32; D in steps
+ *   labels:   (dev) [batch] class indices in [0, C)
+ *   records:  host array of one snn_spikes_out per LIF layer (dev buffers)
+ *   loss:     (dev) [batch + 1] per-sample CE, then the batch mean
+ *   z:        (dev) [batch][C] readout values, or NULL
+ * The library keeps in, W, D and labels for snn_backward: the caller keeps
+ * them alive and unmodified until the matching snn_backward returns.
+ * Errors: SNN_EINVAL (NULL pointers, bad input spikes, bad labels),
+ * SNN_EOVERFLOW (records truncated; outputs otherwise valid), SNN_EDEVICE.
+ */
+int snn_forward(snn_net* net, const snn_spikes_in* in, const float* const* W, const float* const* D,
+                const int32_t* labels, snn_spikes_out* records, float* loss, float* z);
+
+/*
+ * Backward pass of the last forward (Table 1 backward dynamics, lambda_V
+ * jumps with delayed postsynaptic adjoints, weight and delay gradients).
+ *   dW, dD:   host arrays of P device pointers, [n_pre][n_post] fp32; dD is
+ *             dL per step of delay.  Gradients are summed over the batch of
+ *             the mean loss (so they are batch means).
+ * Adjoint state is fp32; gradient sums and the jump's postsynaptic sum are
+ * accumulated in fp64.  Errors: SNN_ESTATE (no successful forward),
+ * SNN_EOVERFLOW (the forward overflowed its records), SNN_EINVAL, SNN_EDEVICE.
+ */
+int snn_backward(snn_net* net, float* const* dW, float* const* dD);
+
+/* Copy the final V and I of non-input layer `layer` after the last forward
+ * into (dev) [batch][n_layer] buffers. */
+int snn_get_state(const snn_net* net, int32_t layer, float* V, float* I);
+
+/* Statistics of the last forward / backward. */
+int snn_get_stats(const snn_net* net, snn_stats* out);
+
+/* Message for the last error on this handle ("" if none); valid until the
+ * next call on the handle. */
+const char* snn_last_error(const snn_net* net);
+
+/* Release the handle and its device scratch (waits for its stream). */
+void snn_destroy(snn_net* net);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SNN_H */

@@ -1,0 +1,222 @@
+"""ctypes marshalling for libsnn (names follow include/snn.h)."""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import List, Optional, Sequence, Tuple
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+SNN_OK, SNN_EINVAL, SNN_ENOMEM, SNN_ESTATE, SNN_EOVERFLOW, SNN_EDEVICE = 0, -1, -2, -3, -4, -5
+SNN_INPUT, SNN_LIF, SNN_LI = 0, 1, 2
+SNN_LOSS_CE_SUM, SNN_LOSS_CE_MAX = 0, 1
+SNN_FLAG_HBM_RINGS = 1
+SNN_FLAG_TIMING = 2
+_NAMES = {0: "SNN_OK", -1: "SNN_EINVAL", -2: "SNN_ENOMEM", -3: "SNN_ESTATE", -4: "SNN_EOVERFLOW",
+          -5: "SNN_EDEVICE"}
+
+
+class SNNError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+class SNNOverflow(SNNError):
+    pass
+
+
+class snn_layer(C.Structure):
+    _fields_ = [("n", C.c_int32), ("kind", C.c_int32), ("recurrent", C.c_int32)]
+
+
+class snn_opts(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("T", C.c_int32), ("loss", C.c_int32),
+                ("readout_scale", C.c_float), ("record_capacity", C.c_int32),
+                ("flags", C.c_int32), ("hip_stream", C.c_void_p)]
+
+
+class snn_spikes_in(C.Structure):
+    _fields_ = [("offsets", C.c_void_p), ("step", C.c_void_p), ("neuron", C.c_void_p),
+                ("nnz", C.c_int32)]
+
+
+class snn_spikes_out(C.Structure):
+    _fields_ = [("count", C.c_void_p), ("step", C.c_void_p), ("neuron", C.c_void_p)]
+
+
+class snn_stats(C.Structure):
+    _fields_ = [("input_spikes", C.c_int64), ("lif_spikes", C.c_int64), ("events", C.c_int64),
+                ("clamped_delays", C.c_int64), ("degenerate_jumps", C.c_int64),
+                ("overflow", C.c_int32), ("lds_rings", C.c_int32),
+                ("forward_kernel_ms", C.c_float), ("backward_a_ms", C.c_float),
+                ("backward_b_ms", C.c_float), ("reserved", C.c_float)]
+
+
+_lib = None
+
+
+def lib_path() -> str:
+    return os.path.join(HERE, "libsnn.so")
+
+
+def load_library():
+    """Load libsnn.so; raises if it has not been built (there is no fallback)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = lib_path()
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with `python -m paper_2501_07331_amd.build` "
+                          "(there is no CPU fallback)")
+    lib = C.CDLL(path)
+    P = C.c_void_p
+    lib.snn_create.argtypes = [C.POINTER(snn_layer), C.c_int32, C.c_float, C.c_float, C.c_float,
+                               C.c_float, C.c_int32, C.POINTER(snn_opts), C.POINTER(P)]
+    lib.snn_num_projections.argtypes = [P, C.POINTER(C.c_int32)]
+    lib.snn_projection_info.argtypes = [P, C.c_int32] + [C.POINTER(C.c_int32)] * 4
+    lib.snn_forward.argtypes = [P, C.POINTER(snn_spikes_in), C.POINTER(P), C.POINTER(P), P,
+                                C.POINTER(snn_spikes_out), P, P]
+    lib.snn_backward.argtypes = [P, C.POINTER(P), C.POINTER(P)]
+    lib.snn_get_state.argtypes = [P, C.c_int32, P, P]
+    lib.snn_get_stats.argtypes = [P, C.POINTER(snn_stats)]
+    lib.snn_last_error.argtypes = [P]
+    lib.snn_last_error.restype = C.c_char_p
+    lib.snn_destroy.argtypes = [P]
+    lib.snn_destroy.restype = None
+    for f in ("snn_create", "snn_num_projections", "snn_projection_info", "snn_forward",
+              "snn_backward", "snn_get_state", "snn_get_stats"):
+        getattr(lib, f).restype = C.c_int
+    _lib = lib
+    return lib
+
+
+def _ptr(t, dtype=None, what="tensor"):
+    import torch
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{what} must be {dtype}, got {t.dtype}")
+    return C.c_void_p(t.data_ptr())
+
+
+def _ptr_array(ts, dtype, what):
+    arr = (C.c_void_p * len(ts))()
+    for i, t in enumerate(ts):
+        arr[i] = _ptr(t, dtype, f"{what}[{i}]")
+    return arr
+
+
+class Network:
+    """One snn_net handle: a topology, constants and scratch for `batch`
+    samples of `T` steps, bound to the current torch stream at creation."""
+
+    def __init__(self, layers: Sequence[Tuple[int, int, int]], tau_m: float, tau_s: float,
+                 theta: float, dt: float, max_delay: int, batch: int, T: int, loss: int,
+                 readout_scale: float, record_capacity: int, flags: int = 0, stream=None):
+        import torch
+        self._lib = load_library()
+        self.layers = [tuple(int(x) for x in l) for l in layers]
+        self.batch, self.T = int(batch), int(T)
+        self.record_capacity = int(record_capacity)
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        self.stream = stream
+        arr = (snn_layer * len(layers))(*[snn_layer(*l) for l in self.layers])
+        opts = snn_opts(self.batch, self.T, int(loss), float(readout_scale), self.record_capacity,
+                        int(flags), C.c_void_p(stream.cuda_stream))
+        h = C.c_void_p()
+        rc = self._lib.snn_create(arr, len(layers), tau_m, tau_s, theta, dt, int(max_delay),
+                                  C.byref(opts), C.byref(h))
+        if rc != SNN_OK:
+            raise SNNError(rc, "snn_create failed")
+        self._h = h
+        n = C.c_int32()
+        self._check(self._lib.snn_num_projections(h, C.byref(n)))
+        self.projections = []
+        for p in range(n.value):
+            v = [C.c_int32() for _ in range(4)]
+            self._check(self._lib.snn_projection_info(h, p, *[C.byref(x) for x in v]))
+            self.projections.append(tuple(x.value for x in v))   # (pre, post, n_pre, n_post)
+
+    def _check(self, rc):
+        if rc == SNN_OK:
+            return rc
+        msg = self._lib.snn_last_error(self._h).decode() if getattr(self, "_h", None) else ""
+        if rc == SNN_EOVERFLOW:
+            raise SNNOverflow(rc, msg)
+        raise SNNError(rc, msg)
+
+    @property
+    def lif_layers(self) -> List[int]:
+        return [l for l, y in enumerate(self.layers) if y[1] == SNN_LIF]
+
+    def forward(self, offsets, step, neuron, W, D, labels, records, loss, z=None):
+        """records: one (count [B], step [B][cap], neuron [B][cap]) int32 triple
+        per LIF layer; loss: fp32 [B+1]; z: fp32 [B][C] or None."""
+        import torch
+        i32, f32 = torch.int32, torch.float32
+        inp = snn_spikes_in(_ptr(offsets, i32, "offsets"), _ptr(step, i32, "step"),
+                            _ptr(neuron, i32, "neuron"), int(step.numel()))
+        if offsets.numel() != self.batch + 1 or neuron.numel() != step.numel():
+            raise ValueError("offsets must hold batch+1 entries and step/neuron the same count")
+        if len(W) != len(self.projections) or len(D) != len(self.projections):
+            raise ValueError("one W and one D tensor per projection")
+        for p, (_, _, npre, npost) in enumerate(self.projections):
+            for t_, nm in ((W[p], "W"), (D[p], "D")):
+                if t_.numel() != npre * npost:
+                    raise ValueError(f"{nm}[{p}] must hold {npre}x{npost} elements")
+        if labels.numel() != self.batch or loss.numel() != self.batch + 1:
+            raise ValueError("labels [B] and loss [B+1]")
+        C_ = self.layers[-1][0]
+        if z is not None and z.numel() != self.batch * C_:
+            raise ValueError("z must hold B x C elements")
+        if len(records) != len(self.lif_layers):
+            raise ValueError("one record triple per LIF layer")
+        recs = (snn_spikes_out * max(len(records), 1))()
+        for i, (cnt, st, ne) in enumerate(records):
+            if cnt.numel() != self.batch or st.numel() != self.batch * self.record_capacity \
+                    or ne.numel() != self.batch * self.record_capacity:
+                raise ValueError("record buffers must be [B] and [B][record_capacity]")
+            recs[i] = snn_spikes_out(_ptr(cnt, i32, "count"), _ptr(st, i32, "rec step"),
+                                     _ptr(ne, i32, "rec neuron"))
+        self._keep = (offsets, step, neuron, list(W), list(D), labels)
+        rc = self._lib.snn_forward(self._h, C.byref(inp), _ptr_array(W, f32, "W"),
+                                   _ptr_array(D, f32, "D"), _ptr(labels, i32, "labels"), recs,
+                                   _ptr(loss, f32, "loss"), _ptr(z, f32, "z") if z is not None else None)
+        return self._check(rc)
+
+    def backward(self, dW, dD):
+        import torch
+        f32 = torch.float32
+        for p, (_, _, npre, npost) in enumerate(self.projections):
+            if dW[p].numel() != npre * npost or dD[p].numel() != npre * npost:
+                raise ValueError(f"dW/dD[{p}] must hold {npre}x{npost} elements")
+        rc = self._lib.snn_backward(self._h, _ptr_array(dW, f32, "dW"), _ptr_array(dD, f32, "dD"))
+        return self._check(rc)
+
+    def state(self, layer: int, V, I):
+        import torch
+        rc = self._lib.snn_get_state(self._h, int(layer), _ptr(V, torch.float32, "V"),
+                                     _ptr(I, torch.float32, "I"))
+        return self._check(rc)
+
+    def stats(self) -> dict:
+        s = snn_stats()
+        self._check(self._lib.snn_get_stats(self._h, C.byref(s)))
+        return {f: getattr(s, f) for f, _ in snn_stats._fields_}
+
+    def close(self):
+        if getattr(self, "_h", None):
+            self._lib.snn_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,105 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every entry point include/snn.h declares, and rejects bad arguments before
+touching the device."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "snn.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(snn_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2501_07331_amd as snn
+    return snn.load_library()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared()
+    assert {"snn_create", "snn_forward", "snn_backward", "snn_destroy"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_struct_layouts_match_header():
+    from paper_2501_07331_amd import binding as b
+    # int32 x5 + int32 flags + pointer; int32 x3; 3 pointers + int32 (+pad)
+    assert C.sizeof(b.snn_opts) == 32
+    assert C.sizeof(b.snn_layer) == 12
+    assert C.sizeof(b.snn_spikes_in) == 32
+    assert C.sizeof(b.snn_spikes_out) == 24
+    assert C.sizeof(b.snn_stats) == 64
+
+
+def _create(lib, layers, tau_m=20.0, tau_s=5.0, theta=1.0, dt=1.0, max_delay=10, **opt):
+    from paper_2501_07331_amd import binding as b
+    arr = (b.snn_layer * len(layers))(*[b.snn_layer(*l) for l in layers])
+    o = dict(batch=2, T=10, loss=0, readout_scale=0.1, record_capacity=8, flags=0, hip_stream=None)
+    o.update(opt)
+    opts = b.snn_opts(**o)
+    h = C.c_void_p(123)
+    rc = lib.snn_create(arr, len(layers), tau_m, tau_s, theta, dt, max_delay, C.byref(opts),
+                        C.byref(h))
+    return rc, h
+
+
+GOOD = [(3, 0, 0), (4, 1, 1), (2, 2, 0)]
+
+
+@pytest.mark.parametrize("layers,kw", [
+    ([(3, 0, 0)], {}),                                   # one layer
+    ([(3, 1, 0), (2, 2, 0)], {}),                        # first layer not input
+    ([(3, 0, 0), (4, 1, 0)], {}),                        # last layer not LI
+    ([(3, 0, 0), (4, 2, 0), (2, 2, 0)], {}),             # hidden layer not LIF
+    ([(3, 0, 0), (4, 1, 0), (2, 2, 1)], {}),             # recurrent LI
+    ([(3, 0, 0), (2000, 1, 0), (2, 2, 0)], {}),          # too wide
+    ([(3, 0, 0), (0, 1, 0), (2, 2, 0)], {}),             # empty layer
+    (GOOD, {"tau_m": 5.0}),                              # tau_m == tau_s
+    (GOOD, {"dt": 0.0}),
+    (GOOD, {"max_delay": 256}),
+    (GOOD, {"max_delay": -1}),
+    (GOOD, {"batch": 0}),
+    (GOOD, {"T": 0}),
+    (GOOD, {"loss": 7}),
+    (GOOD, {"flags": 4}),
+    (GOOD, {"record_capacity": -1}),
+])
+def test_create_rejects_bad_arguments(lib, layers, kw):
+    rc, h = _create(lib, layers, **kw)
+    assert rc == -1 and not h.value
+
+
+def test_null_handles(lib):
+    n = C.c_int32()
+    assert lib.snn_num_projections(None, C.byref(n)) == -1
+    assert lib.snn_forward(None, None, None, None, None, None, None, None) == -1
+    assert lib.snn_backward(None, None, None) == -1
+    assert lib.snn_get_stats(None, None) == -1
+    assert lib.snn_last_error(None) == b"NULL handle"
+    lib.snn_destroy(None)
+
+
+def test_product_path_has_no_fallback(tmp_path, monkeypatch):
+    """Without the built library the binding raises instead of computing."""
+    from paper_2501_07331_amd import binding as b
+    monkeypatch.setattr(b, "_lib", None)
+    monkeypatch.setattr(b, "lib_path", lambda: str(tmp_path / "missing.so"))
+    with pytest.raises(ImportError):
+        b.load_library()
+
+
+def test_package_does_not_import_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2501_07331_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                txt = open(os.path.join(dirpath, f)).read()
+                assert "oracle" not in txt.lower(), f
