@@ -20,28 +20,21 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 
-# Algorithmic bytes per unit of work (fp32 values, uint8 delay slots; V, I and
-# the adjoints held on chip), split over the three kernels of a step:
-#  forward:     event 13 (w 4, slot 1, ring read-modify-write 8); neuron-step 8
-#               (ring read + clear); LIF spike 8 (record write); input spike 4
-#  backward A:  event 13 (w 4, slot 1, lambda_I - lambda_V at arrival 4, dD 4);
-#               neuron-step 4 (history write); LIF spike 8 (record read);
-#               input spike 4
-#  backward B:  event 8 (lambda_I at arrival 4, dW 4); neuron-step 4
-BYTES = {
-    "forward": {"event": 13, "neuron_step": 8, "lif_spike": 8, "input_spike": 4},
-    "backward_a": {"event": 13, "neuron_step": 4, "lif_spike": 8, "input_spike": 4},
-    "backward_b": {"event": 8, "neuron_step": 4, "lif_spike": 0, "input_spike": 0},
-}
+# Algorithmic bytes per unit of work of the step (fp32 values, uint8 delay
+# slots, V / I / adjoints held on chip):
+#   synaptic event  forward 13 (w 4, slot 1, delay-buffer read-modify-write 8),
+#                   backward 21 (w 4, slot 1, delayed adjoints 8, dW 4, dD 4)
+#   neuron-step     forward 8 (delay-buffer read + clear), backward 8 (history)
+#   LIF spike       16 (record write + read);  input spike 8 (read twice)
+BYTES_STEP = {"event": 34, "neuron_step": 16, "lif_spike": 16, "input_spike": 8}
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_bytes(kind, units):
-    c = BYTES[kind]
-    return sum(c[k] * units[k] for k in c)
+def step_bytes(units):
+    return sum(BYTES_STEP[k] * units[k] for k in BYTES_STEP)
 
 
 def cpu_baseline(wl, n_samples):
@@ -118,14 +111,17 @@ def main():
         for _ in range(args.warmup):
             step()
         torch.cuda.synchronize()
-        kt = {"forward": [], "backward_a": [], "backward_b": []}
+        kt = {}
         t0 = time.perf_counter()
         for _ in range(args.steps):
-            step()
-            s = net.stats()
-            kt["forward"].append(s["forward_kernel_ms"])
-            kt["backward_a"].append(s["backward_a_ms"])
-            kt["backward_b"].append(s["backward_b_ms"])
+            net.forward(off, st, ne, W, D, labels, recs, loss, z)
+            fwd = net.stats()["kernel_ms"]
+            net.backward(dW, dD)
+            bwd = net.stats()["kernel_ms"]
+            for k in ("input_scan", "forward_core", "readout_forward"):
+                kt.setdefault(k, []).append(fwd[k])
+            for k in ("readout_adjoint", "backward_core", "group", "gradients"):
+                kt.setdefault(k, []).append(bwd[k])
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t0
     s = net.stats()
@@ -135,7 +131,8 @@ def main():
              "lif_spike": s["lif_spikes"], "input_spike": s["input_spikes"]}
     avg = {k: float(np.mean(v)) for k, v in kt.items()}
     dom = max(avg, key=avg.get)
-    ach = kernel_bytes(dom, units) / (avg[dom] * 1e-3) / 1e9
+    # the whole step's algorithmic bytes over the whole step's time
+    ach = step_bytes(units) / (elapsed / args.steps) / 1e9
     log(f"kernel ms: {avg}  step ms {ms:.3f}  events {E}  lif spikes/neuron/sample "
         f"{s['lif_spikes'] / wl.B / 256:.2f}")
     out = {

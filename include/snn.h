@@ -96,9 +96,8 @@ typedef struct {
  *                   SNN_FLAG_HBM_RINGS: keep every delay and adjoint ring in
  *                   device memory even where it would fit in LDS (same
  *                   results; exercises the HBM ring path);
- *                   SNN_FLAG_TIMING: time the forward kernel and the two
- *                   backward kernels with HIP events on hip_stream (reported
- *                   by snn_get_stats)
+ *                   SNN_FLAG_TIMING: time the main kernels with HIP events
+ *                   on hip_stream (reported by snn_get_stats)
  * hip_stream:       hipStream_t to enqueue on (NULL: default stream)
  */
 #define SNN_FLAG_HBM_RINGS 1
@@ -141,11 +140,11 @@ typedef struct {
     int64_t clamped_delays;    /* delays rounded outside [0, max_delay] or NaN */
     int64_t degenerate_jumps;  /* spikes with I- <= theta whose jump was skipped */
     int32_t overflow;          /* 1 if any record count exceeded the capacity */
-    int32_t lds_rings;         /* bit l set: layer l's rings live in LDS */
-    float forward_kernel_ms;   /* with SNN_FLAG_TIMING: last forward kernel */
-    float backward_a_ms;       /* last backward pass A kernel (adjoints, jumps, dD) */
-    float backward_b_ms;       /* last backward pass B kernel (replay, dW) */
-    float reserved;
+    int32_t lds_rings;         /* bit p set: projection p's forward delay ring lives in LDS */
+    /* with SNN_FLAG_TIMING, milliseconds of the last call's kernels, in order:
+     * input_scan, forward_core, readout_forward (forward); readout_adjoint,
+     * backward_core, group, gradients (backward) */
+    float kernel_ms[8];
 } snn_stats;
 
 /*
@@ -177,7 +176,9 @@ int snn_projection_info(const snn_net* net, int32_t p, int32_t* pre_layer, int32
  * The library keeps in, W, D and labels for snn_backward: the caller keeps
  * them alive and unmodified until the matching snn_backward returns.
  * Errors: SNN_EINVAL (NULL pointers, bad input spikes, bad labels),
- * SNN_EOVERFLOW (records truncated; outputs otherwise valid), SNN_EDEVICE.
+ * SNN_EOVERFLOW (records truncated: counts, kept records and the final
+ * state stay valid; loss and z are then computed from the truncated records
+ * of the layer feeding the readout and carry no meaning), SNN_EDEVICE.
  */
 int snn_forward(snn_net* net, const snn_spikes_in* in, const float* const* W, const float* const* D,
                 const int32_t* labels, snn_spikes_out* records, float* loss, float* z);

@@ -8,8 +8,8 @@
  *
  * What it computes (per sample; samples are independent):
  *
- *   Forward, n = 0 .. T-1, state V = I = 0 at t = 0, ring R_q[S][N_q] = 0 per
- *   post layer q, S = max_delay + 1:
+ *   Forward, n = 0 .. T-1, state V = I = 0 at t = 0, one delay ring
+ *   R_p[S][N_post] = 0 per projection p, S = max_delay + 1:
  *     1. every non-input neuron: V- = fma(alpha, V, gamma*I), I- = beta*I
  *        (n = 0: V- = I- = 0).  alpha = e^{-dt/tau_m}, beta = e^{-dt/tau_s},
  *        gamma = tau_s/(tau_s - tau_m) (beta - alpha): the exact solution of
@@ -19,33 +19,39 @@
  *        (Table 1 transition condition and jump).  LI neurons: V = V-.
  *     3. emit: projections in order, presynaptic spikes at n in ascending
  *        index, posts ascending: m = n + slot_ij; if m <= T-1,
- *        R[m mod S][j] += w_ij (the delayed current jump of Table 1).
- *     4. arrive: I = I- + R[n mod S][j]; R[n mod S][j] = 0.
+ *        R_p[m mod S][j] += w_ij (the delayed current jump of Table 1).
+ *     4. arrive: I = I- + R_p[n mod S][j] for the projections p into the
+ *        layer, in projection order; those cells are cleared.
  *     5. readout of the LI layer: sum  acc_k += V_k;  max  first argmax.
  *   z_k = s * acc_k (sum) or max_n V_k (max); CE loss; g = dL/dz.
  *
- *   Backward, n = T-1 .. 0, lambda = 0, hist_q[S][N_q] of (lambda_V, lambda_I):
+ *   Backward, n = T-1 .. 0, lambda = 0, trajectory H[n][j] of (lambda_V,
+ *   lambda_I):
  *     1. n <= T-2: lambda_I <- beta lambda_I + c lambda_V, lambda_V <- alpha
  *        lambda_V (exact one-step solution of the adjoint ODEs of Table 1,
  *        c = tau_m/(tau_m - tau_s) (alpha - beta)).
- *     2. hist[n mod S][j] = (lambda_V, lambda_I): the "+" values at n.
+ *     2. H[n][j] = (lambda_V, lambda_I): the "+" values at n.
  *     3. LI loss source: sum  lambda_V -= s g_k / tau_m every step;
  *        max  lambda_V -= g_k / tau_m at the first argmax step.
- *     4. every presynaptic spike at n, post j with m = n + slot <= T-1,
- *        (v, u) = hist[m mod S][j]:
- *          SU_ij += u,  SD_ij += w_ij (u - v),  and for LIF pre neurons
- *          A_i += w_ij (v - u).
- *        dL/dw = -tau_s SU and dL/dd = -dt SD per step of delay: the weight
- *        and delay gradients of Table 1 / the Methods, with the post adjoints
- *        taken at the delayed arrival time.
- *     5. every LIF spike (n, i, I-): tau_m V-dot^- = I- - theta at a crossing,
- *        so lambda_V <- lambda_V + (theta lambda_V + A_i) / (I- - theta)
+ *     4. every LIF spike (n, i, I-): with (v, u) = H[m][j] at the arrival
+ *        m = n + slot_ij <= T-1 of each post j, A_i = sum_j w_ij (v - u);
+ *        tau_m V-dot^- = I- - theta at a crossing, so
+ *        lambda_V <- lambda_V + (theta lambda_V + A_i) / (I- - theta)
  *        (the lambda_V jump of Table 1 with the delayed postsynaptic sum);
  *        skipped and counted as degenerate if I- - theta <= 0.
+ *   Then the gradient sums over every presynaptic spike (n, i) (inputs and
+ *   LIF records), in spike order, and post j with m = n + slot <= T-1:
+ *     SU_ij += u,  SD_ij += w_ij (u - v),   (v, u) = H[m][j];
+ *   dL/dw = -tau_s SU and dL/dd = -dt SD per step of delay: the weight and
+ *   delay gradients of Table 1 / the Methods, with the post adjoints taken at
+ *   the delayed arrival time.
  *
  * mode 0 runs the backward in fp64 with fp64 constants (the definition).
  * mode 1 rounds every backward operation to fp32 exactly as the HIP kernels
- * do (fp32 state, fp32 products, fp64 sums), the kernel-precision model.
+ * do, the kernel-precision model: fp32 state and products, each sample's
+ * SU/SD terms summed in fp32 in spike order, the per-sample sums then added
+ * over the batch in fp64 in sample order, and the jump's postsynaptic sum A
+ * in fp64.
  * The forward is fp32 with no contraction in both modes: spike decisions are
  * taken in the kernel's precision.
  */
@@ -193,7 +199,13 @@ int oracle_forward(int L, const int* n, const int* kind, const int* rec,
     unsigned char* slot = (unsigned char*)malloc((size_t)t.n_params);
     float* V = (float*)malloc(sizeof(float) * t.n_state);
     float* I = (float*)malloc(sizeof(float) * t.n_state);
-    float* ring = (float*)malloc(sizeof(float) * (size_t)S * t.n_state);
+    /* one ring per projection: ring_off[p] columns into a row of ring_w */
+    int ring_off[OR_MAXP + 1], ring_w = 0;
+    for (int p = 0; p < t.P; ++p) {
+        ring_off[p] = ring_w;
+        ring_w += t.n[t.post[p]];
+    }
+    float* ring = (float*)malloc(sizeof(float) * (size_t)S * (ring_w > 0 ? ring_w : 1));
     int* spk = (int*)malloc(sizeof(int) * t.n_state);      /* spikes of this step, per layer */
     int spk_n[OR_MAXL];
     float* acc = (float*)malloc(sizeof(float) * C);
@@ -208,7 +220,7 @@ int oracle_forward(int L, const int* n, const int* kind, const int* rec,
     for (int b = 0; b < B; ++b) {
         memset(V, 0, sizeof(float) * t.n_state);
         memset(I, 0, sizeof(float) * t.n_state);
-        memset(ring, 0, sizeof(float) * (size_t)S * t.n_state);
+        memset(ring, 0, sizeof(float) * (size_t)S * ring_w);
         for (int l = 0; l < L; ++l)
             if (t.lif_idx[l] >= 0) rec_count[(size_t)t.lif_idx[l] * B + b] = 0;
         int cur = in_off[b];
@@ -260,15 +272,19 @@ int oracle_forward(int L, const int* n, const int* kind, const int* rec,
                     const unsigned char* srow = slot + t.w_off[p] + (long)i * nq;
                     for (int j = 0; j < nq; ++j) {
                         const int m = n_ + srow[j];
-                        if (m <= T - 1) ring[(size_t)(m % S) * t.n_state + t.st_off[q] + j] += wrow[j];
+                        if (m <= T - 1) ring[(size_t)(m % S) * ring_w + ring_off[p] + j] += wrow[j];
                     }
                 }
             }
-            /* 4. arrivals */
-            float* cell = ring + (size_t)(n_ % S) * t.n_state;
-            for (int s = 0; s < t.n_state; ++s) {
-                I[s] = I[s] + cell[s];
-                cell[s] = 0.0f;
+            /* 4. arrivals, projection by projection */
+            float* row = ring + (size_t)(n_ % S) * ring_w;
+            for (int p = 0; p < t.P; ++p) {
+                const int q = t.post[p];
+                for (int j = 0; j < t.n[q]; ++j) {
+                    float* cell = row + ring_off[p] + j;
+                    I[t.st_off[q] + j] = I[t.st_off[q] + j] + *cell;
+                    *cell = 0.0f;
+                }
             }
             /* 5. readout */
             for (int k = 0; k < C; ++k) {
@@ -357,7 +373,6 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
         beta = exp(-(double)dt / (double)tau_s);
         cc = (double)tau_m / ((double)tau_m - (double)tau_s) * (alpha - beta);
     }
-    const int S = max_delay + 1;
     const int C = t.n[L - 1];
     const int out_l = L - 1;
 
@@ -367,20 +382,27 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
     double* SD = (double*)calloc((size_t)t.n_params, sizeof(double));
     double* lv = (double*)malloc(sizeof(double) * t.n_state);
     double* lI = (double*)malloc(sizeof(double) * t.n_state);
-    double* hist = (double*)malloc(sizeof(double) * 2 * (size_t)S * t.n_state);
+    double* H = (double*)malloc(sizeof(double) * 2 * (size_t)T * t.n_state);
     double* A = (double*)malloc(sizeof(double) * t.n_state);
     double* src = (double*)malloc(sizeof(double) * C);
-    if (!slot || !SU || !SD || !lv || !lI || !hist || !A || !src) {
-        free(slot); free(SU); free(SD); free(lv); free(lI); free(hist); free(A); free(src);
+    /* per-sample partial sums (fp32 model) */
+    double* PU = (double*)calloc((size_t)t.n_params, sizeof(double));
+    double* PD = (double*)calloc((size_t)t.n_params, sizeof(double));
+    if (!slot || !SU || !SD || !lv || !lI || !H || !A || !src || !PU || !PD) {
+        free(slot); free(SU); free(SD); free(lv); free(lI); free(H); free(A); free(src);
+        free(PU); free(PD);
         return OR_ENOMEM;
     }
+    (void)max_delay;
     for (long k = 0; k < t.n_params; ++k) slot[k] = (unsigned char)delay_slot(D[k], max_delay, &clamped);
+    /* f64: terms go straight into the batch sums; f32: into per-sample fp32 sums */
+    double* TU = f32 ? PU : SU;
+    double* TD = f32 ? PD : SD;
 
     int rec_hi[OR_MAXL];
     for (int b = 0; b < B; ++b) {
         memset(lv, 0, sizeof(double) * t.n_state);
         memset(lI, 0, sizeof(double) * t.n_state);
-        memset(hist, 0, sizeof(double) * 2 * (size_t)S * t.n_state);
         for (int k = 0; k < C; ++k) {
             const double gk = (double)g[(size_t)b * C + k];
             const double sk = (loss == OR_LOSS_CE_SUM) ? (double)readout_scale * gk / (double)tau_m
@@ -389,7 +411,6 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
         }
         for (int l = 0; l < L; ++l)
             if (t.lif_idx[l] >= 0) rec_hi[l] = rec_count[(size_t)t.lif_idx[l] * B + b];
-        int in_hi = in_off[b + 1];
         for (int n_ = T - 1; n_ >= 0; --n_) {
             /* 1. adjoint free dynamics over one step */
             if (n_ <= T - 2) {
@@ -399,8 +420,8 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
                     lv[s] = rnd(f32, alpha * v);
                 }
             }
-            /* 2. delayed-access history of the "+" values */
-            double* h = hist + 2 * (size_t)(n_ % S) * t.n_state;
+            /* 2. the "+" values at this step */
+            double* h = H + 2 * (size_t)n_ * t.n_state;
             for (int s = 0; s < t.n_state; ++s) {
                 h[2 * s] = lv[s];
                 h[2 * s + 1] = lI[s];
@@ -411,9 +432,7 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
                 if (loss == OR_LOSS_CE_SUM || nstar[(size_t)b * C + k] == n_)
                     lv[s] = rnd(f32, lv[s] - src[k]);
             }
-            /* spikes at this step: input events and LIF records */
-            int in_lo = in_hi;
-            while (in_lo > in_off[b] && in_step[in_lo - 1] == n_) --in_lo;
+            /* 4. LIF spikes at this step: delayed postsynaptic sums, jumps */
             int rec_lo[OR_MAXL];
             for (int l = 1; l < L; ++l) {
                 if (t.lif_idx[l] < 0) continue;
@@ -423,32 +442,25 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
                 rec_lo[l] = lo;
                 for (int k = lo; k < rec_hi[l]; ++k) A[t.st_off[l] + rec_neuron[base + k]] = 0.0;
             }
-            /* 4. gathers at the delayed arrival times */
             for (int p = 0; p < t.P; ++p) {
                 const int a = t.pre[p], q = t.post[p];
+                if (a == 0) continue;
                 const int nq = t.n[q];
-                const size_t base = (a == 0) ? 0 : (size_t)t.lif_idx[a] * B * cap + (size_t)b * cap;
-                const int lo = (a == 0) ? in_lo : rec_lo[a];
-                const int hi = (a == 0) ? in_hi : rec_hi[a];
-                for (int k = lo; k < hi; ++k) {
-                    const int i = (a == 0) ? in_neuron[k] : rec_neuron[base + k];
+                const size_t base = (size_t)t.lif_idx[a] * B * cap + (size_t)b * cap;
+                for (int k = rec_lo[a]; k < rec_hi[a]; ++k) {
+                    const int i = rec_neuron[base + k];
                     const long row = t.w_off[p] + (long)i * nq;
                     double Ai = 0.0;
                     for (int j = 0; j < nq; ++j) {
                         const int m = n_ + slot[row + j];
                         if (m > T - 1) continue;
-                        const double* hv = hist + 2 * ((size_t)(m % S) * t.n_state + t.st_off[q] + j);
-                        const double v = hv[0], u = hv[1];
-                        const double d = rnd(f32, u - v);
-                        const double wd = rnd(f32, (double)W[row + j] * d);
-                        SU[row + j] += u;
-                        SD[row + j] += wd;
-                        Ai -= wd;
+                        const double* hv = H + 2 * ((size_t)m * t.n_state + t.st_off[q] + j);
+                        const double d = rnd(f32, hv[1] - hv[0]);
+                        Ai -= rnd(f32, (double)W[row + j] * d);
                     }
-                    if (a != 0) A[t.st_off[a] + i] += Ai;
+                    A[t.st_off[a] + i] += Ai;
                 }
             }
-            /* 5. lambda_V jumps at the spikes of this step */
             for (int l = 1; l < L; ++l) {
                 if (t.lif_idx[l] < 0) continue;
                 const size_t base = (size_t)t.lif_idx[l] * B * cap + (size_t)b * cap;
@@ -464,7 +476,36 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
                 }
                 rec_hi[l] = rec_lo[l];
             }
-            in_hi = in_lo;
+        }
+        /* gradient sums over this sample's spikes, in spike order */
+        for (int p = 0; p < t.P; ++p) {
+            const int a = t.pre[p], q = t.post[p];
+            const int nq = t.n[q];
+            const int cnt = (a == 0) ? in_off[b + 1] - in_off[b] : rec_count[(size_t)t.lif_idx[a] * B + b];
+            const size_t base = (a == 0) ? (size_t)in_off[b] : (size_t)t.lif_idx[a] * B * cap + (size_t)b * cap;
+            for (int k = 0; k < cnt; ++k) {
+                const int i = (a == 0) ? in_neuron[base + k] : rec_neuron[base + k];
+                const int n0 = (a == 0) ? in_step[base + k] : rec_step[base + k];
+                const long row = t.w_off[p] + (long)i * nq;
+                for (int j = 0; j < nq; ++j) {
+                    const int m = n0 + slot[row + j];
+                    if (m > T - 1) continue;
+                    const double* hv = H + 2 * ((size_t)m * t.n_state + t.st_off[q] + j);
+                    const double v = hv[0], u = hv[1];
+                    const double d = rnd(f32, u - v);
+                    const double wd = rnd(f32, (double)W[row + j] * d);
+                    TU[row + j] = rnd(f32, TU[row + j] + u);
+                    TD[row + j] = rnd(f32, TD[row + j] + wd);
+                }
+            }
+        }
+        if (f32) {
+            for (long k = 0; k < t.n_params; ++k) {
+                SU[k] += PU[k];
+                SD[k] += PD[k];
+                PU[k] = 0.0;
+                PD[k] = 0.0;
+            }
         }
     }
     for (long k = 0; k < t.n_params; ++k) {
@@ -472,6 +513,7 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
         dD[k] = -(double)dt * SD[k];
     }
     if (stats) stats[0] = degenerate;
-    free(slot); free(SU); free(SD); free(lv); free(lI); free(hist); free(A); free(src);
+    free(slot); free(SU); free(SD); free(lv); free(lI); free(H); free(A); free(src);
+    free(PU); free(PD);
     return OR_OK;
 }

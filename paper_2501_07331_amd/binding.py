@@ -49,8 +49,12 @@ class snn_stats(C.Structure):
     _fields_ = [("input_spikes", C.c_int64), ("lif_spikes", C.c_int64), ("events", C.c_int64),
                 ("clamped_delays", C.c_int64), ("degenerate_jumps", C.c_int64),
                 ("overflow", C.c_int32), ("lds_rings", C.c_int32),
-                ("forward_kernel_ms", C.c_float), ("backward_a_ms", C.c_float),
-                ("backward_b_ms", C.c_float), ("reserved", C.c_float)]
+                ("kernel_ms", C.c_float * 8)]
+
+
+# order of snn_stats.kernel_ms
+KERNELS = ("input_scan", "forward_core", "readout_forward", "readout_adjoint", "backward_core",
+           "group", "gradients")
 
 
 _lib = None
@@ -208,7 +212,9 @@ class Network:
     def stats(self) -> dict:
         s = snn_stats()
         self._check(self._lib.snn_get_stats(self._h, C.byref(s)))
-        return {f: getattr(s, f) for f, _ in snn_stats._fields_}
+        out = {f: getattr(s, f) for f, _ in snn_stats._fields_ if f != "kernel_ms"}
+        out["kernel_ms"] = {k: float(s.kernel_ms[i]) for i, k in enumerate(KERNELS)}
+        return out
 
     def close(self):
         if getattr(self, "_h", None):

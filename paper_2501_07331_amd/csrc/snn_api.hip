@@ -12,7 +12,11 @@
 
 namespace {
 
-constexpr size_t kLdsPerGroup = 160 * 1024;   // gfx950: 160 KiB of LDS per workgroup
+constexpr size_t kLds = 160 * 1024;   // gfx950: 160 KiB of LDS per workgroup
+constexpr int kKB = 8;                // spikes per batch in the kernels (fp64 scratch)
+enum { K_SCAN, K_CORE, K_READ, K_RADJ, K_BCORE, K_GROUP, K_GRAD, K_N };
+
+size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
 
 }  // namespace
 
@@ -20,37 +24,55 @@ struct snn_net {
     Topo t;
     float tau_m, tau_s, theta, dt;
     int max_delay;
-    int threads;
-    size_t lds;                 // dynamic LDS bytes of the persistent kernels
-    int extra_off;              // byte offset of the masks / fp64 jump sums
+    int core_threads;           // LIF-core workgroup size
+    int read_threads;           // readout workgroup size
+    size_t lds_core_f, lds_core_b, lds_scan, lds_read, lds_grad;
+    int mask_off, acc_off, scan_nb, table_lds, red_off;
     hipStream_t stream;
     long long n_params;
     long long cnt[SNN_MAXP];
     int n_state;
     int st_off[SNN_MAX_LAYERS];
+    int grad_blocks;
+    int blk[SNN_MAXP + 1];
     // device scratch
     uint8_t* slot;
-    float* ring[SNN_MAX_LAYERS];
     int* in_idx;
+    float* A_in;
+    float* fring[SNN_MAXP];
+    float* bring[SNN_MAX_LAYERS];
     int* rec_n;
+    int* rec_s;
     float* rec_I;
-    float* rec_D;
     int* rec_idx;
+    int* rec_cnt;
+    int* rec_goff;
+    int* rec_gstep;
     float* z;
     int* nstar;
     float* src;
     float* Vf;
     float* If;
-    double* SU;
-    double* SD;
+    float* table;
+    float* tu_lif;
+    float* td_lif;
+    float* tu_out;
+    float* td_out;
+    double* A2;
+    int* in_goff;
+    int* in_gstep;
+    long long in_gstep_cap;
     DevStatus* st;
     DevStatus* st_host;         // pinned
     // the last forward's inputs, kept for the backward
     const float* W[SNN_MAXP];
+    const int* in_off;
+    const int* in_step;
     const int* in_neuron;
+    int in_nnz;
     int fwd_ok, fwd_overflow;
     int timing;
-    hipEvent_t ev[6];           // around the forward, backward A, backward B kernels
+    hipEvent_t ev[2 * K_N];
     snn_stats stats;
     char err[256];
 };
@@ -73,14 +95,18 @@ static int fail(snn_net* net, int code, const char* fmt, ...) {
     } while (0)
 
 static void free_all(snn_net* n) {
-    void* bufs[] = {n->slot, n->in_idx, n->rec_n, n->rec_I, n->rec_D, n->rec_idx, n->z, n->nstar,
-                    n->src, n->Vf, n->If, n->SU, n->SD, n->st};
+    void* bufs[] = {n->slot,    n->in_idx,  n->A_in,     n->rec_n,     n->rec_s,  n->rec_I,
+                    n->rec_idx, n->rec_cnt, n->rec_goff, n->rec_gstep, n->z,      n->nstar,
+                    n->src,     n->Vf,      n->If,       n->table,     n->tu_lif, n->td_lif,
+                    n->tu_out,  n->td_out,  n->A2,       n->in_goff,   n->in_gstep, n->st};
     for (void* p : bufs)
         if (p) (void)hipFree(p);
+    for (int p = 0; p < SNN_MAXP; ++p)
+        if (n->fring[p]) (void)hipFree(n->fring[p]);
     for (int l = 0; l < SNN_MAX_LAYERS; ++l)
-        if (n->ring[l]) (void)hipFree(n->ring[l]);
+        if (n->bring[l]) (void)hipFree(n->bring[l]);
     if (n->st_host) (void)hipHostFree(n->st_host);
-    for (int i = 0; i < 6; ++i)
+    for (int i = 0; i < 2 * K_N; ++i)
         if (n->ev[i]) (void)hipEventDestroy(n->ev[i]);
 }
 
@@ -107,12 +133,14 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     for (int l = 0; l < n_layers; ++l) {
         const snn_layer& y = layers[l];
         if (y.n < 1) return SNN_EINVAL;
-        if (l == 0 && y.kind != SNN_INPUT) return SNN_EINVAL;
+        if (l == 0 && (y.kind != SNN_INPUT || y.n > SNN_MAX_INPUT)) return SNN_EINVAL;
         if (l > 0 && l < n_layers - 1 && y.kind != SNN_LIF) return SNN_EINVAL;
         if (l == n_layers - 1 && y.kind != SNN_LI) return SNN_EINVAL;
         if (y.recurrent && y.kind != SNN_LIF) return SNN_EINVAL;
         if (l > 0 && y.n > SNN_MAX_NEURONS) return SNN_EINVAL;
     }
+    // the gradient kernel stages two fp32 trajectories of T steps in LDS
+    if ((size_t)opts->T * 2 * sizeof(float) > kLds) return SNN_EINVAL;
     if ((long long)opts->batch * (opts->T + 1) > (1LL << 31)) return SNN_EINVAL;
 
     snn_net* net = (snn_net*)calloc(1, sizeof(snn_net));
@@ -142,18 +170,19 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     net->dt = dt;
     net->max_delay = max_delay;
     net->stream = (hipStream_t)opts->hip_stream;
+    const bool hbm = (opts->flags & SNN_FLAG_HBM_RINGS) != 0;
 
-    int maxn = 0, so = 0;
+    int so = 0;
     for (int l = 0; l < n_layers; ++l) {
         t.n[l] = layers[l].n;
         t.kind[l] = layers[l].kind;
         t.lif[l] = -1;
         t.lif_off[l] = 0;
-        t.ring_lds[l] = -1;
+        t.bring[l] = -1;
         net->st_off[l] = so;
         if (l > 0) {
             so += layers[l].n;
-            maxn = std::max(maxn, layers[l].n);
+            t.maxn = std::max(t.maxn, layers[l].n);
         }
         if (layers[l].kind == SNN_LIF) {
             t.lif[l] = t.n_lif++;
@@ -162,6 +191,7 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         }
     }
     net->n_state = so;
+    t.out_l = n_layers - 1;
     long long off = 0;
     for (int l = 1; l < n_layers; ++l) {
         for (int r = 0; r < 1 + (layers[l].recurrent ? 1 : 0); ++r) {
@@ -169,61 +199,122 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
             t.pre[p] = r ? l : l - 1;
             t.post[p] = l;
             t.woff[p] = off;
+            t.fring[p] = -1;
             net->cnt[p] = (long long)t.n[t.pre[p]] * t.n[l];
             off += net->cnt[p];
         }
     }
     net->n_params = off;
-    net->threads = ((maxn + 63) / 64) * 64;
-    const int nwaves = net->threads / 64;
+    t.out_p = t.P - 1;
+    const int C = t.n[t.out_l];
 
-    // LDS plan: ballot masks (forward) or fp64 jump sums (backward A) after the
-    // rings; LIF rings first (they carry most events), then the readout ring.
-    const size_t masks = (size_t)2 * t.n_lif * nwaves * sizeof(unsigned long long);
-    const size_t accs = (size_t)2 * t.lif_total * sizeof(double);
-    const size_t extra = (std::max(masks, accs) + 15) & ~(size_t)15;
-    size_t ring_bytes = 0;
-    for (int pass = 0; pass < 2; ++pass) {
-        for (int l = 1; l < n_layers; ++l) {
-            const bool want = (pass == 0) ? (t.kind[l] == SNN_LIF) : (t.kind[l] == SNN_LI);
-            if (!want) continue;
-            const size_t bytes = (size_t)t.S * t.n[l] * sizeof(float);
-            if (!(opts->flags & SNN_FLAG_HBM_RINGS) && ring_bytes + bytes + extra <= kLdsPerGroup) {
-                t.ring_lds[l] = (int)(ring_bytes / sizeof(float));
-                ring_bytes += bytes;
+    // ---- LDS plans
+    int maxlif = 0;
+    for (int l = 1; l < n_layers; ++l)
+        if (t.kind[l] == SNN_LIF) maxlif = std::max(maxlif, t.n[l]);
+    net->core_threads = std::max(64, ((maxlif + 63) / 64) * 64);
+    const int nwaves = net->core_threads / 64;
+    // forward core: LIF->LIF rings (projection order), then the ballot masks
+    {
+        const size_t masks = align16((size_t)2 * t.n_lif * nwaves * sizeof(unsigned long long));
+        size_t used = 0;
+        for (int p = 0; p < t.P; ++p) {
+            if (t.pre[p] == 0 || t.kind[t.post[p]] != SNN_LIF) continue;
+            const size_t bytes = (size_t)t.S * t.n[t.post[p]] * sizeof(float);
+            if (!hbm && used + bytes + masks <= kLds) {
+                t.fring[p] = (int)(used / sizeof(float));
+                used += bytes;
             }
         }
+        net->mask_off = (int)align16(used);
+        net->lds_core_f = net->mask_off + masks;
     }
-    ring_bytes = (ring_bytes + 15) & ~(size_t)15;
-    net->extra_off = (int)ring_bytes;
-    net->lds = ring_bytes + extra;
+    // backward core: adjoint rings of the LIF layers read by LIF-pre projections
+    bool read_by_lif[SNN_MAX_LAYERS] = {false};
+    for (int p = 0; p < t.P; ++p)
+        if (t.pre[p] != 0 && t.kind[t.post[p]] == SNN_LIF) read_by_lif[t.post[p]] = true;
+    {
+        const size_t accs = align16((size_t)2 * t.lif_total * sizeof(double));
+        size_t used = 0;
+        for (int l = 1; l < n_layers; ++l) {
+            if (!read_by_lif[l]) continue;
+            const size_t bytes = (size_t)t.S * t.n[l] * sizeof(float);
+            if (!hbm && used + bytes + accs <= kLds) {
+                t.bring[l] = (int)(used / sizeof(float));
+                used += bytes;
+            }
+        }
+        net->acc_off = (int)align16(used);
+        net->lds_core_b = net->acc_off + accs;
+    }
+    // input scan: posts per workgroup so that the ring [S][nb] fits
+    {
+        int nb = (int)(kLds / ((size_t)t.S * sizeof(float)));
+        nb = std::min(256, (nb / 64) * 64);
+        nb = std::min(nb, t.n[1]);
+        net->scan_nb = nb;
+        net->lds_scan = (size_t)t.S * nb * sizeof(float);
+    }
+    // readout: arrival table / adjoint table [T][C] and an fp64 scratch
+    net->read_threads = ((C + 63) / 64) * 64;
+    {
+        const size_t tab = align16((size_t)t.T * C * sizeof(float));
+        const size_t red = (size_t)kKB * sizeof(double);
+        if (!hbm && tab + red <= kLds) {
+            net->table_lds = 0;
+            net->red_off = (int)tab;
+            net->lds_read = tab + red;
+        } else {
+            net->table_lds = -1;
+            net->red_off = 0;
+            net->lds_read = red;
+        }
+    }
+    net->lds_grad = (size_t)2 * t.T * sizeof(float);
+    net->blk[0] = 0;
+    for (int p = 0; p < t.P; ++p) net->blk[p + 1] = net->blk[p] + t.n[t.post[p]];
+    net->grad_blocks = net->blk[t.P];
 
+    // ---- device scratch
     hipError_t e = hipSuccess;
-    const size_t B = t.B, T1 = (size_t)t.T + 1, cap = (size_t)t.cap, nl = (size_t)std::max(t.n_lif, 1);
-    const size_t C = t.n[n_layers - 1];
+    const size_t B = t.B, T = (size_t)t.T, T1 = T + 1, cap = (size_t)t.cap;
+    const size_t nl = (size_t)std::max(t.n_lif, 1);
+    const int feed = t.pre[t.out_p];
 #define ALLOC(ptr, count)                                 \
     if (e == hipSuccess) e = dalloc(&(ptr), (count));
     ALLOC(net->slot, (size_t)net->n_params);
-    for (int l = 1; l < n_layers; ++l)
-        if (t.ring_lds[l] < 0) ALLOC(net->ring[l], B * t.S * t.n[l]);
     ALLOC(net->in_idx, B * T1);
+    ALLOC(net->A_in, B * T * t.n[1]);
+    for (int p = 0; p < t.P; ++p)
+        if (t.pre[p] != 0 && t.kind[t.post[p]] == SNN_LIF && t.fring[p] < 0)
+            ALLOC(net->fring[p], B * t.S * t.n[t.post[p]]);
+    for (int l = 1; l < n_layers; ++l)
+        if (read_by_lif[l] && t.bring[l] < 0) ALLOC(net->bring[l], B * t.S * t.n[l]);
     ALLOC(net->rec_n, nl * B * cap);
+    ALLOC(net->rec_s, nl * B * cap);
     ALLOC(net->rec_I, nl * B * cap);
-    ALLOC(net->rec_D, nl * B * cap);
     ALLOC(net->rec_idx, nl * B * T1);
+    ALLOC(net->rec_cnt, nl * B);
+    ALLOC(net->rec_goff, nl * B * (t.maxn + 1));
+    ALLOC(net->rec_gstep, nl * B * cap);
     ALLOC(net->z, B * C);
     ALLOC(net->nstar, B * C);
     ALLOC(net->src, B * C);
     ALLOC(net->Vf, B * so);
     ALLOC(net->If, B * so);
-    ALLOC(net->SU, (size_t)net->n_params);
-    ALLOC(net->SD, (size_t)net->n_params);
+    if (net->table_lds < 0) ALLOC(net->table, B * T * C);
+    ALLOC(net->tu_lif, B * t.lif_total * T);
+    ALLOC(net->td_lif, B * t.lif_total * T);
+    ALLOC(net->tu_out, B * C * T);
+    ALLOC(net->td_out, B * C * T);
+    if (feed != 0) ALLOC(net->A2, B * cap);
+    ALLOC(net->in_goff, B * (t.n_in + 1));
     ALLOC(net->st, 1);
 #undef ALLOC
     if (e == hipSuccess) e = hipHostMalloc((void**)&net->st_host, sizeof(DevStatus), hipHostMallocDefault);
-    if (e == hipSuccess) e = set_kernel_lds_limits(std::max(net->lds, (size_t)1));
+    if (e == hipSuccess) e = set_kernel_lds_limits(kLds);
     net->timing = (opts->flags & SNN_FLAG_TIMING) ? 1 : 0;
-    for (int i = 0; i < 6 && net->timing && e == hipSuccess; ++i) e = hipEventCreate(&net->ev[i]);
+    for (int i = 0; i < 2 * K_N && net->timing && e == hipSuccess; ++i) e = hipEventCreate(&net->ev[i]);
     if (e != hipSuccess) {
         const int code = (e == hipErrorOutOfMemory) ? SNN_ENOMEM : SNN_EDEVICE;
         free_all(net);
@@ -257,6 +348,24 @@ static int read_status(snn_net* net) {
     return SNN_OK;
 }
 
+#define TIMED(net, k, expr)                                                                 \
+    do {                                                                                    \
+        if ((net)->timing) HIP_TRY(net, hipEventRecord((net)->ev[2 * (k)], (net)->stream)); \
+        HIP_TRY(net, expr);                                                                 \
+        if ((net)->timing)                                                                  \
+            HIP_TRY(net, hipEventRecord((net)->ev[2 * (k) + 1], (net)->stream));           \
+    } while (0)
+
+static int collect_times(snn_net* net, int k0, int k1, bool has_core) {
+    if (!net->timing) return SNN_OK;
+    for (int k = k0; k < k1; ++k) {
+        net->stats.kernel_ms[k] = 0.0f;
+        if (!has_core && (k == K_CORE || k == K_BCORE)) continue;
+        HIP_TRY(net, hipEventElapsedTime(&net->stats.kernel_ms[k], net->ev[2 * k], net->ev[2 * k + 1]));
+    }
+    return SNN_OK;
+}
+
 extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* const* W,
                            const float* const* D, const int32_t* labels, snn_spikes_out* records,
                            float* loss, float* z) {
@@ -277,40 +386,67 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
             return fail(net, SNN_EINVAL, "NULL record buffers of layer %d", l);
     }
     hipStream_t s = net->stream;
-    const int C = t.n[t.L - 1];
+    const int C = t.n[t.out_l];
     HIP_TRY(net, launch_reset_status(net->st, s));
     HIP_TRY(net, launch_validate(in->offsets, in->step, in->neuron, in->nnz, t.B, t.T, t.n_in, labels,
                                  C, net->st, s));
     HIP_TRY(net, launch_step_index(in->offsets, in->step, t.B, t.T, net->in_idx, net->st, s));
     HIP_TRY(net, launch_round_delays(D, t.woff, net->cnt, t.P, net->max_delay, net->slot, net->st, s));
 
-    FwdArgs a{};
-    a.t = t;
-    for (int p = 0; p < t.P; ++p) a.W[p] = W[p];
-    a.slot = net->slot;
-    for (int l = 0; l < SNN_MAX_LAYERS; ++l) a.ring[l] = net->ring[l];
-    a.in_neuron = in->neuron;
-    a.in_idx = net->in_idx;
-    for (int l = 1; l < t.L; ++l) {
-        if (t.kind[l] != SNN_LIF) continue;
-        a.out_count[l] = records[t.lif[l]].count;
-        a.out_step[l] = records[t.lif[l]].step;
-        a.out_neuron[l] = records[t.lif[l]].neuron;
+    InScanArgs sa{};
+    sa.t = t;
+    sa.W0 = W[0];
+    sa.slot0 = net->slot;
+    sa.in_neuron = in->neuron;
+    sa.in_idx = net->in_idx;
+    sa.A_in = net->A_in;
+    sa.st = net->st;
+    sa.nb = net->scan_nb;
+    TIMED(net, K_SCAN, launch_input_scan(sa, net->lds_scan, s));
+
+    if (t.n_lif > 0) {
+        CoreFwdArgs a{};
+        a.t = t;
+        for (int p = 0; p < t.P; ++p) a.W[p] = W[p];
+        a.slot = net->slot;
+        for (int p = 0; p < t.P; ++p) a.ring[p] = net->fring[p];
+        a.A_in = net->A_in;
+        for (int l = 1; l < t.L; ++l) {
+            if (t.kind[l] != SNN_LIF) continue;
+            a.out_count[l] = records[t.lif[l]].count;
+            a.out_step[l] = records[t.lif[l]].step;
+            a.out_neuron[l] = records[t.lif[l]].neuron;
+        }
+        a.rec_n = net->rec_n;
+        a.rec_s = net->rec_s;
+        a.rec_I = net->rec_I;
+        a.rec_idx = net->rec_idx;
+        a.rec_cnt = net->rec_cnt;
+        a.Vf = net->Vf;
+        a.If = net->If;
+        a.st = net->st;
+        a.mask_off = net->mask_off;
+        TIMED(net, K_CORE, launch_forward_core(a, net->core_threads, net->lds_core_f, s));
     }
-    a.rec_n = net->rec_n;
-    a.rec_I = net->rec_I;
-    a.rec_idx = net->rec_idx;
-    a.z = net->z;
-    a.nstar = net->nstar;
-    a.Vf = net->Vf;
-    a.If = net->If;
-    a.st = net->st;
-    a.mask_off = net->extra_off;
-    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[0], s));
-    HIP_TRY(net, launch_forward(a, net->threads, net->lds, s));
-    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[1], s));
-    HIP_TRY(net, launch_loss(net->z, labels, net->nstar, t.B, C, t.loss, t.rscale, net->tau_m, loss,
-                             net->src, net->st, s));
+    ReadoutArgs r{};
+    r.t = t;
+    r.W = W[t.out_p];
+    r.slot = net->slot;
+    r.A_in = net->A_in;
+    r.rec_n = net->rec_n;
+    r.rec_s = net->rec_s;
+    r.rec_idx = net->rec_idx;
+    r.table = net->table;
+    r.table_lds = net->table_lds;
+    r.red_off = net->red_off;
+    r.z = net->z;
+    r.nstar = net->nstar;
+    r.Vf = net->Vf;
+    r.If = net->If;
+    r.st = net->st;
+    TIMED(net, K_READ, launch_readout_forward(r, net->read_threads, net->lds_read, s));
+    HIP_TRY(net, launch_loss(net->z, labels, t.B, C, t.loss, t.rscale, net->tau_m, loss, net->src,
+                             net->st, s));
     if (z)
         HIP_TRY(net, hipMemcpyAsync(z, net->z, sizeof(float) * t.B * C, hipMemcpyDeviceToDevice, s));
     int rc = read_status(net);
@@ -319,11 +455,13 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
     if (h.bad_input)
         return fail(net, SNN_EINVAL, "input spikes or labels invalid (offsets, range, order)");
     memset(&net->stats, 0, sizeof(net->stats));
+    rc = collect_times(net, K_SCAN, K_RADJ, t.n_lif > 0);
+    if (rc) return rc;
     net->stats.input_spikes = in->nnz;
     net->stats.clamped_delays = (int64_t)h.clamped;
     net->stats.overflow = h.overflow;
-    for (int l = 1; l < t.L; ++l)
-        if (t.ring_lds[l] >= 0) net->stats.lds_rings |= 1 << l;
+    for (int p = 0; p < t.P; ++p)
+        if (t.fring[p] >= 0) net->stats.lds_rings |= 1 << p;
     long long ev = 0;
     for (int p = 0; p < t.P; ++p) {
         const int pre = t.pre[p];
@@ -332,9 +470,11 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
     }
     for (int li = 0; li < t.n_lif; ++li) net->stats.lif_spikes += (int64_t)h.layer_spikes[li];
     net->stats.events = ev;
-    if (net->timing) HIP_TRY(net, hipEventElapsedTime(&net->stats.forward_kernel_ms, net->ev[0], net->ev[1]));
     for (int p = 0; p < t.P; ++p) net->W[p] = W[p];
+    net->in_off = in->offsets;
+    net->in_step = in->step;
     net->in_neuron = in->neuron;
+    net->in_nnz = in->nnz;
     net->fwd_ok = 1;
     net->fwd_overflow = h.overflow;
     if (h.overflow) return fail(net, SNN_EOVERFLOW, "a sample exceeded record_capacity spikes");
@@ -352,38 +492,106 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
     for (int p = 0; p < t.P; ++p)
         if (!dW[p] || !dD[p]) return fail(net, SNN_EINVAL, "NULL dW or dD of projection %d", p);
     hipStream_t s = net->stream;
-    HIP_TRY(net, launch_fill_f64(net->SU, net->n_params, s));
-    HIP_TRY(net, launch_fill_f64(net->SD, net->n_params, s));
-    BwdArgs a{};
-    a.t = t;
-    for (int p = 0; p < t.P; ++p) a.W[p] = net->W[p];
-    a.slot = net->slot;
-    for (int l = 0; l < SNN_MAX_LAYERS; ++l) a.ring[l] = net->ring[l];
-    a.in_neuron = net->in_neuron;
-    a.in_idx = net->in_idx;
-    a.rec_n = net->rec_n;
-    a.rec_I = net->rec_I;
-    a.rec_D = net->rec_D;
-    a.rec_idx = net->rec_idx;
-    a.src = net->src;
-    a.nstar = net->nstar;
-    a.SU = net->SU;
-    a.SD = net->SD;
-    a.st = net->st;
-    a.acc_off = net->extra_off;
-    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2], s));
-    HIP_TRY(net, launch_backward_a(a, net->threads, net->lds, s));
-    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[3], s));
-    HIP_TRY(net, launch_backward_b(a, net->threads, net->lds, s));
-    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[4], s));
-    HIP_TRY(net, launch_finalize(net->SU, net->SD, dW, dD, t.woff, net->cnt, t.P, t.tau_s, t.dt, s));
+    // the grouped input steps need one slot per input spike of the last forward
+    if (net->in_nnz > net->in_gstep_cap) {
+        HIP_TRY(net, hipStreamSynchronize(s));
+        if (net->in_gstep) HIP_TRY(net, hipFree(net->in_gstep));
+        net->in_gstep = nullptr;
+        net->in_gstep_cap = 0;
+        const hipError_t e = hipMalloc((void**)&net->in_gstep, (size_t)net->in_nnz * sizeof(int));
+        if (e != hipSuccess)
+            return fail(net, e == hipErrorOutOfMemory ? SNN_ENOMEM : SNN_EDEVICE, "hipMalloc: %s",
+                        hipGetErrorString(e));
+        net->in_gstep_cap = net->in_nnz;
+    }
+    ReadoutArgs r{};
+    r.t = t;
+    r.W = net->W[t.out_p];
+    r.slot = net->slot;
+    r.rec_n = net->rec_n;
+    r.rec_s = net->rec_s;
+    r.rec_idx = net->rec_idx;
+    r.nstar = net->nstar;
+    r.src = net->src;
+    r.tu = net->tu_out;
+    r.td = net->td_out;
+    r.table_lds = net->table_lds;
+    r.red_off = net->red_off;
+    r.A2 = net->A2;
+    r.st = net->st;
+    TIMED(net, K_RADJ, launch_readout_adjoint(r, net->read_threads, net->lds_read, s));
+    if (t.n_lif > 0) {
+        CoreBwdArgs a{};
+        a.t = t;
+        for (int p = 0; p < t.P; ++p) a.W[p] = net->W[p];
+        a.slot = net->slot;
+        for (int l = 0; l < SNN_MAX_LAYERS; ++l) a.ring[l] = net->bring[l];
+        a.rec_n = net->rec_n;
+        a.rec_I = net->rec_I;
+        a.rec_idx = net->rec_idx;
+        a.A2 = net->A2;
+        a.tu = net->tu_lif;
+        a.td = net->td_lif;
+        a.st = net->st;
+        a.acc_off = net->acc_off;
+        TIMED(net, K_BCORE, launch_backward_core(a, net->core_threads, net->lds_core_b, s));
+    }
+    // spikes grouped by presynaptic neuron: inputs, then every LIF layer
+    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GROUP], s));
+    {
+        GroupArgs g{};
+        g.off = net->in_off;
+        g.end = net->in_off;
+        g.step = net->in_step;
+        g.neuron = net->in_neuron;
+        g.n = t.n_in;
+        g.g_off = net->in_goff;
+        g.g_step = net->in_gstep;
+        g.st = net->st;
+        HIP_TRY(net, launch_group(g, t.B, s));
+    }
+    for (int l = 1; l < t.L; ++l) {
+        if (t.kind[l] != SNN_LIF) continue;
+        const size_t li = (size_t)t.lif[l];
+        GroupArgs g{};
+        g.cnt = net->rec_cnt + li * t.B;
+        g.off_stride = t.cap;
+        g.step = net->rec_s + li * t.B * t.cap;
+        g.neuron = net->rec_n + li * t.B * t.cap;
+        g.n = t.n[l];
+        g.g_off = net->rec_goff + li * t.B * (t.maxn + 1);
+        g.g_step = net->rec_gstep + li * t.B * t.cap;
+        g.st = net->st;
+        HIP_TRY(net, launch_group(g, t.B, s));
+    }
+    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GROUP + 1], s));
+    GradArgs ga{};
+    ga.t = t;
+    for (int p = 0; p < t.P; ++p) {
+        ga.W[p] = net->W[p];
+        ga.dW[p] = dW[p];
+        ga.dD[p] = dD[p];
+    }
+    ga.slot = net->slot;
+    ga.tu_lif = net->tu_lif;
+    ga.td_lif = net->td_lif;
+    ga.tu_out = net->tu_out;
+    ga.td_out = net->td_out;
+    ga.g_off[0] = net->in_goff;
+    ga.g_step[0] = net->in_gstep;
+    for (int l = 1; l < t.L; ++l) {
+        if (t.kind[l] != SNN_LIF) continue;
+        const size_t li = (size_t)t.lif[l];
+        ga.g_off[l] = net->rec_goff + li * t.B * (t.maxn + 1);
+        ga.g_step[l] = net->rec_gstep + li * t.B * t.cap;
+    }
+    for (int p = 0; p <= t.P; ++p) ga.blk[p] = net->blk[p];
+    TIMED(net, K_GRAD, launch_gradients(ga, net->grad_blocks, net->lds_grad, s));
     int rc = read_status(net);
     if (rc) return rc;
+    rc = collect_times(net, K_RADJ, K_N, t.n_lif > 0);
+    if (rc) return rc;
     net->stats.degenerate_jumps = (int64_t)net->st_host->degenerate;
-    if (net->timing) {
-        HIP_TRY(net, hipEventElapsedTime(&net->stats.backward_a_ms, net->ev[2], net->ev[3]));
-        HIP_TRY(net, hipEventElapsedTime(&net->stats.backward_b_ms, net->ev[3], net->ev[4]));
-    }
     return SNN_OK;
 }
 

@@ -36,7 +36,7 @@ def test_struct_layouts_match_header():
     assert C.sizeof(b.snn_layer) == 12
     assert C.sizeof(b.snn_spikes_in) == 32
     assert C.sizeof(b.snn_spikes_out) == 24
-    assert C.sizeof(b.snn_stats) == 64
+    assert C.sizeof(b.snn_stats) == 80
 
 
 def _create(lib, layers, tau_m=20.0, tau_s=5.0, theta=1.0, dt=1.0, max_delay=10, **opt):
