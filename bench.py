@@ -20,21 +20,59 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 
-# Algorithmic bytes per unit of work of the step (fp32 values, uint8 delay
-# slots, V / I / adjoints held on chip):
-#   synaptic event  forward 13 (w 4, slot 1, delay-buffer read-modify-write 8),
+# Algorithmic bytes per unit of work (fp32 values, uint8 delay slots, V / I /
+# adjoints held on chip), per unit and per kernel of the step:
+#   synaptic event  forward 13 (w 4, slot 1, delay-buffer read-modify-write 8);
 #                   backward 21 (w 4, slot 1, delayed adjoints 8, dW 4, dD 4)
-#   neuron-step     forward 8 (delay-buffer read + clear), backward 8 (history)
-#   LIF spike       16 (record write + read);  input spike 8 (read twice)
-BYTES_STEP = {"event": 34, "neuron_step": 16, "lif_spike": 16, "input_spike": 8}
+#   neuron-step     forward 8 (delay-buffer read + clear); backward 8 (adjoint
+#                   history write)
+#   LIF spike       8 written by the forward, 8 read by the backward
+#   input spike     4 read by the forward, 4 by the backward
+# Whole step: 34 per event, 16 per neuron-step, 16 per LIF spike, 8 per input
+# spike.  The kernels split this as follows; the jump sums of LIF-pre events
+# read w, slot and the delayed adjoints a second time (13 per event) in the
+# kernel that applies the jumps, before the gradient kernel's own pass.
+def kernel_bytes(u):
+    return {
+        "input_scan": 13 * u["E_in"] + 4 * u["S_in"],
+        "forward_core": 13 * u["E_ll"] + 8 * u["NS_lif"] + 8 * u["S_lif"],
+        "readout_forward": 13 * u["E_ro"] + 8 * u["NS_li"],
+        "readout_adjoint": 13 * u["E_ro"] + 8 * u["NS_li"],
+        "backward_core": 13 * u["E_ll"] + 8 * u["NS_lif"] + 8 * u["S_lif"],
+        "group": 4 * u["S_in"] + 8 * u["S_lif"],
+        "gradients": 21 * (u["E_in"] + u["E_ll"] + u["E_ro"]),
+    }
+
+
+def step_bytes(u):
+    E = u["E_in"] + u["E_ll"] + u["E_ro"]
+    return 34 * E + 16 * (u["NS_lif"] + u["NS_li"]) + 16 * u["S_lif"] + 8 * u["S_in"]
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or
+    None when the kernel sources changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_audio-700-256rec-20.txt")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    for line in open(path):
+        f = line.split()
+        if len(f) >= 2 and not line.startswith("#"):
+            rec[" ".join(f[:-1])] = f[-1]
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2501_07331_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        with open(os.path.join(d, f), "rb") as fh:
+            h.update(fh.read())
+    if rec.get("source_sha256") != h.hexdigest() or f"traffic {kernel}" not in rec:
+        return None
+    return int(rec[f"traffic {kernel}"])
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
-
-
-def step_bytes(units):
-    return sum(BYTES_STEP[k] * units[k] for k in BYTES_STEP)
 
 
 def cpu_baseline(wl, n_samples):
@@ -64,6 +102,18 @@ def cpu_baseline(wl, n_samples):
                       f"{dt:.2f} s wall on one host core, {E} events"}
 
 
+def copy_calibration(mib):
+    import torch
+    n = mib * (1 << 20) // 4
+    x = torch.ones(n, device="cuda")
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "launches": 5}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -71,7 +121,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-samples", type=int, default=256,
                     help="samples of the batch the oracle baseline runs (0: skip)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB five times (the reference "
+                         "kernel the HBM byte counters are scaled by) and exit")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (--gpus {args.gpus} requested): the data-parallel "
               "split over GPUs (an all-reduce of dW/dD per step) is designed, not built.",
@@ -127,12 +183,18 @@ def main():
     s = net.stats()
     E = s["events"]
     ms = 1e3 * elapsed / args.steps
-    units = {"event": E, "neuron_step": wl.B * wl.T * sum(l[0] for l in c.layers[1:]),
-             "lif_spike": s["lif_spikes"], "input_spike": s["input_spikes"]}
+    # units of work, from the spike counts of this batch (one LIF layer)
+    S_lif = int(recs[0][0].sum().item())
+    n_in, n_h, C = c.layers[0][0], c.layers[1][0], c.layers[2][0]
+    u = {"E_in": s["input_spikes"] * n_h, "E_ll": S_lif * n_h, "E_ro": S_lif * C,
+         "NS_lif": wl.B * wl.T * n_h, "NS_li": wl.B * wl.T * C, "S_lif": S_lif,
+         "S_in": s["input_spikes"]}
+    assert u["E_in"] + u["E_ll"] + u["E_ro"] == E
     avg = {k: float(np.mean(v)) for k, v in kt.items()}
     dom = max(avg, key=avg.get)
-    # the whole step's algorithmic bytes over the whole step's time
-    ach = step_bytes(units) / (elapsed / args.steps) / 1e9
+    kb = kernel_bytes(u)
+    ach = kb[dom] / (avg[dom] * 1e-3) / 1e9
+    kernel_frac = {k: round(kb[k] / (avg[k] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4) for k in avg}
     log(f"kernel ms: {avg}  step ms {ms:.3f}  events {E}  lif spikes/neuron/sample "
         f"{s['lif_spikes'] / wl.B / 256:.2f}")
     out = {
@@ -152,9 +214,13 @@ def main():
                                "20 LI, B=256, T=1000, dt=1ms, delays ff U[0,150] rec U[0,50]",
                    "events_per_step": E, "input_spikes": s["input_spikes"],
                    "lif_spikes": s["lif_spikes"],
-                   "kernel_ms": {k: round(v, 4) for k, v in avg.items()}},
+                   "kernel_ms": {k: round(v, 4) for k, v in avg.items()},
+                   "kernel_hbm_frac": kernel_frac,
+                   "step_alg_bytes": step_bytes(u),
+                   "step_hbm_frac": round(step_bytes(u) / (elapsed / args.steps) / 1e9 / HBM_PEAK_GBS, 4)},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": ach, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": ach / HBM_PEAK_GBS, "traffic": None},
+                     "unit": "GB/s", "frac": ach / HBM_PEAK_GBS, "traffic": measured_traffic(dom),
+                     "alg_bytes_per_launch": kb[dom]},
     }
     if args.cpu_samples > 0:
         log("timing the oracle on the host ...")

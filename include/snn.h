@@ -26,13 +26,16 @@
  * gamma*I), I- = beta*I with alpha = e^{-dt/tau_m}, beta = e^{-dt/tau_s},
  * gamma = tau_s/(tau_s - tau_m) (beta - alpha) (constants computed in fp64 on
  * the host, rounded to fp32); threshold V- >= theta, reset, record (n, i, I-);
- * emit every presynaptic spike into a per-(sample, post layer) delay ring at
- * slot (n + d) mod S, S = max_delay + 1, dropping arrivals at or after T;
- * then I = I- + ring[n mod S].  Delays are integer multiples of dt: the slot
- * is rint(D) (round half to even) clamped to [0, max_delay], NaN -> 0.
- * All forward arithmetic is IEEE fp32 with no contraction, in the fixed order
- * (emission step, projection, presynaptic index) per ring cell, so spike
- * records are bit-reproducible.
+ * emit every presynaptic spike into its projection's delay ring (one per
+ * sample and projection) at slot (n + d) mod S, S = max_delay + 1, dropping
+ * arrivals at or after T; then I = I- + ring_p[n mod S] for the projections p
+ * into the layer, in projection order.  Delays are integer multiples of dt:
+ * the slot is rint(D) (round half to even) clamped to [0, max_delay],
+ * NaN -> 0.  All forward arithmetic is IEEE fp32 with no contraction; a ring
+ * cell sums its weights in (emission step, presynaptic index) order, so spike
+ * records are bit-reproducible.  The backward pass keeps adjoints in fp32 and
+ * sums each synapse's gradient terms over one sample in fp32, in spike order,
+ * and over the samples in fp64, in sample order: dW and dD are deterministic.
  *
  * Projections.  Fixed order: for l = 1 .. L-1, the feed-forward projection
  * (l-1 -> l), then the recurrent one (l -> l) if layer l is recurrent.  Weight
@@ -42,9 +45,10 @@
  *
  * Memory.  Every pointer argument marked (dev) is device memory owned by the
  * caller.  Inputs are read-only; outputs are fully overwritten.  The library
- * owns its scratch (delay rings, adjoint rings, internal spike records,
- * per-step indices, fp64 gradient accumulators, a status word), allocated
- * in snn_create and released in snn_destroy.  Work is enqueued on
+ * owns its scratch (delay rings, adjoint rings and trajectories, internal
+ * spike records, per-step indices, a status word), allocated in snn_create
+ * (grown on demand by the first calls that need more) and released in
+ * snn_destroy.  Work is enqueued on
  * opts.hip_stream (NULL = the default stream); each snn_forward and
  * snn_backward ends with one small status read-back, so counts and error
  * codes are final when the call returns.  A handle is not thread-safe;
