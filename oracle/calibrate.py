@@ -2,8 +2,10 @@
 
 For each configuration with a target activity, and each feed-forward projection
 into a LIF layer in projection order, bisect the weight mean mu so that the
-oracle forward over the first 8 samples gives the target mean number of spikes
-per neuron per sample in that projection's post layer (about 14, the hidden
+oracle forward over the first samples of the batch (the whole batch, at most 32
+samples for the two-layer 1024-neuron config whose oracle is slow) gives the
+target mean number of spikes per neuron per sample in that projection's post
+layer (about 14, the hidden
 spike-count target the paper uses on SHD; about 1 for the latency-coded
 config).  Writes ``workloads/calibration.json``; run once:
 
@@ -23,7 +25,12 @@ from workloads.generators import input_spikes, weights_and_delays
 
 from . import grid
 
-N_SAMPLES = 8
+MAX_SAMPLES_WIDE = 32       # for networks wider than 512 LIF neurons
+
+
+def n_samples(cfg):
+    wide = sum(n for n, k, _ in cfg.layers if k == 1) > 512
+    return min(cfg.B, MAX_SAMPLES_WIDE) if wide else cfg.B
 
 
 def _rate(cfg, mus, layer, off, st, ne):
@@ -32,7 +39,7 @@ def _rate(cfg, mus, layer, off, st, ne):
                          cfg.loss, cfg.readout_scale)
     f = grid.forward(net, off, st, ne, W, D)
     li = [l for l in range(len(cfg.layers)) if cfg.layers[l][1] == 1].index(layer)
-    return f.count[li].sum() / (N_SAMPLES * cfg.layers[layer][0])
+    return f.count[li].sum() / ((len(off) - 1) * cfg.layers[layer][0])
 
 
 def calibrate(cid: int):
@@ -40,7 +47,7 @@ def calibrate(cid: int):
     mus = [m for m, _ in cfg.w_init]
     if cfg.target_rate <= 0:
         return mus
-    off, st, ne = input_spikes(cfg, N_SAMPLES)
+    off, st, ne = input_spikes(cfg, n_samples(cfg))
     for p, (a, q) in enumerate(projections(cfg.layers)):
         if p not in cfg.calibrate:
             continue
@@ -78,7 +85,7 @@ def main(argv):
         mus = calibrate(cid)
         cal[str(cid)] = {"mu": {str(p): float(mus[p]) for p in CONFIGS[cid].calibrate},
                          "target_spikes_per_neuron": CONFIGS[cid].target_rate,
-                         "samples": N_SAMPLES}
+                         "samples": n_samples(CONFIGS[cid])}
         with open(_CAL_PATH, "w") as f:
             json.dump(cal, f, indent=1, sort_keys=True)
     return 0

@@ -10,7 +10,8 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRCS = [os.path.join(HERE, "csrc", f) for f in ("snn_api.hip", "snn_kernels.hip")]
+SRCS = sorted(os.path.join(HERE, "csrc", f) for f in os.listdir(os.path.join(HERE, "csrc"))
+              if f.endswith(".hip"))
 OUT = os.path.join(HERE, "libsnn.so")
 ARCH = os.environ.get("SNN_OFFLOAD_ARCH", "gfx950")
 

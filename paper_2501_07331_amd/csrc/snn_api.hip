@@ -13,7 +13,6 @@
 namespace {
 
 constexpr size_t kLds = 160 * 1024;   // gfx950: 160 KiB of LDS per workgroup
-constexpr int kKB = 8;                // spikes per batch in the kernels (fp64 scratch)
 enum { K_SCAN, K_CORE, K_READ, K_RADJ, K_BCORE, K_GROUP, K_GRAD, K_N };
 
 size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
@@ -26,17 +25,22 @@ struct snn_net {
     int max_delay;
     int core_threads;           // LIF-core workgroup size
     int read_threads;           // readout workgroup size
-    size_t lds_core_f, lds_core_b, lds_scan, lds_read, lds_grad;
-    int mask_off, acc_off, scan_nb, table_lds, red_off;
+    size_t lds_core_f, lds_core_b, lds_scan, lds_read, lds_grad, lds_radj;
+    int mask_off, scan_nb, table_lds;
+    int bpart_off;              // backward-core LDS plan
+    int bring_mode[SNN_MAX_LAYERS];   // adjoint ring of a LIF layer: -2 none, -1 HBM, >= 0 LDS
+    int radj_threads, radj_tab;
+    int grad_J, grad_threads, grad_SB, grad_bs, grad_nblk, grad_ngroups;
+    GradGroup grad_grp[SNN_MAX_LAYERS];
     hipStream_t stream;
     long long n_params;
     long long cnt[SNN_MAXP];
     int n_state;
     int st_off[SNN_MAX_LAYERS];
-    int grad_blocks;
-    int blk[SNN_MAXP + 1];
     // device scratch
     uint8_t* slot;
+    uint2* ws;                  // (weight bits, slot) of every synapse
+    int* steptab;
     int* in_idx;
     float* A_in;
     float* fring[SNN_MAXP];
@@ -59,6 +63,7 @@ struct snn_net {
     float* tu_out;
     float* td_out;
     double* A2;
+    double* gpart;
     int* in_goff;
     int* in_gstep;
     long long in_gstep_cap;
@@ -98,7 +103,8 @@ static void free_all(snn_net* n) {
     void* bufs[] = {n->slot,    n->in_idx,  n->A_in,     n->rec_n,     n->rec_s,  n->rec_I,
                     n->rec_idx, n->rec_cnt, n->rec_goff, n->rec_gstep, n->z,      n->nstar,
                     n->src,     n->Vf,      n->If,       n->table,     n->tu_lif, n->td_lif,
-                    n->tu_out,  n->td_out,  n->A2,       n->in_goff,   n->in_gstep, n->st};
+                    n->tu_out,  n->td_out,  n->A2,       n->in_goff,   n->in_gstep, n->st,
+                    n->gpart,   n->ws,      n->steptab};
     for (void* p : bufs)
         if (p) (void)hipFree(p);
     for (int p = 0; p < SNN_MAXP; ++p)
@@ -139,7 +145,7 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         if (y.recurrent && y.kind != SNN_LIF) return SNN_EINVAL;
         if (l > 0 && y.n > SNN_MAX_NEURONS) return SNN_EINVAL;
     }
-    // the gradient kernel stages two fp32 trajectories of T steps in LDS
+    // the gradient kernel stages (lambda_I, lambda_I - lambda_V) of T steps in LDS
     if ((size_t)opts->T * 2 * sizeof(float) > kLds) return SNN_EINVAL;
     if ((long long)opts->batch * (opts->T + 1) > (1LL << 31)) return SNN_EINVAL;
 
@@ -229,23 +235,34 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         net->mask_off = (int)align16(used);
         net->lds_core_f = net->mask_off + masks;
     }
-    // backward core: adjoint rings of the LIF layers read by LIF-pre projections
+    // backward core: partial jump sums [2][NL][KP][4 NW] and the adjoint
+    // rings of the LIF layers read by LIF-pre projections (all in LDS, or all
+    // in HBM)
     bool read_by_lif[SNN_MAX_LAYERS] = {false};
     for (int p = 0; p < t.P; ++p)
         if (t.pre[p] != 0 && t.kind[t.post[p]] == SNN_LIF) read_by_lif[t.post[p]] = true;
     {
-        const size_t accs = align16((size_t)2 * t.lif_total * sizeof(double));
-        size_t used = 0;
-        for (int l = 1; l < n_layers; ++l) {
+        const int NL = std::max(t.n_lif, 1);
+        const int KP = (NL == 1) ? 16 : 4;
+        net->bpart_off = 0;
+        const size_t part = align16((size_t)2 * NL * KP * 4 * nwaves * sizeof(double));
+        size_t used = part;
+        bool all_lds = !hbm;
+        for (int l = 0; l < n_layers; ++l) {
+            net->bring_mode[l] = -2;
             if (!read_by_lif[l]) continue;
             const size_t bytes = (size_t)t.S * t.n[l] * sizeof(float);
-            if (!hbm && used + bytes + accs <= kLds) {
-                t.bring[l] = (int)(used / sizeof(float));
-                used += bytes;
-            }
+            net->bring_mode[l] = (int)(used / sizeof(float));
+            used += bytes;
         }
-        net->acc_off = (int)align16(used);
-        net->lds_core_b = net->acc_off + accs;
+        if (used > kLds) all_lds = false;
+        if (!all_lds) {
+            used = part;
+            for (int l = 0; l < n_layers; ++l)
+                if (net->bring_mode[l] >= 0) net->bring_mode[l] = -1;
+        }
+        for (int l = 0; l < n_layers; ++l) t.bring[l] = net->bring_mode[l] >= 0 ? net->bring_mode[l] : -1;
+        net->lds_core_b = used;
     }
     // input scan: posts per workgroup so that the ring [S][nb] fits
     {
@@ -255,25 +272,64 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         net->scan_nb = nb;
         net->lds_scan = (size_t)t.S * nb * sizeof(float);
     }
-    // readout: arrival table / adjoint table [T][C] and an fp64 scratch
+    // readout forward: arrival table [T][C] in LDS when it fits
     net->read_threads = ((C + 63) / 64) * 64;
     {
         const size_t tab = align16((size_t)t.T * C * sizeof(float));
-        const size_t red = (size_t)kKB * sizeof(double);
-        if (!hbm && tab + red <= kLds) {
+        if (!hbm && tab <= kLds) {
             net->table_lds = 0;
-            net->red_off = (int)tab;
-            net->lds_read = tab + red;
+            net->lds_read = tab;
         } else {
             net->table_lds = -1;
-            net->red_off = 0;
-            net->lds_read = red;
+            net->lds_read = 0;
         }
     }
-    net->lds_grad = (size_t)2 * t.T * sizeof(float);
-    net->blk[0] = 0;
-    for (int p = 0; p < t.P; ++p) net->blk[p + 1] = net->blk[p] + t.n[t.post[p]];
-    net->grad_blocks = net->blk[t.P];
+    // readout adjoint: the [T][C] table of lambda_I - lambda_V in LDS when it fits
+    net->radj_threads = std::min(1024, std::max(256, ((C + 63) / 64) * 64));
+    net->radj_tab = (!hbm && (size_t)t.T * C * sizeof(float) <= kLds) ? 1 : 0;
+    net->lds_radj = net->radj_tab ? (size_t)t.T * C * sizeof(float) : 0;
+    // gradients: one group per post layer (its projections in projection
+    // order), J posts per workgroup, samples split into SB blocks so that the
+    // grid has about 512 workgroups; workgroups in units of 4 J-blocks
+    {
+        net->grad_J = ((size_t)8 * t.T * 2 * sizeof(float) <= kLds) ? 8 : 1;
+        const int J = net->grad_J;
+        int ng = 0, jblocks = 0, maxpre = 64;
+        for (int q = 1; q < n_layers; ++q) {
+            GradGroup& g = net->grad_grp[ng];
+            g = GradGroup{};
+            g.nq = t.n[q];
+            g.jb = (g.nq + J - 1) / J;
+            g.out = (q == t.out_l) ? 1 : 0;
+            g.off = g.out ? 0 : t.lif_off[q];
+            for (int p = 0; p < t.P; ++p) {
+                if (t.post[p] != q) continue;
+                g.p[g.np] = p;
+                g.pre[g.np] = t.pre[p];
+                g.npre[g.np] = t.n[t.pre[p]];
+                ++g.np;
+            }
+            maxpre = std::max(maxpre, g.npre[0] + (g.np > 1 ? g.npre[1] : 0));
+            jblocks += g.jb;
+            ++ng;
+        }
+        int SB = std::max(1, std::min(t.B, (512 + jblocks - 1) / jblocks));
+        const int bs = (t.B + SB - 1) / SB;
+        SB = (t.B + bs - 1) / bs;
+        int blk = 0;
+        for (int g = 0; g < ng; ++g) {
+            GradGroup& G = net->grad_grp[g];
+            G.blk0 = blk;
+            G.units = (((G.jb + 3) / 4) * SB + 7) / 8 * 8;
+            blk += G.units * 4;
+        }
+        net->grad_ngroups = ng;
+        net->grad_SB = SB;
+        net->grad_bs = bs;
+        net->grad_nblk = blk;
+        net->grad_threads = std::min(1024, ((maxpre + 63) / 64) * 64);
+        net->lds_grad = (size_t)J * t.T * 2 * sizeof(float);
+    }
 
     // ---- device scratch
     hipError_t e = hipSuccess;
@@ -283,13 +339,15 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
 #define ALLOC(ptr, count)                                 \
     if (e == hipSuccess) e = dalloc(&(ptr), (count));
     ALLOC(net->slot, (size_t)net->n_params);
+    ALLOC(net->ws, (size_t)net->n_params);
+    ALLOC(net->steptab, nl * B * T * (size_t)SNN_STEP_ROW);
     ALLOC(net->in_idx, B * T1);
     ALLOC(net->A_in, B * T * t.n[1]);
     for (int p = 0; p < t.P; ++p)
         if (t.pre[p] != 0 && t.kind[t.post[p]] == SNN_LIF && t.fring[p] < 0)
             ALLOC(net->fring[p], B * t.S * t.n[t.post[p]]);
     for (int l = 1; l < n_layers; ++l)
-        if (read_by_lif[l] && t.bring[l] < 0) ALLOC(net->bring[l], B * t.S * t.n[l]);
+        if (net->bring_mode[l] == -1) ALLOC(net->bring[l], B * t.S * t.n[l]);
     ALLOC(net->rec_n, nl * B * cap);
     ALLOC(net->rec_s, nl * B * cap);
     ALLOC(net->rec_I, nl * B * cap);
@@ -303,16 +361,18 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     ALLOC(net->Vf, B * so);
     ALLOC(net->If, B * so);
     if (net->table_lds < 0) ALLOC(net->table, B * T * C);
-    ALLOC(net->tu_lif, B * t.lif_total * T);
-    ALLOC(net->td_lif, B * t.lif_total * T);
-    ALLOC(net->tu_out, B * C * T);
-    ALLOC(net->td_out, B * C * T);
+    ALLOC(net->tu_lif, B * T * t.lif_total);
+    ALLOC(net->td_lif, B * T * t.lif_total);
+    ALLOC(net->tu_out, B * T * C);
+    ALLOC(net->td_out, B * T * C);
+    if (net->grad_SB > 1) ALLOC(net->gpart, (size_t)net->grad_SB * 2 * (size_t)net->n_params);
     if (feed != 0) ALLOC(net->A2, B * cap);
     ALLOC(net->in_goff, B * (t.n_in + 1));
     ALLOC(net->st, 1);
 #undef ALLOC
     if (e == hipSuccess) e = hipHostMalloc((void**)&net->st_host, sizeof(DevStatus), hipHostMallocDefault);
-    if (e == hipSuccess) e = set_kernel_lds_limits(kLds);
+    if (e == hipSuccess) e = set_forward_lds_limits(kLds);
+    if (e == hipSuccess) e = set_backward_lds_limits(kLds);
     net->timing = (opts->flags & SNN_FLAG_TIMING) ? 1 : 0;
     for (int i = 0; i < 2 * K_N && net->timing && e == hipSuccess; ++i) e = hipEventCreate(&net->ev[i]);
     if (e != hipSuccess) {
@@ -391,7 +451,8 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
     HIP_TRY(net, launch_validate(in->offsets, in->step, in->neuron, in->nnz, t.B, t.T, t.n_in, labels,
                                  C, net->st, s));
     HIP_TRY(net, launch_step_index(in->offsets, in->step, t.B, t.T, net->in_idx, net->st, s));
-    HIP_TRY(net, launch_round_delays(D, t.woff, net->cnt, t.P, net->max_delay, net->slot, net->st, s));
+    HIP_TRY(net, launch_round_delays(D, W, t.woff, net->cnt, t.P, net->max_delay, net->slot, net->ws,
+                                     net->st, s));
 
     InScanArgs sa{};
     sa.t = t;
@@ -422,6 +483,7 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
         a.rec_I = net->rec_I;
         a.rec_idx = net->rec_idx;
         a.rec_cnt = net->rec_cnt;
+        a.steptab = net->steptab;
         a.Vf = net->Vf;
         a.If = net->If;
         a.st = net->st;
@@ -438,7 +500,6 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
     r.rec_idx = net->rec_idx;
     r.table = net->table;
     r.table_lds = net->table_lds;
-    r.red_off = net->red_off;
     r.z = net->z;
     r.nstar = net->nstar;
     r.Vf = net->Vf;
@@ -504,37 +565,86 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
                         hipGetErrorString(e));
         net->in_gstep_cap = net->in_nnz;
     }
-    ReadoutArgs r{};
-    r.t = t;
-    r.W = net->W[t.out_p];
-    r.slot = net->slot;
-    r.rec_n = net->rec_n;
-    r.rec_s = net->rec_s;
-    r.rec_idx = net->rec_idx;
-    r.nstar = net->nstar;
-    r.src = net->src;
-    r.tu = net->tu_out;
-    r.td = net->td_out;
-    r.table_lds = net->table_lds;
-    r.red_off = net->red_off;
-    r.A2 = net->A2;
-    r.st = net->st;
-    TIMED(net, K_RADJ, launch_readout_adjoint(r, net->read_threads, net->lds_read, s));
+    const int C = t.n[t.out_l];
+    const int feed = t.pre[t.out_p];
+    const size_t B = t.B, cap = t.cap;
+    {
+        ReadoutBwdArgs r{};
+        r.B = t.B;
+        r.T = t.T;
+        r.C = C;
+        r.cap = t.cap;
+        r.loss = t.loss;
+        r.alpha = t.alpha;
+        r.beta = t.beta;
+        r.cc = t.cc;
+        r.ws = net->ws + t.woff[t.out_p];
+        if (feed != 0) {
+            const size_t li = (size_t)t.lif[feed];
+            r.rec_n = net->rec_n + li * B * cap;
+            r.rec_s = net->rec_s + li * B * cap;
+            r.rec_cnt = net->rec_cnt + li * B;
+        }
+        r.nstar = net->nstar;
+        r.src = net->src;
+        r.tu = net->tu_out;
+        r.td = net->td_out;
+        r.A2 = net->A2;
+        r.tab_lds = net->radj_tab;
+        TIMED(net, K_RADJ, launch_readout_adjoint(r, net->radj_threads, net->lds_radj, s));
+    }
     if (t.n_lif > 0) {
         CoreBwdArgs a{};
-        a.t = t;
-        for (int p = 0; p < t.P; ++p) a.W[p] = net->W[p];
-        a.slot = net->slot;
-        for (int l = 0; l < SNN_MAX_LAYERS; ++l) a.ring[l] = net->bring[l];
-        a.rec_n = net->rec_n;
-        a.rec_I = net->rec_I;
-        a.rec_idx = net->rec_idx;
-        a.A2 = net->A2;
+        a.B = t.B;
+        a.T = t.T;
+        a.S = t.S;
+        a.cap = t.cap;
+        a.NW = net->core_threads / 64;
+        a.lif_total = t.lif_total;
+        a.alpha = t.alpha;
+        a.beta = t.beta;
+        a.cc = t.cc;
+        a.theta = t.theta;
+        for (int l = 1; l < t.L; ++l) {
+            if (t.kind[l] != SNN_LIF) continue;
+            const size_t li = (size_t)t.lif[l];
+            BwdLayer& y = a.ly[li];
+            y.n = t.n[l];
+            y.lif_off = t.lif_off[l];
+            y.ring_lds = net->bring_mode[l];
+            y.ring = net->bring[l];
+            for (int p = 0; p < t.P; ++p) {
+                const int q = t.post[p];
+                if (t.pre[p] != l || t.kind[q] != SNN_LIF) continue;
+                y.ws[y.npost] = net->ws + t.woff[p];
+                y.nq[y.npost] = t.n[q];
+                y.qring_lds[y.npost] = net->bring_mode[q] >= 0 ? net->bring_mode[q] : -1;
+                y.qring[y.npost] = net->bring[q];
+                ++y.npost;
+            }
+            for (int k = y.npost; k < 2; ++k) {
+                // any LIF-post projection of the network stands in for unused entries
+                for (int p = 0; p < t.P && !y.ws[k]; ++p) {
+                    const int q = t.post[p];
+                    if (t.pre[p] == 0 || t.kind[q] != SNN_LIF) continue;
+                    y.ws[k] = net->ws + t.woff[p];
+                    y.nq[k] = t.n[q];
+                    y.qring_lds[k] = net->bring_mode[q] >= 0 ? net->bring_mode[q] : -1;
+                    y.qring[k] = net->bring[q];
+                }
+            }
+            y.recI = net->rec_I + li * B * cap;
+            y.recn = net->rec_n + li * B * cap;
+            y.steptab = net->steptab + li * B * (size_t)t.T * SNN_STEP_ROW;
+            y.use_a2 = (l == feed) ? 1 : 0;
+        }
         a.tu = net->tu_lif;
         a.td = net->td_lif;
+        a.A2 = net->A2;
         a.st = net->st;
-        a.acc_off = net->acc_off;
-        TIMED(net, K_BCORE, launch_backward_core(a, net->core_threads, net->lds_core_b, s));
+        a.part_off = net->bpart_off;
+        TIMED(net, K_BCORE,
+              launch_backward_core(a, t.n_lif, net->core_threads, net->lds_core_b, s));
     }
     // spikes grouped by presynaptic neuron: inputs, then every LIF layer
     if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GROUP], s));
@@ -566,17 +676,27 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
     }
     if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GROUP + 1], s));
     GradArgs ga{};
-    ga.t = t;
-    for (int p = 0; p < t.P; ++p) {
-        ga.W[p] = net->W[p];
-        ga.dW[p] = dW[p];
-        ga.dD[p] = dD[p];
-    }
-    ga.slot = net->slot;
+    ga.B = t.B;
+    ga.T = t.T;
+    ga.SB = net->grad_SB;
+    ga.bs = net->grad_bs;
+    ga.lif_total = t.lif_total;
+    ga.C = C;
+    ga.ngroups = net->grad_ngroups;
+    ga.nblk = net->grad_nblk;
+    ga.tau_s = t.tau_s;
+    ga.dt = t.dt;
+    ga.nparams = net->n_params;
     ga.tu_lif = net->tu_lif;
     ga.td_lif = net->td_lif;
     ga.tu_out = net->tu_out;
     ga.td_out = net->td_out;
+    for (int p = 0; p < t.P; ++p) {
+        ga.woff[p] = t.woff[p];
+        ga.dW[p] = dW[p];
+        ga.dD[p] = dD[p];
+    }
+    ga.ws = net->ws;
     ga.g_off[0] = net->in_goff;
     ga.g_step[0] = net->in_gstep;
     for (int l = 1; l < t.L; ++l) {
@@ -585,8 +705,12 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
         ga.g_off[l] = net->rec_goff + li * t.B * (t.maxn + 1);
         ga.g_step[l] = net->rec_gstep + li * t.B * t.cap;
     }
-    for (int p = 0; p <= t.P; ++p) ga.blk[p] = net->blk[p];
-    TIMED(net, K_GRAD, launch_gradients(ga, net->grad_blocks, net->lds_grad, s));
+    for (int g = 0; g < net->grad_ngroups; ++g) ga.grp[g] = net->grad_grp[g];
+    ga.part = net->gpart;
+    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GRAD], s));
+    HIP_TRY(net, launch_gradients(ga, net->grad_J, net->grad_threads, net->lds_grad, s));
+    if (ga.SB > 1) HIP_TRY(net, launch_grad_reduce(ga, t.P, s));
+    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GRAD + 1], s));
     int rc = read_status(net);
     if (rc) return rc;
     rc = collect_times(net, K_RADJ, K_N, t.n_lif > 0);

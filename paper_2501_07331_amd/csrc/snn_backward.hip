@@ -1,0 +1,673 @@
+// Backward-pass kernels of libsnn (gfx950, wave64): the readout adjoint, the
+// LIF adjoint core, spike grouping and the weight / delay gradients (Table 1,
+// backward dynamics and gradient updates; Methods, the lambda_V jump with
+// delayed postsynaptic adjoints and the weight and delay gradients).
+//
+//  readout_adjoint  one workgroup per sample: the LI adjoints over reverse time
+//                   (loss source only), their trajectories, then the readout
+//                   part of the jump sum of every spike of the feeding layer,
+//                   computed in parallel over the spikes.
+//  backward_core    one workgroup per sample runs the LIF adjoints in reverse
+//                   time.  The spikes of every step are known from the
+//                   forward's per-step masks, so the weights and slots of a
+//                   step's spikes, their I- and readout jump parts are
+//                   loaded one step ahead; the per-step chain is then LDS and
+//                   ALU work only: free dynamics, trajectory tile, adjoint
+//                   ring, delayed postsynaptic sums, one barrier, jumps.
+//  group            spikes of every sample grouped by presynaptic neuron.
+//  gradients        workgroup = (post layer, block of J posts, block of
+//                   samples): lanes over the presynaptic neurons of every
+//                   projection into the layer; per sample the J post
+//                   trajectories are staged in LDS and each lane sums, over
+//                   its spikes in step order, lambda_I and w (lambda_I -
+//                   lambda_V) at the delayed arrivals in fp32, then adds the
+//                   sample's sums in fp64.  Sample blocks are reduced in a
+//                   fixed order: no atomics, deterministic.
+#include "snn_device.h"
+
+namespace {
+
+// ------------------------------------------------------------------ readout adjoint
+
+// Lanes k < C: lambda_I <- beta lambda_I + c lambda_V, lambda_V <- alpha
+// lambda_V (old lambda_V in both), then the step's loss source; the "+"
+// values before the source are the trajectory.  Then every thread takes
+// spikes (n, i) of the feeding LIF layer: A2 = sum_k w_ik (lambda_V -
+// lambda_I)_k at step n + slot_ik, fp64 over k ascending.
+__global__ void __launch_bounds__(1024) readout_adjoint_kernel(ReadoutBwdArgs a) {
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const int C = a.C, T = a.T;
+    lds_f32* tab = (lds_f32*)smem;                                // [T][C] lambda_I - lambda_V
+    if (tid < C) {
+        const float srcv = a.src[(size_t)b * C + tid];
+        const int nst = a.nstar[(size_t)b * C + tid];
+        global_f32* tu = (global_f32*)(a.tu + (size_t)b * T * C + tid);
+        global_f32* td = (global_f32*)(a.td + (size_t)b * T * C + tid);
+        float lv = 0.0f, lI = 0.0f;
+        for (int n = T - 1; n >= 0; --n) {
+            if (n <= T - 2) {
+                const float v = lv;
+                lI = __fadd_rn(__fmul_rn(a.beta, lI), __fmul_rn(a.cc, v));
+                lv = __fmul_rn(a.alpha, v);
+            }
+            const float d = __fsub_rn(lI, lv);
+            tu[(size_t)n * C] = lI;
+            td[(size_t)n * C] = d;
+            if (a.tab_lds) tab[n * C + tid] = d;
+            if (a.loss == SNN_LOSS_CE_SUM || nst == n) lv = __fsub_rn(lv, srcv);
+        }
+    }
+    if (!a.rec_n) return;
+    __syncthreads();
+    const int cnt = a.rec_cnt[b];
+    const size_t base = (size_t)b * a.cap;
+    const float* tdb = a.td + (size_t)b * T * C;
+    for (int r = tid; r < cnt; r += blockDim.x) {
+        const int i = a.rec_n[base + r], n = a.rec_s[base + r];
+        const uint2* wsr = a.ws + (size_t)i * C;
+        double acc = 0.0;
+        for (int k = 0; k < C; ++k) {
+            const uint2 e = wsr[k];
+            const int m = n + (int)e.y;
+            if (m <= T - 1) {
+                const float d = a.tab_lds ? (float)tab[m * C + k] : tdb[(size_t)m * C + k];
+                acc -= (double)__fmul_rn(__uint_as_float(e.x), d);
+            }
+        }
+        a.A2[base + r] = acc;
+    }
+}
+
+// ------------------------------------------------------------------ backward core
+
+// Row sums of four fp64 values per lane (a transposed butterfly within each
+// 16-lane row: xor 1 and xor 2 exchange half of the values, xor 4 and xor 8
+// the last one).  Afterwards lane row*16 + k, k < 4, holds the sum over the
+// row of v[2 (k & 1) + (k >> 1)].
+__device__ __forceinline__ double row_sum4(const double (&v)[4], int lane) {
+    const bool b0 = lane & 1, b1 = lane & 2, b2 = lane & 4;
+    double u[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const double send = b0 ? v[k] : v[k + 2];
+        const double keep = b0 ? v[k + 2] : v[k];
+        u[k] = keep + dpp_f64<0xB1>(send);             // quad_perm [1,0,3,2]: xor 1
+    }
+    const double send = b1 ? u[0] : u[1];
+    const double keep = b1 ? u[1] : u[0];
+    double x = keep + dpp_f64<0x4E>(send);             // quad_perm [2,3,0,1]: xor 2
+    const double up = dpp_f64<0x104>(x);               // row_shl:4, from lane + 4
+    const double dn = dpp_f64<0x114>(x);               // row_shr:4, from lane - 4
+    x += b2 ? dn : up;
+    x += dpp_f64<0x128>(x);                            // row_ror:8: xor 8
+    return x;
+}
+
+// Loads in flight for the steps after the one being processed: the spike
+// table row of step n - 1, and for step n everything the delayed sums and
+// jumps need.  Spikes beyond KP in a step are loaded when they are processed.
+template <int NL, int KP, int NPA>
+struct BwdState {
+    int cnt2[NL], ri2[NL];        // step n - 1: spikes, record index of the first
+    int id2[NL][KP];              //   first KP spiking neurons (raw; valid for q < cnt2)
+    int cnt3[NL], ri3[NL];        // step n
+    int id3[NL][KP];
+    uint2 ws[NL][NPA][KP];        //   (weight bits, slot) of the LIF-post projections, this lane's post
+    int mine[NL];                 //   1 + position of this lane's neuron among id3[0 .. KP), 0: none
+    float I[NL];                  //   I- and readout jump part of this lane's spike (raw)
+    double A2[NL];
+};
+
+// s_waitcnt vmcnt(0), expcnt and lgkmcnt left at their maximum (gfx9 encoding)
+constexpr int kWaitVm0 = 0x0F70;
+
+template <int MAXT, int NL, int KP, int NP, bool RL>
+struct BwdCore {
+    static constexpr int NPA = NP > 0 ? NP : 1;
+    static constexpr int ROW4 = (2 + KP + 3) / 4;      // int4 loads of a spike-table row
+    typedef BwdState<NL, KP, NPA> State;
+
+    // Spike-table row of step x: count, record index, first KP neurons.
+    static __device__ __forceinline__ void load_row(const BwdLayer& y, int b, int T, int x, int& cnt,
+                                                    int& ri, int (&ids)[KP]) {
+        const int4* rp = reinterpret_cast<const int4*>(y.steptab + ((size_t)b * T + x) * SNN_STEP_ROW);
+        int v[ROW4 * 4];
+#pragma unroll
+        for (int k = 0; k < ROW4; ++k) {
+            const int4 e = rp[k];
+            v[4 * k + 0] = e.x;
+            v[4 * k + 1] = e.y;
+            v[4 * k + 2] = e.z;
+            v[4 * k + 3] = e.w;
+        }
+        cnt = v[0];
+        ri = v[1];
+#pragma unroll
+        for (int q = 0; q < KP; ++q) ids[q] = v[2 + q];
+    }
+
+    // Weights, slots, own position, I- and A2 of a step's spikes ids[0 .. KP)
+    // (valid for q < cnt; record index of ids[0] is ri + r0).  Only the
+    // chunks of 4 that hold spikes are loaded; ids are made uniform so that
+    // a row's address is scalar and the lane adds its column.
+    static __device__ __forceinline__ void load_step(const CoreBwdArgs& a, int b, int tid, int l,
+                                                     int ri, int cnt, const int (&ids)[KP], int r0,
+                                                     uint2 (&ws)[NPA][KP], int& mine, float& I,
+                                                     double& A2) {
+        const BwdLayer& y = a.ly[l];
+        int idc[KP];
+#pragma unroll
+        for (int q = 0; q < KP; ++q)
+            idc[q] = (q < cnt) ? min(max(__builtin_amdgcn_readfirstlane(ids[q]), 0), y.n - 1) : 0;
+        mine = 0;
+#pragma unroll
+        for (int q0 = 0; q0 < KP; q0 += 4) {
+            if (cnt <= q0) break;
+#pragma unroll
+            for (int pp = 0; pp < NP; ++pp) {
+                const int nq = y.nq[pp];
+                const unsigned col8 = (unsigned)min(tid, nq - 1) * 8u;
+#pragma unroll
+                for (int q = q0; q < q0 + 4; ++q) {
+                    const char* row = reinterpret_cast<const char*>(y.ws[pp] + (size_t)idc[q] * nq);
+                    ws[pp][q] = *reinterpret_cast<const uint2*>(row + col8);
+                }
+            }
+#pragma unroll
+            for (int q = q0; q < q0 + 4; ++q)
+                if (q < cnt && idc[q] == tid) mine = q + 1;
+        }
+        if (mine) {
+            const size_t r = (size_t)b * a.cap + (ri + r0 + mine - 1);
+            I = y.recI[r];
+            A2 = a.A2[r];
+        }
+    }
+
+    // Issue the loads of B from A (processing step n).
+    static __device__ __forceinline__ void advance(const CoreBwdArgs& a, int b, int tid, int n,
+                                                   const State& A, State& B) {
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            load_row(a.ly[l], b, a.T, max(n - 2, 0), B.cnt2[l], B.ri2[l], B.id2[l]);
+            B.cnt3[l] = A.cnt2[l];
+            B.ri3[l] = A.ri2[l];
+#pragma unroll
+            for (int q = 0; q < KP; ++q) B.id3[l][q] = A.id2[l][q];
+            load_step(a, b, tid, l, A.ri2[l], A.cnt2[l], A.id2[l], 0, B.ws[l], B.mine[l], B.I[l],
+                      B.A2[l]);
+        }
+    }
+
+    // Delayed postsynaptic sums of spikes ids[q0 .. q0 + 4) (valid for q < cnt)
+    // of layer l, reduced per 16-lane row into part_l[q][wave * 4 + row].
+    static __device__ __forceinline__ void gather4(const CoreBwdArgs& a, int b, int tid, int n,
+                                                   int n_mod, int l, int q0, int cnt,
+                                                   const int (&ids)[KP], const uint2 (&ws)[NPA][KP],
+                                                   double* part_l) {
+        const BwdLayer& y = a.ly[l];
+        const int lane = tid & 63, wave = tid >> 6;
+        float* lds = reinterpret_cast<float*>(smem);
+        double v[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int q = q0 + k;
+            v[k] = 0.0;
+#pragma unroll
+            for (int pp = 0; pp < NP; ++pp) {
+                const int nq = y.nq[pp];
+                const int sq = (int)ws[pp][q].y;
+                int row = n_mod + sq;
+                row = (row >= a.S) ? row - a.S : row;
+                const bool ok = pp < y.npost && q < cnt && tid < nq && n + sq <= a.T - 1;
+                float d;
+                if (RL)
+                    d = ((lds_f32*)(lds + y.qring_lds[pp]))[(ok ? row : 0) * nq + (ok ? tid : 0)];
+                else
+                    d = ((global_f32*)(y.qring[pp] + ((size_t)b * a.S + (ok ? row : 0)) * nq))[ok ? tid : 0];
+                v[k] -= ok ? (double)__fmul_rn(__uint_as_float(ws[pp][q].x), d) : 0.0;
+            }
+        }
+        const double x = row_sum4(v, lane);
+        const int k = lane & 15;
+        if (k < 4) part_l[(size_t)(q0 + 2 * (k & 1) + (k >> 1)) * (4 * a.NW) + wave * 4 + (lane >> 4)] = x;
+    }
+
+    static __device__ __forceinline__ void gather(const CoreBwdArgs& a, int b, int tid, int n,
+                                                  int n_mod, int l, int cnt, const int (&ids)[KP],
+                                                  const uint2 (&ws)[NPA][KP], double* part_l) {
+#pragma unroll
+        for (int q0 = 0; q0 < KP; q0 += 4)
+            if (cnt > q0) gather4(a, b, tid, n, n_mod, l, q0, cnt, ids, ws, part_l);
+    }
+
+    // The lambda_V jump of this lane's spike at position q of a round.
+    static __device__ __forceinline__ void jump(const CoreBwdArgs& a, const double* part_l, int q,
+                                                float I, double A2, float& lv,
+                                                unsigned long long& deg) {
+        double A = A2;
+        if (NP > 0) {
+            const double* pq = part_l + (size_t)q * (4 * a.NW);
+            double Ap = 0.0;
+            for (int i = 0; i < 4 * a.NW; ++i) Ap += pq[i];
+            A += Ap;
+        }
+        const float den = __fsub_rn(I, a.theta);
+        if (den > 0.0f) {
+            const float D = (float)(((double)a.theta * (double)lv + A) / (double)den);
+            lv = __fadd_rn(lv, D);
+        } else {
+            ++deg;
+        }
+    }
+
+    struct Lane {
+        float lv[NL], lI[NL];
+        unsigned long long deg;
+        int rnd;
+    };
+
+    // One reverse-time step n with the loads of A, issuing those of B.
+    static __device__ __forceinline__ void step(const CoreBwdArgs& a, int b, int tid, int n,
+                                                const State& A, State& B, Lane& L) {
+        const int T = a.T, S = a.S, LT = a.lif_total;
+        const int n_mod = n % S;
+        float* lds = reinterpret_cast<float*>(smem);
+        double* part = reinterpret_cast<double*>(smem + a.part_off);   // [2][NL][KP][4 NW]
+
+        // the loads issued one step ago (A) have landed: wait for them once,
+        // here, so that no later use waits for this step's loads
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        advance(a, b, tid, n, A, B);
+
+        // ---- adjoint free dynamics, trajectory, adjoint ring
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            const BwdLayer& y = a.ly[l];
+            if (tid >= y.n) continue;
+            if (n <= T - 2) {
+                const float v = L.lv[l];
+                L.lI[l] = __fadd_rn(__fmul_rn(a.beta, L.lI[l]), __fmul_rn(a.cc, v));
+                L.lv[l] = __fmul_rn(a.alpha, v);
+            }
+            const float d = __fsub_rn(L.lI[l], L.lv[l]);
+            const size_t o = ((size_t)b * T + n) * LT + y.lif_off + tid;
+            a.tu[o] = L.lI[l];
+            a.td[o] = d;
+            if (y.ring_lds == -2) continue;
+            if (RL)
+                ((lds_f32*)(lds + y.ring_lds))[n_mod * y.n + tid] = d;
+            else
+                ((global_f32*)(y.ring + ((size_t)b * S + n_mod) * y.n))[tid] = d;
+        }
+
+        // ---- round 0: the first KP spikes of every layer, prefetched
+        {
+            const int pb = L.rnd & 1;
+            ++L.rnd;
+            if (NP > 0) {
+#pragma unroll
+                for (int l = 0; l < NL; ++l) {
+                    double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
+                    gather(a, b, tid, n, n_mod, l, A.cnt3[l], A.id3[l], A.ws[l], part_l);
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int l = 0; l < NL; ++l) {
+                if (!A.mine[l]) continue;
+                const double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
+                jump(a, part_l, A.mine[l] - 1, A.I[l], a.ly[l].use_a2 ? A.A2[l] : 0.0, L.lv[l], L.deg);
+            }
+        }
+        // ---- further rounds when a step has more than KP spikes
+        int rounds = 1;
+#pragma unroll
+        for (int l = 0; l < NL; ++l) rounds = max(rounds, (A.cnt3[l] + KP - 1) / KP);
+        for (int r = 1; r < rounds; ++r) {
+            const int pb = L.rnd & 1;
+            ++L.rnd;
+            int mine[NL];
+            float I[NL];
+            double A2[NL];
+#pragma unroll
+            for (int l = 0; l < NL; ++l) {
+                const BwdLayer& y = a.ly[l];
+                const int cnt = A.cnt3[l] - r * KP;          // spikes left from this round on
+                int ids[KP];
+                const int capm = max(a.cap - 1, 0);
+#pragma unroll
+                for (int q = 0; q < KP; ++q)
+                    ids[q] = y.recn[(size_t)b * a.cap + min(max(A.ri3[l] + r * KP + q, 0), capm)];
+                uint2 ws[NPA][KP];
+                load_step(a, b, tid, l, A.ri3[l], cnt, ids, r * KP, ws, mine[l], I[l], A2[l]);
+                double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
+                if (NP > 0) gather(a, b, tid, n, n_mod, l, cnt, ids, ws, part_l);
+            }
+            __syncthreads();
+#pragma unroll
+            for (int l = 0; l < NL; ++l) {
+                if (!mine[l]) continue;
+                const double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
+                jump(a, part_l, mine[l] - 1, I[l], a.ly[l].use_a2 ? A2[l] : 0.0, L.lv[l], L.deg);
+            }
+        }
+    }
+
+    static __device__ void run(const CoreBwdArgs& a) {
+        const int b = blockIdx.x, tid = threadIdx.x;
+        const int T = a.T;
+        Lane L;
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            L.lv[l] = 0.0f;
+            L.lI[l] = 0.0f;
+        }
+        L.deg = 0;
+        L.rnd = 0;
+        State A, B;
+        // step T - 1's data and step T - 2's table row, before the loop
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            load_row(a.ly[l], b, T, T - 1, A.cnt3[l], A.ri3[l], A.id3[l]);
+            load_row(a.ly[l], b, T, max(T - 2, 0), A.cnt2[l], A.ri2[l], A.id2[l]);
+            load_step(a, b, tid, l, A.ri3[l], A.cnt3[l], A.id3[l], 0, A.ws[l], A.mine[l], A.I[l],
+                      A.A2[l]);
+        }
+        int n = T - 1;
+        for (; n >= 1; n -= 2) {
+            step(a, b, tid, n, A, B, L);
+            step(a, b, tid, n - 1, B, A, L);
+        }
+        if (n == 0) step(a, b, tid, 0, A, B, L);
+        if (L.deg) atomicAdd(&a.st->degenerate, L.deg);
+    }
+};
+
+// RL: every adjoint ring lives in LDS (else every one in HBM).
+template <int MAXT, int NL, int KP, int NP, bool RL>
+__global__ void __launch_bounds__(MAXT) backward_core_kernel(CoreBwdArgs a) {
+    BwdCore<MAXT, NL, KP, NP, RL>::run(a);
+}
+
+// ------------------------------------------------------------------ grouping
+
+// One workgroup per sample: counting sort of the sample's spikes by
+// presynaptic neuron (LDS histogram), then each neuron's steps sorted.
+__global__ void __launch_bounds__(1024) group_kernel(GroupArgs a) {
+    if (a.st->bad_input) return;
+    const int b = blockIdx.x, tid = threadIdx.x, nt = blockDim.x;
+    const int start = a.cnt ? b * a.off_stride : a.off[b];
+    const int end = a.cnt ? start + a.cnt[b] : a.end[b + 1];
+    int* h = reinterpret_cast<int*>(smem);        // [n + 1] counts, then cursors
+    int* part = h + a.n + 1;                      // [nt] block scan
+    for (int i = tid; i <= a.n; i += nt) h[i] = 0;
+    __syncthreads();
+    for (int e = start + tid; e < end; e += nt) atomicAdd(&h[a.neuron[e]], 1);
+    __syncthreads();
+    // exclusive scan of h[0 .. n): thread tid scans a contiguous segment
+    const int seg = (a.n + nt - 1) / nt;
+    const int i0 = min(tid * seg, a.n), i1 = min(i0 + seg, a.n);
+    int s = 0;
+    for (int i = i0; i < i1; ++i) s += h[i];
+    part[tid] = s;
+    __syncthreads();
+    if (tid == 0) {
+        int run = 0;
+        for (int w = 0; w < nt; ++w) {
+            const int v = part[w];
+            part[w] = run;
+            run += v;
+        }
+    }
+    __syncthreads();
+    int run = part[tid];
+    int* goff = a.g_off + (size_t)b * (a.n + 1);
+    for (int i = i0; i < i1; ++i) {
+        const int v = h[i];
+        h[i] = run;
+        goff[i] = start + run;
+        run += v;
+    }
+    if (tid == 0) goff[a.n] = end;
+    __syncthreads();
+    for (int e = start + tid; e < end; e += nt) {
+        const int pos = atomicAdd(&h[a.neuron[e]], 1);
+        a.g_step[start + pos] = a.step[e];
+    }
+    __syncthreads();
+    for (int i = tid; i < a.n; i += nt) {
+        const int lo = goff[i], hi = goff[i + 1];
+        for (int x = lo + 1; x < hi; ++x) {
+            const int v = a.g_step[x];
+            int y = x - 1;
+            while (y >= lo && a.g_step[y] > v) {
+                a.g_step[y + 1] = a.g_step[y];
+                --y;
+            }
+            a.g_step[y + 1] = v;
+        }
+    }
+}
+
+// ------------------------------------------------------------------ gradients
+
+// dL/dw_ij = -tau_s sum_spikes lambda_I,j(t + d_ij) and dL/dd_ij = -w_ij
+// sum_spikes (lambda_I - lambda_V)_j(t + d_ij), per step of delay (x dt).
+//
+// Workgroups come in units of four J-post blocks that share 128-byte lines of
+// the [B][T][N] trajectories; a unit's four blocks have indices 8 apart, so
+// with round-robin dispatch over the 8 XCDs they run on one XCD and share its
+// L2.
+template <int J>
+__global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
+    const int tid = threadIdx.x, nt = blockDim.x;
+    int g = 0;
+    while (g + 1 < a.ngroups && (int)blockIdx.x >= a.grp[g + 1].blk0) ++g;
+    const GradGroup& G = a.grp[g];
+    const int local = (int)blockIdx.x - G.blk0;
+    const int unit = (local / 32) * 8 + (local % 8), u = (local % 32) / 8;
+    const int LG = (G.jb + 3) / 4;
+    if (unit >= LG * a.SB) return;
+    const int jb = (unit / a.SB) * 4 + u, sb = unit % a.SB;
+    if (jb >= G.jb) return;
+    const int nq = G.nq, j0 = jb * J, nj = min(J, nq - j0);
+    const int T = a.T;
+    float2* st = reinterpret_cast<float2*>(smem);              // [T][J]
+    const float* tu = G.out ? a.tu_out : a.tu_lif;
+    const float* td = G.out ? a.td_out : a.td_lif;
+    const int LN = G.out ? a.C : a.lif_total;
+    const int vtot = G.npre[0] + (G.np > 1 ? G.npre[1] : 0);
+    const int b0 = sb * a.bs, b1 = min(a.B, b0 + a.bs);
+    for (int v0 = 0; v0 < vtot; v0 += nt) {
+        const int v = v0 + tid;
+        const bool live = v < vtot;
+        const int pi = (live && v >= G.npre[0]) ? 1 : 0;
+        const int i = v - (pi ? G.npre[0] : 0);
+        const int p = G.p[pi], pre = G.pre[pi], npre = G.npre[pi];
+        float w[J];
+        int s[J];
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) {
+            w[jj] = 0.0f;
+            s[jj] = T;                                         // never arrives
+            if (live && jj < nj) {
+                const uint2 e = a.ws[a.woff[p] + (size_t)i * nq + j0 + jj];
+                w[jj] = __uint_as_float(e.x);
+                s[jj] = (int)e.y;
+            }
+        }
+        double su[J], sd[J];
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) {
+            su[jj] = 0.0;
+            sd[jj] = 0.0;
+        }
+        for (int b = b0; b < b1; ++b) {
+            __syncthreads();
+            const size_t base = (size_t)b * T * LN + G.off + j0;
+            for (int e = tid; e < T * J; e += nt) {
+                const int m = e / J, jj = e % J;
+                float2 x = make_float2(0.0f, 0.0f);
+                if (jj < nj) x = make_float2(tu[base + (size_t)m * LN + jj], td[base + (size_t)m * LN + jj]);
+                st[e] = x;
+            }
+            __syncthreads();
+            if (!live) continue;
+            const int* go = a.g_off[pre] + (size_t)b * (npre + 1) + i;
+            const int lo = go[0], hi = go[1];
+            const int* gs = a.g_step[pre];
+            float pu[J], pd[J];
+#pragma unroll
+            for (int jj = 0; jj < J; ++jj) {
+                pu[jj] = 0.0f;
+                pd[jj] = 0.0f;
+            }
+            for (int x = lo; x < hi; x += 4) {
+                int nn[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) nn[k] = (x + k < hi) ? gs[x + k] : T;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+#pragma unroll
+                    for (int jj = 0; jj < J; ++jj) {
+                        const int m = nn[k] + s[jj];
+                        if (m <= T - 1) {
+                            const float2 ud = st[m * J + jj];
+                            pu[jj] = __fadd_rn(pu[jj], ud.x);
+                            pd[jj] = __fadd_rn(pd[jj], __fmul_rn(w[jj], ud.y));
+                        }
+                    }
+                }
+            }
+#pragma unroll
+            for (int jj = 0; jj < J; ++jj) {
+                su[jj] += (double)pu[jj];
+                sd[jj] += (double)pd[jj];
+            }
+        }
+        if (!live) continue;
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) {
+            if (jj >= nj) continue;
+            const size_t kk = (size_t)i * nq + j0 + jj;
+            if (a.SB == 1) {
+                a.dW[p][kk] = (float)(-(double)a.tau_s * su[jj]);
+                a.dD[p][kk] = (float)(-(double)a.dt * sd[jj]);
+            } else {
+                const size_t gi = (size_t)a.woff[p] + kk;
+                a.part[((size_t)sb * 2 + 0) * a.nparams + gi] = su[jj];
+                a.part[((size_t)sb * 2 + 1) * a.nparams + gi] = sd[jj];
+            }
+        }
+    }
+}
+
+// Sample-block partial sums, added in block order.
+__global__ void grad_reduce_kernel(GradArgs a, int P) {
+    const long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (g >= a.nparams) return;
+    int p = 0;
+    while (p + 1 < P && g >= a.woff[p + 1]) ++p;
+    double su = 0.0, sd = 0.0;
+    for (int sb = 0; sb < a.SB; ++sb) {
+        su += a.part[((size_t)sb * 2 + 0) * a.nparams + g];
+        sd += a.part[((size_t)sb * 2 + 1) * a.nparams + g];
+    }
+    const long long kk = g - a.woff[p];
+    a.dW[p][kk] = (float)(-(double)a.tau_s * su);
+    a.dD[p][kk] = (float)(-(double)a.dt * sd);
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------ launchers
+
+hipError_t launch_readout_adjoint(const ReadoutBwdArgs& a, int threads, size_t lds, hipStream_t s) {
+    hipLaunchKernelGGL(readout_adjoint_kernel, dim3(a.B), dim3(threads), lds, s, a);
+    return hipGetLastError();
+}
+
+template <int MAXT, int NL, int NP>
+static void launch_core3(const CoreBwdArgs& a, bool rl, int threads, size_t lds, hipStream_t s) {
+    constexpr int KP = (NL == 1) ? 16 : 4;
+    if (rl)
+        hipLaunchKernelGGL((backward_core_kernel<MAXT, NL, KP, NP, true>), dim3(a.B), dim3(threads),
+                           lds, s, a);
+    else
+        hipLaunchKernelGGL((backward_core_kernel<MAXT, NL, KP, NP, false>), dim3(a.B), dim3(threads),
+                           lds, s, a);
+}
+
+template <int MAXT>
+static bool launch_core_t(const CoreBwdArgs& a, int n_lif, int np, bool rl, int threads, size_t lds,
+                          hipStream_t s) {
+    switch (n_lif * 4 + np) {
+        case 4 + 0: launch_core3<MAXT, 1, 0>(a, rl, threads, lds, s); return true;
+        case 4 + 1: launch_core3<MAXT, 1, 1>(a, rl, threads, lds, s); return true;
+        case 8 + 1: launch_core3<MAXT, 2, 1>(a, rl, threads, lds, s); return true;
+        case 8 + 2: launch_core3<MAXT, 2, 2>(a, rl, threads, lds, s); return true;
+        case 12 + 1: launch_core3<MAXT, 3, 1>(a, rl, threads, lds, s); return true;
+        case 12 + 2: launch_core3<MAXT, 3, 2>(a, rl, threads, lds, s); return true;
+        case 16 + 1: launch_core3<MAXT, 4, 1>(a, rl, threads, lds, s); return true;
+        case 16 + 2: launch_core3<MAXT, 4, 2>(a, rl, threads, lds, s); return true;
+        default: return false;
+    }
+}
+
+hipError_t launch_backward_core(const CoreBwdArgs& a, int n_lif, int threads, size_t lds,
+                                hipStream_t s) {
+    if (n_lif < 1 || n_lif > SNN_MAX_LIF || threads != 64 * a.NW) return hipErrorInvalidValue;
+    int np = 0;
+    bool rl = true;
+    for (int l = 0; l < n_lif; ++l) {
+        np = max(np, a.ly[l].npost);
+        if (a.ly[l].ring_lds == -1) rl = false;
+        for (int pp = 0; pp < a.ly[l].npost; ++pp)
+            if (a.ly[l].qring_lds[pp] < 0) rl = false;
+    }
+    const bool ok = (threads <= 256) ? launch_core_t<256>(a, n_lif, np, rl, threads, lds, s)
+                                     : launch_core_t<1024>(a, n_lif, np, rl, threads, lds, s);
+    if (!ok) return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+hipError_t launch_group(const GroupArgs& a, int B, hipStream_t s) {
+    const size_t lds = sizeof(int) * ((size_t)a.n + 1 + 1024);
+    hipLaunchKernelGGL(group_kernel, dim3(B), dim3(1024), lds, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_gradients(const GradArgs& a, int J, int threads, size_t lds, hipStream_t s) {
+    if (J == 8)
+        hipLaunchKernelGGL(gradients_kernel<8>, dim3(a.nblk), dim3(threads), lds, s, a);
+    else if (J == 1)
+        hipLaunchKernelGGL(gradients_kernel<1>, dim3(a.nblk), dim3(threads), lds, s, a);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+hipError_t launch_grad_reduce(const GradArgs& a, int P, hipStream_t s) {
+    hipLaunchKernelGGL(grad_reduce_kernel, dim3(grid_for(a.nparams, 256)), dim3(256), 0, s, a, P);
+    return hipGetLastError();
+}
+
+#define CORE_FNS2(M, R)                                                                          \
+    (const void*)backward_core_kernel<M, 1, 16, 0, R>, (const void*)backward_core_kernel<M, 1, 16, 1, R>, \
+    (const void*)backward_core_kernel<M, 2, 4, 1, R>, (const void*)backward_core_kernel<M, 2, 4, 2, R>, \
+    (const void*)backward_core_kernel<M, 3, 4, 1, R>, (const void*)backward_core_kernel<M, 3, 4, 2, R>, \
+    (const void*)backward_core_kernel<M, 4, 4, 1, R>, (const void*)backward_core_kernel<M, 4, 4, 2, R>
+#define CORE_FNS(M) CORE_FNS2(M, true), CORE_FNS2(M, false)
+
+hipError_t set_backward_lds_limits(size_t bytes) {
+    const void* fns[] = {(const void*)readout_adjoint_kernel, CORE_FNS(256), CORE_FNS(1024),
+                         (const void*)group_kernel, (const void*)gradients_kernel<8>,
+                         (const void*)gradients_kernel<1>};
+    for (const void* f : fns) {
+        const hipError_t e =
+            hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}

@@ -7,7 +7,14 @@
 #include "snn.h"
 
 #define SNN_MAXP (2 * SNN_MAX_LAYERS)
+#define SNN_MAX_LIF (SNN_MAX_LAYERS - 2)  // LIF layers are 1 .. L-2
 #define SNN_MAX_INPUT 16384          // input neurons (per-sample spike grouping in LDS)
+
+// Per-step spike table of a LIF layer, one row per (sample, step):
+// [spikes at the step, record index of its first spike, first SNN_STEP_IDS
+// spiking neurons ascending, padding]; entries past the count are stale.
+#define SNN_STEP_IDS 16
+#define SNN_STEP_ROW 20
 
 // Device status word, one per handle.
 struct DevStatus {
@@ -66,6 +73,7 @@ struct CoreFwdArgs {
     float* rec_I;                      // [n_lif][B][cap] I- at the spike
     int* rec_idx;                      // [n_lif][B][T+1] first record of each step
     int* rec_cnt;                      // [n_lif][B] spikes per sample
+    int* steptab;                      // [n_lif][B][T][SNN_STEP_ROW] per-step spike table
     float* Vf;                         // [B][sum n_l] final state
     float* If;
     DevStatus* st;
@@ -85,29 +93,55 @@ struct ReadoutArgs {
     int* nstar;                        // [B][C]
     float* Vf;
     float* If;
-    // backward
-    const float* src;                  // [B][C]
-    float* tu;                         // [B][C][T] lambda_I of the readout
-    float* td;                         // [B][C][T] lambda_I - lambda_V of the readout
     int table_lds;                     // LDS float offset of the [T][C] table, -1: global
-    int red_off;                       // byte offset of the fp64 reduction scratch in LDS
-    double* A2;                        // [B][cap] readout part of each feeding spike's jump sum
     const DevStatus* st;
 };
 
+// Readout adjoint: lambda of the LI layer from its loss source, trajectories,
+// and the readout part of the jump sum of every spike of the feeding layer.
+struct ReadoutBwdArgs {
+    int B, T, C, cap, loss;
+    float alpha, beta, cc;
+    const uint2* ws;                   // [n_feed][C] (weight bits, slot)
+    const int* rec_n;                  // records of the feeding LIF layer [B][cap], or NULL
+    const int* rec_s;
+    const int* rec_cnt;                // [B]
+    const int* nstar;                  // [B][C]
+    const float* src;                  // [B][C]
+    float* tu;                         // [B][T][C] lambda_I
+    float* td;                         // [B][T][C] lambda_I - lambda_V
+    double* A2;                        // [B][cap]
+    int tab_lds;                       // 1: the [T][C] table of td lives in LDS
+};
+
+// One LIF layer as seen by the backward core.
+struct BwdLayer {
+    int n, lif_off;
+    int ring_lds;                      // LDS float offset of the adjoint ring [S][n]; -1 global; -2 none
+    float* ring;                       // global adjoint ring [B][S][n] when ring_lds == -1
+    int npost;                         // LIF-post projections out of this layer: the recurrent
+                                       // one, then the feed-forward one (projection order); the
+                                       // entries past npost repeat a valid projection (loads stay
+                                       // in bounds; their contributions are masked)
+    int nq[2];                         // their post layer's neurons,
+    int qring_lds[2];                  //   adjoint ring (LDS float offset, or -1: global qring)
+    float* qring[2];
+    const uint2* ws[2];                //   (weight bits, slot) [n][nq]
+    const float* recI;                 // [B][cap] I- of the records
+    const int* recn;                   // [B][cap] neuron of the records
+    const int* steptab;                // [B][T][SNN_STEP_ROW] per-step spike table
+    int use_a2;                        // 1: the layer feeds the readout (jump sums get A2)
+};
+
 struct CoreBwdArgs {
-    Topo t;
-    const float* W[SNN_MAXP];
-    const uint8_t* slot;
-    float* ring[SNN_MAX_LAYERS];       // global adjoint rings [B][S][n_l] (layers not in LDS)
-    const int* rec_n;
-    const float* rec_I;
-    const int* rec_idx;
-    const double* A2;                  // readout part of the jump sums of the last LIF layer
-    float* tu;                         // [B][lif_total][T] lambda_I
-    float* td;                         // [B][lif_total][T] lambda_I - lambda_V
+    int B, T, S, cap, NW, lif_total;
+    float alpha, beta, cc, theta;
+    BwdLayer ly[SNN_MAX_LIF];
+    float* tu;                         // [B][T][lif_total] lambda_I
+    float* td;                         // [B][T][lif_total] lambda_I - lambda_V
+    const double* A2;                  // [B][cap] readout part of the jump sums (feeding layer)
     DevStatus* st;
-    int acc_off;                       // byte offset of the fp64 jump sums in LDS
+    int part_off;                      // LDS byte offset of the partial jump sums
 };
 
 // Spikes of each sample grouped by presynaptic neuron, in step order.
@@ -124,38 +158,59 @@ struct GroupArgs {
     const DevStatus* st;
 };
 
-struct GradArgs {
-    Topo t;
-    const float* W[SNN_MAXP];
-    const uint8_t* slot;
-    const float* tu_lif;               // [B][lif_total][T]
-    const float* td_lif;
-    const float* tu_out;               // [B][C][T]
-    const float* td_out;
-    const int* g_off[SNN_MAX_LAYERS];  // per presynaptic layer: [B][n+1]
-    const int* g_step[SNN_MAX_LAYERS];
-    float* dW[SNN_MAXP];
-    float* dD[SNN_MAXP];
-    int blk[SNN_MAXP + 1];             // workgroups of projection p: [blk[p], blk[p+1]) = posts
+// The projections into one post layer, for the gradient pass.
+struct GradGroup {
+    int nq;                            // post neurons
+    int jb;                            // blocks of J posts
+    int units;                         // (4-block line group, sample block) units, rounded up to 8
+    int out;                           // 1: the readout layer (trajectories tu_out / td_out)
+    int off;                           // neuron offset of the layer in its trajectory array
+    int np;                            // projections into the layer (1 or 2), in projection order
+    int p[2];
+    int npre[2];
+    int pre[2];                        // their presynaptic layer
+    int blk0;                          // first workgroup of the group
 };
 
-// Kernel launchers (snn_kernels.hip).
+struct GradArgs {
+    int B, T, SB, bs, lif_total, C, ngroups, nblk;
+    float tau_s, dt;
+    long long nparams;
+    const float* tu_lif;               // [B][T][lif_total]
+    const float* td_lif;
+    const float* tu_out;               // [B][T][C]
+    const float* td_out;
+    const uint2* ws;                   // flat [params] (weight bits, slot)
+    long long woff[SNN_MAXP];
+    const int* g_off[SNN_MAX_LAYERS];  // per presynaptic layer: [B][n+1]
+    const int* g_step[SNN_MAX_LAYERS];
+    GradGroup grp[SNN_MAX_LAYERS];
+    double* part;                      // [SB][2][nparams] per sample block (SB > 1)
+    float* dW[SNN_MAXP];
+    float* dD[SNN_MAXP];
+};
+
+// Kernel launchers (snn_forward.hip, snn_backward.hip).
 hipError_t launch_reset_status(DevStatus* st, hipStream_t s);
 hipError_t launch_validate(const int* off, const int* step, const int* neuron, int nnz, int B, int T,
                            int n_in, const int* labels, int C, DevStatus* st, hipStream_t s);
 hipError_t launch_step_index(const int* off, const int* step, int B, int T, int* idx,
                              const DevStatus* st, hipStream_t s);
-hipError_t launch_round_delays(const float* const* D, const long long* woff, const long long* cnt,
-                               int P, int max_delay, uint8_t* slot, DevStatus* st, hipStream_t s);
+hipError_t launch_round_delays(const float* const* D, const float* const* W, const long long* woff,
+                               const long long* cnt, int P, int max_delay, uint8_t* slot, uint2* ws,
+                               DevStatus* st, hipStream_t s);
 hipError_t launch_input_scan(const InScanArgs& a, size_t lds, hipStream_t s);
 hipError_t launch_forward_core(const CoreFwdArgs& a, int threads, size_t lds, hipStream_t s);
 hipError_t launch_readout_forward(const ReadoutArgs& a, int threads, size_t lds, hipStream_t s);
 hipError_t launch_loss(const float* z, const int* labels, int B, int C, int loss, float rscale,
                        float tau_m, float* loss_out, float* src, const DevStatus* st, hipStream_t s);
-hipError_t launch_readout_adjoint(const ReadoutArgs& a, int threads, size_t lds, hipStream_t s);
-hipError_t launch_backward_core(const CoreBwdArgs& a, int threads, size_t lds, hipStream_t s);
-hipError_t launch_group(const GroupArgs& a, int B, hipStream_t s);
-hipError_t launch_gradients(const GradArgs& a, int blocks, size_t lds, hipStream_t s);
 hipError_t launch_copy_state(const float* src, int stride, int off, int n, int B, float* dst,
                              hipStream_t s);
-hipError_t set_kernel_lds_limits(size_t bytes);
+hipError_t launch_readout_adjoint(const ReadoutBwdArgs& a, int threads, size_t lds, hipStream_t s);
+hipError_t launch_backward_core(const CoreBwdArgs& a, int n_lif, int threads, size_t lds,
+                                hipStream_t s);
+hipError_t launch_group(const GroupArgs& a, int B, hipStream_t s);
+hipError_t launch_gradients(const GradArgs& a, int J, int threads, size_t lds, hipStream_t s);
+hipError_t launch_grad_reduce(const GradArgs& a, int P, hipStream_t s);
+hipError_t set_forward_lds_limits(size_t bytes);
+hipError_t set_backward_lds_limits(size_t bytes);

@@ -14,8 +14,8 @@ tables for the task each stands in for (Yin-Yang for config 2, Braille for
 config 3, SHD for configs 4 and 5: recurrent N(0, 0.02), hidden-to-output
 N(0.02, 0.03), feed-forward hidden-to-hidden N(0.02, 0.03), input std 0.01).
 The means of the feed-forward projections into LIF layers are then calibrated
-once (bisection on the oracle forward over the first 8 samples, see
-``oracle/calibrate.py``) to a mean hidden activity of about 14 spikes per neuron
+once (bisection on the oracle forward over the batch, at most its first 32
+samples for the two-layer 1024-neuron config, see ``oracle/calibrate.py``) to a mean hidden activity of about 14 spikes per neuron
 per sample (the SHD spike-count target of the Results section) or about 1
 (latency-coded config 2); the values live in ``calibration.json``.
 """
