@@ -207,7 +207,8 @@ int snn_get_state(const snn_net* net, int32_t layer, float* V, float* I);
 int snn_get_stats(const snn_net* net, snn_stats* out);
 
 /* Message for the last error on this handle ("" if none); valid until the
- * next call on the handle. */
+ * next call on the handle.  With net NULL: the reason of the last failed
+ * snn_create on the calling thread ("" if none). */
 const char* snn_last_error(const snn_net* net);
 
 /* Release the handle and its device scratch (waits for its stream). */

@@ -137,7 +137,8 @@ class Network:
         rc = self._lib.snn_create(arr, len(layers), tau_m, tau_s, theta, dt, int(max_delay),
                                   C.byref(opts), C.byref(h))
         if rc != SNN_OK:
-            raise SNNError(rc, "snn_create failed")
+            why = self._lib.snn_last_error(None).decode()
+            raise SNNError(rc, "snn_create failed" + (f" ({why})" if why else ""))
         self._h = h
         n = C.c_int32()
         self._check(self._lib.snn_num_projections(h, C.byref(n)))

@@ -26,7 +26,7 @@ struct snn_net {
     int core_threads;           // LIF-core workgroup size
     int read_threads;           // readout workgroup size
     size_t lds_core_f, lds_core_b, lds_scan, lds_read, lds_grad, lds_radj;
-    int mask_off, scan_nb, table_lds;
+    int mask_off, scan_tw, table_lds;
     int bpart_off;              // backward-core LDS plan
     int bring_mode[SNN_MAX_LAYERS];   // adjoint ring of a LIF layer: -2 none, -1 HBM, >= 0 LDS
     int radj_threads, radj_tab;
@@ -123,9 +123,13 @@ static hipError_t dalloc(T** p, size_t count) {
     return hipMalloc((void**)p, count * sizeof(T));
 }
 
+// reason of the last failed snn_create on this thread
+static thread_local char g_create_err[256] = "";
+
 extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m, float tau_s,
                           float theta, float dt, int32_t max_delay, const snn_opts* opts,
                           snn_net** out) {
+    g_create_err[0] = '\0';
     if (!out) return SNN_EINVAL;
     *out = nullptr;
     if (!layers || !opts) return SNN_EINVAL;
@@ -220,17 +224,19 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         if (t.kind[l] == SNN_LIF) maxlif = std::max(maxlif, t.n[l]);
     net->core_threads = std::max(64, ((maxlif + 63) / 64) * 64);
     const int nwaves = net->core_threads / 64;
-    // forward core: LIF->LIF rings (projection order), then the ballot masks
+    // forward core: the delay rings [S+1][n_post] of the LIF->LIF projections
+    // (row S: dummy), all in LDS or all in HBM, then the ballot masks [3][NL][NW]
     {
-        const size_t masks = align16((size_t)2 * t.n_lif * nwaves * sizeof(unsigned long long));
+        const size_t masks = align16((size_t)3 * std::max(t.n_lif, 1) * nwaves * sizeof(unsigned long long));
         size_t used = 0;
         for (int p = 0; p < t.P; ++p) {
             if (t.pre[p] == 0 || t.kind[t.post[p]] != SNN_LIF) continue;
-            const size_t bytes = (size_t)t.S * t.n[t.post[p]] * sizeof(float);
-            if (!hbm && used + bytes + masks <= kLds) {
-                t.fring[p] = (int)(used / sizeof(float));
-                used += bytes;
-            }
+            t.fring[p] = (int)(used / sizeof(float));
+            used += (size_t)(t.S + 1) * t.n[t.post[p]] * sizeof(float);
+        }
+        if (hbm || used + masks > kLds) {
+            used = 0;
+            for (int p = 0; p < t.P; ++p) t.fring[p] = -1;
         }
         net->mask_off = (int)align16(used);
         net->lds_core_f = net->mask_off + masks;
@@ -264,18 +270,13 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         for (int l = 0; l < n_layers; ++l) t.bring[l] = net->bring_mode[l] >= 0 ? net->bring_mode[l] : -1;
         net->lds_core_b = used;
     }
-    // input scan: posts per workgroup so that the ring [S][nb] fits
-    {
-        int nb = (int)(kLds / ((size_t)t.S * sizeof(float)));
-        nb = std::min(256, (nb / 64) * 64);
-        nb = std::min(nb, t.n[1]);
-        net->scan_nb = nb;
-        net->lds_scan = (size_t)t.S * nb * sizeof(float);
-    }
-    // readout forward: arrival table [T][C] in LDS when it fits
+    // input scan: windows of 128 arrival steps (a [128][64] table per wave)
+    net->scan_tw = std::min(128, t.T);
+    net->lds_scan = (size_t)(net->scan_tw + 1) * 64 * sizeof(float);
+    // readout forward: arrival table [T + 1][C] (row T: dummy) in LDS when it fits
     net->read_threads = ((C + 63) / 64) * 64;
     {
-        const size_t tab = align16((size_t)t.T * C * sizeof(float));
+        const size_t tab = align16((size_t)(t.T + 1) * C * sizeof(float));
         if (!hbm && tab <= kLds) {
             net->table_lds = 0;
             net->lds_read = tab;
@@ -345,7 +346,7 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     ALLOC(net->A_in, B * T * t.n[1]);
     for (int p = 0; p < t.P; ++p)
         if (t.pre[p] != 0 && t.kind[t.post[p]] == SNN_LIF && t.fring[p] < 0)
-            ALLOC(net->fring[p], B * t.S * t.n[t.post[p]]);
+            ALLOC(net->fring[p], B * (t.S + 1) * t.n[t.post[p]]);
     for (int l = 1; l < n_layers; ++l)
         if (net->bring_mode[l] == -1) ALLOC(net->bring[l], B * t.S * t.n[l]);
     ALLOC(net->rec_n, nl * B * cap);
@@ -360,7 +361,7 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     ALLOC(net->src, B * C);
     ALLOC(net->Vf, B * so);
     ALLOC(net->If, B * so);
-    if (net->table_lds < 0) ALLOC(net->table, B * T * C);
+    if (net->table_lds < 0) ALLOC(net->table, B * (T + 1) * C);
     ALLOC(net->tu_lif, B * T * t.lif_total);
     ALLOC(net->td_lif, B * T * t.lif_total);
     ALLOC(net->tu_out, B * T * C);
@@ -370,12 +371,27 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     ALLOC(net->in_goff, B * (t.n_in + 1));
     ALLOC(net->st, 1);
 #undef ALLOC
+    const char* what = "device allocation";
+    int bad = -1;   // index of the kernel whose LDS limit was refused
     if (e == hipSuccess) e = hipHostMalloc((void**)&net->st_host, sizeof(DevStatus), hipHostMallocDefault);
-    if (e == hipSuccess) e = set_forward_lds_limits(kLds);
-    if (e == hipSuccess) e = set_backward_lds_limits(kLds);
+    if (e == hipSuccess) {
+        what = "forward LDS limits";
+        e = set_forward_lds_limits(kLds, &bad);
+    }
+    if (e == hipSuccess) {
+        what = "forward core LDS limits";
+        e = set_core_lds_limits(kLds, &bad);
+    }
+    if (e == hipSuccess) {
+        what = "backward LDS limits";
+        e = set_backward_lds_limits(kLds, &bad);
+    }
     net->timing = (opts->flags & SNN_FLAG_TIMING) ? 1 : 0;
+    if (e == hipSuccess) what = "timing events";
     for (int i = 0; i < 2 * K_N && net->timing && e == hipSuccess; ++i) e = hipEventCreate(&net->ev[i]);
     if (e != hipSuccess) {
+        snprintf(g_create_err, sizeof(g_create_err), "snn_create: %s (kernel %d): %s", what, bad,
+                 hipGetErrorString(e));
         const int code = (e == hipErrorOutOfMemory) ? SNN_ENOMEM : SNN_EDEVICE;
         free_all(net);
         free(net);
@@ -455,45 +471,98 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
                                      net->st, s));
 
     InScanArgs sa{};
-    sa.t = t;
-    sa.W0 = W[0];
-    sa.slot0 = net->slot;
+    sa.B = t.B;
+    sa.T = t.T;
+    sa.S = t.S;
+    sa.n_in = t.n_in;
+    sa.n1 = t.n[1];
+    sa.TW = net->scan_tw;
+    sa.ws0 = net->ws;
     sa.in_neuron = in->neuron;
+    sa.in_step = in->step;
     sa.in_idx = net->in_idx;
     sa.A_in = net->A_in;
     sa.st = net->st;
-    sa.nb = net->scan_nb;
     TIMED(net, K_SCAN, launch_input_scan(sa, net->lds_scan, s));
 
     if (t.n_lif > 0) {
         CoreFwdArgs a{};
-        a.t = t;
-        for (int p = 0; p < t.P; ++p) a.W[p] = W[p];
-        a.slot = net->slot;
-        for (int p = 0; p < t.P; ++p) a.ring[p] = net->fring[p];
-        a.A_in = net->A_in;
+        a.B = t.B;
+        a.T = t.T;
+        a.S = t.S;
+        a.cap = t.cap;
+        a.NW = net->core_threads / 64;
+        a.n1 = t.n[1];
+        a.nstate = net->n_state;
+        a.alpha = t.alpha;
+        a.beta = t.beta;
+        a.gamma = t.gamma;
+        a.theta = t.theta;
+        const size_t B = t.B, cap = t.cap;
         for (int l = 1; l < t.L; ++l) {
             if (t.kind[l] != SNN_LIF) continue;
-            a.out_count[l] = records[t.lif[l]].count;
-            a.out_step[l] = records[t.lif[l]].step;
-            a.out_neuron[l] = records[t.lif[l]].neuron;
+            const int li = t.lif[l];
+            FwdLayer& y = a.ly[li];
+            y.n = t.n[l];
+            a.soff[li] = net->st_off[l];
+            // projections into the layer, in projection order
+            for (int p = 0; p < t.P; ++p) {
+                if (t.post[p] != l) continue;
+                const int pre = t.pre[p];
+                y.in_l[y.nin] = (pre == 0) ? -1 : t.lif[pre];
+                y.in_pp[y.nin] = 0;
+                if (pre != 0) {
+                    // position of p among the LIF-post projections of its source layer
+                    int k = 0;
+                    for (int p2 = 0; p2 < p; ++p2)
+                        if (t.pre[p2] == pre && t.kind[t.post[p2]] == SNN_LIF) ++k;
+                    y.in_pp[y.nin] = k;
+                }
+                ++y.nin;
+            }
+            // LIF-post projections out of the layer, in projection order
+            for (int p = 0; p < t.P; ++p) {
+                const int q = t.post[p];
+                if (t.pre[p] != l || t.kind[q] != SNN_LIF) continue;
+                y.nq[y.npost] = t.n[q];
+                y.npre[y.npost] = t.n[l];
+                y.ring_lds[y.npost] = t.fring[p];
+                y.ring[y.npost] = net->fring[p];
+                y.ws[y.npost] = net->ws + t.woff[p];
+                ++y.npost;
+            }
+            for (int k = y.npost; k < 2; ++k) {
+                // any LIF-post projection of the network stands in for unused entries
+                for (int p = 0; p < t.P && !y.ws[k]; ++p) {
+                    const int q = t.post[p];
+                    if (t.pre[p] == 0 || t.kind[q] != SNN_LIF) continue;
+                    y.nq[k] = t.n[q];
+                    y.npre[k] = t.n[t.pre[p]];
+                    y.ring_lds[k] = t.fring[p];
+                    y.ring[k] = net->fring[p];
+                    y.ws[k] = net->ws + t.woff[p];
+                }
+            }
+            y.rec_n = net->rec_n + li * B * cap;
+            y.rec_s = net->rec_s + li * B * cap;
+            y.rec_I = net->rec_I + li * B * cap;
+            y.rec_idx = net->rec_idx + li * B * (size_t)(t.T + 1);
+            y.rec_cnt = net->rec_cnt + li * B;
+            y.steptab = net->steptab + li * B * (size_t)t.T * SNN_STEP_ROW;
+            y.out_count = records[li].count;
+            y.out_step = records[li].step;
+            y.out_neuron = records[li].neuron;
         }
-        a.rec_n = net->rec_n;
-        a.rec_s = net->rec_s;
-        a.rec_I = net->rec_I;
-        a.rec_idx = net->rec_idx;
-        a.rec_cnt = net->rec_cnt;
-        a.steptab = net->steptab;
+        a.A_in = net->A_in;
         a.Vf = net->Vf;
         a.If = net->If;
         a.st = net->st;
         a.mask_off = net->mask_off;
-        TIMED(net, K_CORE, launch_forward_core(a, net->core_threads, net->lds_core_f, s));
+        TIMED(net, K_CORE, launch_forward_core(a, t.n_lif, net->core_threads, net->lds_core_f, s));
     }
     ReadoutArgs r{};
     r.t = t;
-    r.W = W[t.out_p];
-    r.slot = net->slot;
+    r.ws = net->ws + t.woff[t.out_p];
     r.A_in = net->A_in;
     r.rec_n = net->rec_n;
     r.rec_s = net->rec_s;
@@ -738,7 +807,7 @@ extern "C" int snn_get_stats(const snn_net* net, snn_stats* out) {
     return SNN_OK;
 }
 
-extern "C" const char* snn_last_error(const snn_net* net) { return net ? net->err : "NULL handle"; }
+extern "C" const char* snn_last_error(const snn_net* net) { return net ? net->err : g_create_err; }
 
 extern "C" void snn_destroy(snn_net* net) {
     if (!net) return;

@@ -118,9 +118,6 @@ struct BwdState {
     double A2[NL];
 };
 
-// s_waitcnt vmcnt(0), expcnt and lgkmcnt left at their maximum (gfx9 encoding)
-constexpr int kWaitVm0 = 0x0F70;
-
 template <int MAXT, int NL, int KP, int NP, bool RL>
 struct BwdCore {
     static constexpr int NPA = NP > 0 ? NP : 1;
@@ -473,7 +470,7 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
     if (jb >= G.jb) return;
     const int nq = G.nq, j0 = jb * J, nj = min(J, nq - j0);
     const int T = a.T;
-    float2* st = reinterpret_cast<float2*>(smem);              // [T][J]
+    float2* st = reinterpret_cast<float2*>(smem);              // [J][T]: random steps spread banks
     const float* tu = G.out ? a.tu_out : a.tu_lif;
     const float* td = G.out ? a.td_out : a.td_lif;
     const int LN = G.out ? a.C : a.lif_total;
@@ -510,7 +507,7 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
                 const int m = e / J, jj = e % J;
                 float2 x = make_float2(0.0f, 0.0f);
                 if (jj < nj) x = make_float2(tu[base + (size_t)m * LN + jj], td[base + (size_t)m * LN + jj]);
-                st[e] = x;
+                st[jj * T + m] = x;
             }
             __syncthreads();
             if (!live) continue;
@@ -533,7 +530,7 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
                     for (int jj = 0; jj < J; ++jj) {
                         const int m = nn[k] + s[jj];
                         if (m <= T - 1) {
-                            const float2 ud = st[m * J + jj];
+                            const float2 ud = st[jj * T + m];
                             pu[jj] = __fadd_rn(pu[jj], ud.x);
                             pd[jj] = __fadd_rn(pd[jj], __fmul_rn(w[jj], ud.y));
                         }
@@ -660,14 +657,17 @@ hipError_t launch_grad_reduce(const GradArgs& a, int P, hipStream_t s) {
     (const void*)backward_core_kernel<M, 4, 4, 1, R>, (const void*)backward_core_kernel<M, 4, 4, 2, R>
 #define CORE_FNS(M) CORE_FNS2(M, true), CORE_FNS2(M, false)
 
-hipError_t set_backward_lds_limits(size_t bytes) {
+hipError_t set_backward_lds_limits(size_t bytes, int* bad) {
     const void* fns[] = {(const void*)readout_adjoint_kernel, CORE_FNS(256), CORE_FNS(1024),
                          (const void*)group_kernel, (const void*)gradients_kernel<8>,
                          (const void*)gradients_kernel<1>};
-    for (const void* f : fns) {
+    for (int i = 0; i < (int)(sizeof(fns) / sizeof(fns[0])); ++i) {
         const hipError_t e =
-            hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-        if (e != hipSuccess) return e;
+            hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+        if (e != hipSuccess) {
+            if (bad) *bad = i;
+            return e;
+        }
     }
     return hipSuccess;
 }

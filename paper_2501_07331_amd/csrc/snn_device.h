@@ -153,4 +153,160 @@ __device__ __forceinline__ bool bits_chunk(BitIter& it, int (&ids)[N]) {
     return any;
 }
 
+// The words of a spike-mask row, uniform (NWM >= NW words; the rest zero).
+template <int NWM>
+__device__ __forceinline__ void row_words(const unsigned long long* row, int NW,
+                                          unsigned long long (&m)[NWM]) {
+#pragma unroll
+    for (int w = 0; w < NWM; ++w) m[w] = (w < NW) ? row[w] : 0ull;
+#pragma unroll
+    for (int w = 0; w < NWM; ++w) m[w] = uniform64(m[w]);
+}
+
+// Set bits of a spike-mask row, ascending: skip the first `skip`, return the
+// next N (-1 past the end).  Up to four words the row's words m (uniform, in
+// registers) are walked fully unrolled; longer rows (row: the same words in
+// LDS, NW of them) are walked word by word at run time, which keeps the code
+// small.
+template <int NWM, int N>
+__device__ __forceinline__ void word_ids(const unsigned long long (&m)[NWM],
+                                         const unsigned long long* row, int NW, int skip,
+                                         int (&ids)[N]) {
+    if constexpr (NWM > 4) {
+        BitIter it = bits_begin(row, NW);
+        for (;;) {
+            const int c = __popcll(it.cur);
+            if (c > skip || it.w + 1 >= NW) break;
+            skip -= c;
+            it.cur = uniform64(row[++it.w]);
+        }
+        for (; skip > 0 && it.cur; --skip) it.cur &= it.cur - 1;
+        bits_chunk<N>(it, ids);
+    } else {
+        unsigned long long rem[NWM];
+#pragma unroll
+        for (int w = 0; w < NWM; ++w) rem[w] = m[w];
+        for (int k = 0; k < skip; ++k) {
+            bool done = false;
+#pragma unroll
+            for (int w = 0; w < NWM; ++w) {
+                if (!done && rem[w]) {
+                    rem[w] &= rem[w] - 1;
+                    done = true;
+                }
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < N; ++q) {
+            int id = -1;
+#pragma unroll
+            for (int w = 0; w < NWM; ++w) {
+                if (id < 0 && rem[w]) {
+                    id = w * 64 + __builtin_ctzll(rem[w]);
+                    rem[w] &= rem[w] - 1;
+                }
+            }
+            ids[q] = id;
+        }
+    }
+}
+
+// s_waitcnt vmcnt(0), expcnt and lgkmcnt left at their maximum (gfx9 encoding)
+constexpr int kWaitVm0 = 0x0F70;
+
+// Adds w[k] to cell row[k] of one lane's column (cell r at col[r * stride])
+// for k = 0 .. KB-1 in order, where every row is valid (out-of-range entries
+// point at a dummy row that is never read out).  Reads first, equal rows
+// merged in registers, then the writes: the same fp32 result as one
+// read-modify-write per entry in order, without branches.
+template <typename Ptr>
+__device__ __forceinline__ void column_add_all(Ptr col, int stride, const int (&row)[KB],
+                                               const float (&w)[KB]) {
+    float v[KB];
+#pragma unroll
+    for (int k = 0; k < KB; ++k) v[k] = col[row[k] * stride];
+#pragma unroll
+    for (int k = 0; k < KB; ++k) {
+        float base = v[k];
+#pragma unroll
+        for (int j = 0; j < k; ++j) base = (row[j] == row[k]) ? v[j] : base;
+        v[k] = __fadd_rn(base, w[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < KB; ++k) col[row[k] * stride] = v[k];
+}
+
+// Delayed scatter of a sorted event list into a table, one column per lane:
+// for every event e in [e_lo, e_hi) in order (presynaptic neuron ids[e] at
+// step steps[e]), the lane adds w(ids[e], col) to the cell of arrival step
+// m = steps[e] + slot(ids[e], col) when m lies in [m0, m_end): cell
+// tab[(m - m0) * ld] of the lane's column; everything else goes to the dummy
+// row `dummy` (>= m_end - m0) of the column.  ws holds (weight bits, slot)
+// rows of npost entries (ws_bytes in all, the bound of the buffer loads);
+// lanes with live == false add to the dummy row only.
+//
+// Chunks of KB events, software-pipelined in pairs: while a chunk is added,
+// the weight rows of the next chunk and the ids and steps of the next pair
+// of chunks (one event per lane) are in flight.  One wait at each chunk
+// start covers the loads issued a chunk earlier, and the weight registers
+// alternate between the two chunks of a pair, so no register copy waits for
+// a load in flight.  A lane adds a chunk to its own column with one
+// read-modify-write per cell, equal rows merged in registers in event order
+// (fp32 LDS atomics would keep the order too, but are far slower).
+template <typename Ptr>
+__device__ __forceinline__ void scatter_events(const int* ids, const int* steps, int e_lo, int e_hi,
+                                               const uint2* ws, int ws_bytes, int npost, int col,
+                                               bool live, int m0, int m_end, int dummy, Ptr tab,
+                                               int ld) {
+    if (e_hi <= e_lo) return;
+    const int lane = threadIdx.x & 63;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void*)ws, (short)0, ws_bytes,
+                                                                        0x00020000);
+    const int col8 = min(max(col, 0), npost - 1) * 8;
+    const int row8 = npost * 8;
+    const unsigned span = (unsigned)(live ? m_end - m0 : 0);   // dead lanes: all to the dummy
+    auto load_pair = [&](int e0, int& id, int& st) {  // lane q < 2 KB: event e0 + q
+        const int e = min(e0 + (lane & (2 * KB - 1)), e_hi - 1);
+        id = ids[e];
+        st = steps[e];
+    };
+    auto load_ws = [&](int id_v, int qoff, uint2 (&w)[KB]) {
+#pragma unroll
+        for (int q = 0; q < KB; ++q) {
+            const int id = __builtin_amdgcn_readlane(id_v, qoff + q);
+            const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, col8, id * row8, 0);
+            w[q] = make_uint2((unsigned)v[0], (unsigned)v[1]);
+        }
+    };
+    auto add = [&](int e0, int st_v, int qoff, const uint2 (&w)[KB]) {
+        const int nv = e_hi - e0;                      // valid events from e0 on (uniform)
+        int row[KB];
+        float wv[KB];
+#pragma unroll
+        for (int q = 0; q < KB; ++q) {
+            const int d = __builtin_amdgcn_readlane(st_v, qoff + q) + (int)w[q].y - m0;
+            row[q] = (q < nv && (unsigned)d < span) ? d : dummy;
+            wv[q] = __uint_as_float(w[q].x);
+        }
+        column_add_all(tab, ld, row, wv);
+    };
+    int idA, stA, idB, stB;
+    uint2 w0[KB], w1[KB];
+    load_pair(e_lo, idA, stA);
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);
+    load_ws(idA, 0, w0);
+    for (int e0 = e_lo; e0 < e_hi; e0 += 2 * KB) {
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        load_pair(e0 + 2 * KB, idB, stB);
+        load_ws(idA, KB, w1);                          // second chunk of this pair
+        add(e0, stA, 0, w0);
+        if (e0 + KB >= e_hi) break;
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        load_ws(idB, 0, w0);                           // first chunk of the next pair
+        add(e0 + KB, stA, KB, w1);
+        idA = idB;                                     // landed at the wait above
+        stA = stB;
+    }
+}
+
 }  // namespace

@@ -85,239 +85,39 @@ __global__ void round_delays_kernel(RoundArgs a, uint8_t* slot, uint2* ws, DevSt
 
 // ------------------------------------------------------------------ input scan
 
-// Workgroup (sample b, posts [j0, j0 + nb) of layer 1); lane owns post j.
-__global__ void __launch_bounds__(256) input_scan_kernel(InScanArgs a) {
-    const Topo& t = a.t;
+// Workgroup = (sample b, block of 64 posts of layer 1, window of TW arrival
+// steps), one wave: the input events that can arrive in the window (emitted
+// within S - 1 steps before it, or in it) are added in emission order into
+// an LDS table [TW][64], which then goes out as A_in rows.  No step-by-step
+// dependency: all windows run in parallel.
+__global__ void __launch_bounds__(64) input_scan_kernel(InScanArgs a) {
     if (a.st->bad_input) return;
-    const int n1 = t.n[1], S = t.S, T = t.T, nb = a.nb;
-    const int nblk = (n1 + nb - 1) / nb;
-    const int b = blockIdx.x / nblk, tid = threadIdx.x;
-    const int j = (blockIdx.x % nblk) * nb + tid;
-    const bool live = tid < nb && j < n1;
-    lds_f32* col = (lds_f32*)smem + tid;                      // ring [S][nb]
-    if (live)
-        for (int s = 0; s < S; ++s) col[s * nb] = 0.0f;
+    const int n1 = a.n1, T = a.T, TW = a.TW;
+    const int nblk = (n1 + 63) / 64, nwin = (T + TW - 1) / TW;
+    const int g = blockIdx.x;
+    const int b = g / (nblk * nwin), rem = g % (nblk * nwin);
+    const int jb = rem / nwin, win = rem % nwin;
+    const int lane = threadIdx.x;
+    const int j = jb * 64 + lane;
+    const bool live = j < n1;
+    const int m0 = win * TW, m_end = min(T, m0 + TW);
+    lds_f32* tab = (lds_f32*)smem + lane;                        // [TW + 1][64], row TW: dummy
+    for (int r = 0; r < TW; ++r) tab[r * 64] = 0.0f;
     const int* idx = a.in_idx + (size_t)b * (T + 1);
-    global_f32* out = (global_f32*)(a.A_in + (size_t)b * T * n1 + (live ? j : 0));
-    int e_lo = uniform32(idx[0]);
-    int n_mod = 0;
-    for (int n = 0; n < T; ++n) {
-        const int e_hi = uniform32(idx[n + 1]);
-        for (int e0 = e_lo; e0 < e_hi; e0 += KB) {
-            int ids[KB], row[KB];
-            float w[KB];
-            list_chunk(a.in_neuron, e0, e_hi, ids);
-            if (live) {
-                chunk_rows(a.W0, a.slot0, n1, j, n, n_mod, S, T, ids, row, w);
-                column_add(col, nb, row, w);
-            }
-        }
-        if (live) {
-            out[(size_t)n * n1] = col[n_mod * nb];
-            col[n_mod * nb] = 0.0f;
-        }
-        e_lo = e_hi;
-        n_mod = (n_mod + 1 == S) ? 0 : n_mod + 1;
-    }
-}
-
-template <int MAXT>
-__global__ void __launch_bounds__(MAXT) forward_core_kernel(CoreFwdArgs a) {
-    const Topo& t = a.t;
-    if (a.st->bad_input) return;
-    const int b = blockIdx.x, tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6, nwaves = blockDim.x >> 6;
-    float* lds = reinterpret_cast<float*>(smem);
-    unsigned long long* masks = reinterpret_cast<unsigned long long*>(smem + a.mask_off);
-    const int S = t.S, T = t.T, L = t.L;
-
-    // zero the ring columns this lane owns
-    for (int p = 0; p < t.P; ++p) {
-        const int q = t.post[p], nq = t.n[q];
-        if (t.pre[p] == 0 || t.kind[q] != SNN_LIF || tid >= nq) continue;
-        if (t.fring[p] >= 0) {
-            lds_f32* c = (lds_f32*)(lds + t.fring[p]) + tid;
-            for (int s = 0; s < S; ++s) c[s * nq] = 0.0f;
-        } else {
-            global_f32* c = (global_f32*)(a.ring[p] + (size_t)b * S * nq) + tid;
-            for (int s = 0; s < S; ++s) c[s * nq] = 0.0f;
-        }
-    }
-
-    float V[SNN_MAX_LAYERS], I[SNN_MAX_LAYERS];
-    bool spk[SNN_MAX_LAYERS];
-    int cnt[SNN_MAX_LAYERS];
-#pragma unroll
-    for (int l = 0; l < SNN_MAX_LAYERS; ++l) {
-        V[l] = 0.0f;
-        I[l] = 0.0f;
-        spk[l] = false;
-        cnt[l] = 0;
-    }
-    const int n1 = t.n[1];
-    const global_f32* ain = (const global_f32*)(a.A_in + (size_t)b * T * n1) + tid;
-    float ain_next = (tid < n1) ? ain[0] : 0.0f;
-    int n_mod = 0;
-
-    for (int n = 0; n < T; ++n) {
-        const int par = n & 1;
-        const float ain_n = ain_next;
-        if (tid < n1 && n + 1 < T) ain_next = ain[(size_t)(n + 1) * n1];
-        // ---- free dynamics over one step, threshold, reset
-#pragma unroll
-        for (int l = 1; l < SNN_MAX_LAYERS; ++l) {
-            if (l >= L || t.kind[l] != SNN_LIF) break;
-            bool s_ = false;
-            if (tid < t.n[l]) {
-                const float gi = __fmul_rn(t.gamma, I[l]);
-                const float Vm = __fmaf_rn(t.alpha, V[l], gi);
-                I[l] = __fmul_rn(t.beta, I[l]);
-                s_ = Vm >= t.theta;
-                V[l] = s_ ? 0.0f : Vm;
-            }
-            spk[l] = s_;
-            const unsigned long long m = __ballot(s_);
-            if (lane == 0) masks[((size_t)par * t.n_lif + t.lif[l]) * nwaves + wave] = m;
-        }
-        __syncthreads();
-
-        // ---- spike records (ascending neuron order: waves ascending, lanes ascending)
-#pragma unroll
-        for (int l = 1; l < SNN_MAX_LAYERS; ++l) {
-            if (l >= L || t.kind[l] != SNN_LIF) break;
-            const int li = t.lif[l];
-            const unsigned long long* mk = masks + ((size_t)par * t.n_lif + li) * nwaves;
-            int before = 0, total = 0;
-            for (int w = 0; w < nwaves; ++w) {
-                const int c = __popcll(uniform64(mk[w]));
-                before += (w < wave) ? c : 0;
-                total += c;
-            }
-            // internal record indices never pass the capacity (the caller's
-            // count stays exact)
-            int* row = a.steptab + (((size_t)li * t.B + b) * T + n) * SNN_STEP_ROW;
-            if (tid == 0) {
-                a.rec_idx[((size_t)li * t.B + b) * (T + 1) + n] = min(cnt[l], t.cap);
-                row[0] = total;
-                row[1] = min(cnt[l], t.cap);
-            }
-            if (spk[l]) {
-                const int rank = before + lanes_below(mk[wave]);
-                if (rank < SNN_STEP_IDS) row[2 + rank] = tid;
-                const int pos = cnt[l] + rank;
-                if (pos < t.cap) {
-                    const size_t r = ((size_t)li * t.B + b) * t.cap + pos;
-                    a.rec_n[r] = tid;
-                    a.rec_s[r] = n;
-                    a.rec_I[r] = I[l];
-                    const size_t o = (size_t)b * t.cap + pos;
-                    a.out_step[l][o] = n;
-                    a.out_neuron[l][o] = tid;
-                }
-            }
-            if (tid == 0 && cnt[l] + total > t.cap) a.st->overflow = 1;
-            cnt[l] += total;
-        }
-
-        // ---- delayed scatter of the LIF spikes into the LIF-post rings
-        for (int p = 0; p < t.P; ++p) {
-            const int pa = t.pre[p], q = t.post[p], nq = t.n[q];
-            if (pa == 0 || t.kind[q] != SNN_LIF || tid >= nq) continue;
-            const float* Wp = a.W[p];
-            const uint8_t* Sp = a.slot + t.woff[p];
-            BitIter it = bits_begin(masks + ((size_t)par * t.n_lif + t.lif[pa]) * nwaves, nwaves);
-            int ids[KB], row[KB];
-            float w[KB];
-            while (bits_chunk(it, ids)) {
-                chunk_rows(Wp, Sp, nq, tid, n, n_mod, S, T, ids, row, w);
-                if (t.fring[p] >= 0)
-                    column_add((lds_f32*)(lds + t.fring[p]) + tid, nq, row, w);
-                else
-                    column_add((global_f32*)(a.ring[p] + (size_t)b * S * nq) + tid, nq, row, w);
-            }
-        }
-
-        // ---- arrivals: per projection into the layer, in projection order
-        for (int p = 0; p < t.P; ++p) {
-            const int q = t.post[p], nq = t.n[q];
-            if (t.kind[q] != SNN_LIF || tid >= nq) continue;
-            float add;
-            if (t.pre[p] == 0) {
-                add = ain_n;
-            } else if (t.fring[p] >= 0) {
-                lds_f32* c = (lds_f32*)(lds + t.fring[p]) + n_mod * nq + tid;
-                add = *c;
-                *c = 0.0f;
-            } else {
-                global_f32* c = (global_f32*)(a.ring[p] + ((size_t)b * S + n_mod) * nq) + tid;
-                add = *c;
-                *c = 0.0f;
-            }
-#pragma unroll
-            for (int l = 1; l < SNN_MAX_LAYERS; ++l)
-                if (l == q) I[l] = __fadd_rn(I[l], add);
-        }
-        n_mod = (n_mod + 1 == S) ? 0 : n_mod + 1;
-    }
-
-    // ---- epilogue
-    int soff = 0, nstate = 0;
-    for (int l = 1; l < L; ++l) nstate += t.n[l];
-#pragma unroll
-    for (int l = 1; l < SNN_MAX_LAYERS; ++l) {
-        if (l >= L || t.kind[l] != SNN_LIF) break;
-        if (tid < t.n[l]) {
-            a.Vf[(size_t)b * nstate + soff + tid] = V[l];
-            a.If[(size_t)b * nstate + soff + tid] = I[l];
-        }
-        soff += t.n[l];
-        if (tid == 0) {
-            const int li = t.lif[l];
-            a.rec_idx[((size_t)li * t.B + b) * (T + 1) + T] = min(cnt[l], t.cap);
-            a.rec_cnt[(size_t)li * t.B + b] = min(cnt[l], t.cap);
-            a.out_count[l][b] = cnt[l];
-            atomicAdd(&a.st->layer_spikes[li], (unsigned long long)cnt[l]);
-        }
+    const int e_lo = idx[max(0, m0 - (a.S - 1))], e_hi = idx[m_end];
+    scatter_events(a.in_neuron, a.in_step, e_lo, e_hi, a.ws0, a.n_in * n1 * 8, n1, j, live, m0, m_end,
+                   TW, tab, 64);
+    if (live) {
+        global_f32* out = (global_f32*)(a.A_in + ((size_t)b * T + m0) * n1 + j);
+        for (int r = 0; r < m_end - m0; ++r) out[(size_t)r * n1] = tab[r * 64];
     }
 }
 
 // ------------------------------------------------------------------ readout
 
-// Readout arrivals of sample b into the column of output k: table cell m at
-// col[m * C] for every step m (an arrival table, not a ring: the spikes are
-// all known).  Spikes in record (emission) order.
-template <typename Ptr>
-__device__ __forceinline__ void readout_table(const ReadoutArgs& a, int b, int k, Ptr col) {
-    const Topo& t = a.t;
-    const int C = t.n[t.out_l], T = t.T;
-    const int pa = t.pre[t.out_p];
-    const size_t base = ((size_t)t.lif[pa] * t.B + b) * t.cap;
-    const int cnt = uniform32(a.rec_idx[((size_t)t.lif[pa] * t.B + b) * (T + 1) + T]);
-    for (int k0 = 0; k0 < cnt; k0 += KB) {
-        int ids[KB], steps[KB], row[KB];
-        float w[KB];
-        list_chunk(a.rec_n + base, k0, cnt, ids);
-        list_chunk(a.rec_s + base, k0, cnt, steps);
-        if (k < C) {
-#pragma unroll
-            for (int q = 0; q < KB; ++q) {
-                row[q] = -1;
-                w[q] = 0.0f;
-                if (ids[q] >= 0) {
-                    const size_t kk = (size_t)ids[q] * C + k;
-                    const int m = steps[q] + a.slot[t.woff[t.out_p] + kk];
-                    w[q] = a.W[kk];
-                    if (m <= T - 1) row[q] = m;
-                }
-            }
-            column_add(col, C, row, w);
-        }
-    }
-}
-
 // One workgroup per sample, lane k owns output neuron k.  table_lds >= 0:
-// the arrival table [T][C] lives in LDS; else in the global ring buffer
-// (sized [B][T][C] by the host for this case).
+// the arrival table [T + 1][C] (row T: dummy) lives in LDS; else in global
+// memory ([B][T + 1][C], sized by the host for this case).
 __global__ void __launch_bounds__(1024) readout_forward_kernel(ReadoutArgs a) {
     const Topo& t = a.t;
     if (a.st->bad_input) return;
@@ -326,15 +126,25 @@ __global__ void __launch_bounds__(1024) readout_forward_kernel(ReadoutArgs a) {
     const int pa = t.pre[t.out_p];
     float* lds = reinterpret_cast<float*>(smem);
     const bool in_lds = a.table_lds >= 0;
-    lds_f32* lcol = (lds_f32*)(lds + (in_lds ? a.table_lds : 0)) + k;
-    global_f32* gcol = in_lds ? nullptr : (global_f32*)(a.table + (size_t)b * T * C) + k;
+    // table [T + 1][C] (row T: dummy); lanes past C share column C - 1's
+    // dummy cell and touch nothing else
+    const int kc = min(k, C - 1);
+    lds_f32* lcol = (lds_f32*)(lds + (in_lds ? a.table_lds : 0)) + kc;
+    global_f32* gcol = in_lds ? nullptr : (global_f32*)(a.table + (size_t)b * (T + 1) * C) + kc;
     if (pa != 0) {
+        // arrival table of the feeding layer's spikes, in emission order
         if (k < C) {
             for (int m = 0; m < T; ++m) {
                 if (in_lds) lcol[m * C] = 0.0f; else gcol[m * C] = 0.0f;
             }
         }
-        if (in_lds) readout_table(a, b, k, lcol); else readout_table(a, b, k, gcol);
+        const size_t base = ((size_t)t.lif[pa] * t.B + b) * t.cap;
+        const int cnt = a.rec_idx[((size_t)t.lif[pa] * t.B + b) * (T + 1) + T];
+        const int wsb = t.n[pa] * C * 8;
+        if (in_lds)
+            scatter_events(a.rec_n + base, a.rec_s + base, 0, cnt, a.ws, wsb, C, k, k < C, 0, T, T, lcol, C);
+        else
+            scatter_events(a.rec_n + base, a.rec_s + base, 0, cnt, a.ws, wsb, C, k, k < C, 0, T, T, gcol, C);
     }
     if (k >= C) return;
     const global_f32* ain = (const global_f32*)(a.A_in + (size_t)b * T * C) + k;
@@ -449,19 +259,8 @@ hipError_t launch_round_delays(const float* const* D, const float* const* W, con
 }
 
 hipError_t launch_input_scan(const InScanArgs& a, size_t lds, hipStream_t s) {
-    const int nblk = (a.t.n[1] + a.nb - 1) / a.nb;
-    const int threads = ((a.nb + 63) / 64) * 64;
-    hipLaunchKernelGGL(input_scan_kernel, dim3(a.t.B * nblk), dim3(threads), lds, s, a);
-    return hipGetLastError();
-}
-
-// Workgroups of up to 256 threads get the 256-thread instantiation (one wave
-// per SIMD, up to 512 registers per lane); wider networks the 1024-thread one.
-hipError_t launch_forward_core(const CoreFwdArgs& a, int threads, size_t lds, hipStream_t s) {
-    if (threads <= 256)
-        hipLaunchKernelGGL(forward_core_kernel<256>, dim3(a.t.B), dim3(threads), lds, s, a);
-    else
-        hipLaunchKernelGGL(forward_core_kernel<1024>, dim3(a.t.B), dim3(threads), lds, s, a);
+    const int nblk = (a.n1 + 63) / 64, nwin = (a.T + a.TW - 1) / a.TW;
+    hipLaunchKernelGGL(input_scan_kernel, dim3(a.B * nblk * nwin), dim3(64), lds, s, a);
     return hipGetLastError();
 }
 
@@ -484,13 +283,40 @@ hipError_t launch_copy_state(const float* src, int stride, int off, int n, int B
     return hipGetLastError();
 }
 
-hipError_t set_forward_lds_limits(size_t bytes) {
-    const void* fns[] = {(const void*)input_scan_kernel, (const void*)forward_core_kernel<256>,
-                         (const void*)forward_core_kernel<1024>, (const void*)readout_forward_kernel};
-    for (const void* f : fns) {
+hipError_t set_forward_lds_limits(size_t bytes, int* bad) {
+    const void* fns[] = {(const void*)input_scan_kernel, (const void*)readout_forward_kernel};
+    for (int i = 0; i < (int)(sizeof(fns) / sizeof(fns[0])); ++i) {
         const hipError_t e =
-            hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-        if (e != hipSuccess) return e;
+            hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+        if (e != hipSuccess) {
+            if (bad) *bad = i;
+            return e;
+        }
     }
     return hipSuccess;
+}
+
+hipError_t launch_forward_core(const CoreFwdArgs& a, int n_lif, int threads, size_t lds,
+                               hipStream_t s) {
+    if (n_lif < 1 || n_lif > SNN_MAX_LIF || threads != 64 * a.NW) return hipErrorInvalidValue;
+    int np = 0;
+    bool rl = true;
+    for (int l = 0; l < n_lif; ++l) {
+        np = max(np, a.ly[l].npost);
+        for (int pp = 0; pp < a.ly[l].npost; ++pp)
+            if (a.ly[l].ring_lds[pp] < 0) rl = false;
+    }
+    const bool ok = (threads <= 256) ? launch_forward_core_256(a, n_lif, np, rl, threads, lds, s)
+                                     : launch_forward_core_1024(a, n_lif, np, rl, threads, lds, s);
+    if (!ok) return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+hipError_t set_core_lds_limits(size_t bytes, int* bad) {
+    hipError_t e = set_core_lds_limits_256(bytes, bad);
+    if (e == hipSuccess) {
+        e = set_core_lds_limits_1024(bytes, bad);
+        if (e != hipSuccess && bad) *bad += 16;   // 1024-thread kernels: 16 .. 31
+    }
+    return e;
 }

@@ -49,41 +49,54 @@ struct Topo {
 // Input projection arrivals: A_in[b][n][j] = sum, in emission order, of the
 // input-projection weights arriving at post j of layer 1 at step n.
 struct InScanArgs {
-    Topo t;
-    const float* W0;
-    const uint8_t* slot0;
+    int B, T, S, n_in, n1, TW;         // TW: arrival steps per workgroup window
+    const uint2* ws0;                  // input projection (weight bits, slot) [n_in][n1]
     const int* in_neuron;
+    const int* in_step;
     const int* in_idx;                 // [B][T+1] first input event of each step
     float* A_in;                       // [B][T][n_1]
     const DevStatus* st;
-    int nb;                            // posts per workgroup (ring [S][nb] in LDS)
+};
+
+// One LIF layer as seen by the forward core.
+struct FwdLayer {
+    int n;
+    int nin;                           // projections into the layer, in projection order:
+    int in_l[2];                       //   source LIF layer (0-based), -1: the input projection
+    int in_pp[2];                      //   index among the source layer's LIF-post projections
+    int npost;                         // LIF-post projections out of the layer (recurrent, then
+                                       // feed-forward); entries past npost repeat a valid one
+    int nq[2];                         //   post neurons
+    int npre[2];                       //   rows of ws (the presynaptic layer's neurons)
+    int ring_lds[2];                   //   delay ring [S+1][nq] (row S: dummy): LDS float offset,
+    float* ring[2];                    //   or the HBM ring [B][S+1][nq]
+    const uint2* ws[2];                //   (weight bits, slot) [n][nq]
+    int* rec_n;                        // [B][cap] records: neuron, step, I-
+    int* rec_s;
+    float* rec_I;
+    int* rec_idx;                      // [B][T+1] first record of each step
+    int* rec_cnt;                      // [B]
+    int* steptab;                      // [B][T][SNN_STEP_ROW]
+    int* out_count;                    // caller's records: [B], [B][cap], [B][cap]
+    int* out_step;
+    int* out_neuron;
 };
 
 struct CoreFwdArgs {
-    Topo t;
-    const float* W[SNN_MAXP];
-    const uint8_t* slot;               // flat [params]
-    float* ring[SNN_MAXP];             // global rings of LIF->LIF projections not in LDS
-    const float* A_in;
-    int* out_count[SNN_MAX_LAYERS];    // caller's records, by layer index
-    int* out_step[SNN_MAX_LAYERS];
-    int* out_neuron[SNN_MAX_LAYERS];
-    int* rec_n;                        // [n_lif][B][cap] neuron
-    int* rec_s;                        // [n_lif][B][cap] step
-    float* rec_I;                      // [n_lif][B][cap] I- at the spike
-    int* rec_idx;                      // [n_lif][B][T+1] first record of each step
-    int* rec_cnt;                      // [n_lif][B] spikes per sample
-    int* steptab;                      // [n_lif][B][T][SNN_STEP_ROW] per-step spike table
-    float* Vf;                         // [B][sum n_l] final state
+    int B, T, S, cap, NW, n1, nstate;
+    float alpha, beta, gamma, theta;
+    FwdLayer ly[SNN_MAX_LIF];
+    int soff[SNN_MAX_LIF];             // offset of each LIF layer in the [B][nstate] final state
+    const float* A_in;                 // [B][T][n_1] input-projection arrivals
+    float* Vf;                         // [B][nstate] final state
     float* If;
     DevStatus* st;
-    int mask_off;                      // byte offset of the ballot masks in LDS
+    int mask_off;                      // byte offset of the ballot masks [3][NL][NW] in LDS
 };
 
 struct ReadoutArgs {
     Topo t;
-    const float* W;                    // projection into the readout layer
-    const uint8_t* slot;
+    const uint2* ws;                   // projection into the readout layer (weight bits, slot)
     const float* A_in;                 // arrivals when the readout is fed by the inputs
     const int* rec_n;                  // records of the layer feeding the readout
     const int* rec_s;
@@ -200,7 +213,8 @@ hipError_t launch_round_delays(const float* const* D, const float* const* W, con
                                const long long* cnt, int P, int max_delay, uint8_t* slot, uint2* ws,
                                DevStatus* st, hipStream_t s);
 hipError_t launch_input_scan(const InScanArgs& a, size_t lds, hipStream_t s);
-hipError_t launch_forward_core(const CoreFwdArgs& a, int threads, size_t lds, hipStream_t s);
+hipError_t launch_forward_core(const CoreFwdArgs& a, int n_lif, int threads, size_t lds,
+                               hipStream_t s);
 hipError_t launch_readout_forward(const ReadoutArgs& a, int threads, size_t lds, hipStream_t s);
 hipError_t launch_loss(const float* z, const int* labels, int B, int C, int loss, float rscale,
                        float tau_m, float* loss_out, float* src, const DevStatus* st, hipStream_t s);
@@ -212,5 +226,12 @@ hipError_t launch_backward_core(const CoreBwdArgs& a, int n_lif, int threads, si
 hipError_t launch_group(const GroupArgs& a, int B, hipStream_t s);
 hipError_t launch_gradients(const GradArgs& a, int J, int threads, size_t lds, hipStream_t s);
 hipError_t launch_grad_reduce(const GradArgs& a, int P, hipStream_t s);
-hipError_t set_forward_lds_limits(size_t bytes);
-hipError_t set_backward_lds_limits(size_t bytes);
+hipError_t set_forward_lds_limits(size_t bytes, int* bad);
+hipError_t set_core_lds_limits(size_t bytes, int* bad);
+bool launch_forward_core_256(const CoreFwdArgs& a, int n_lif, int np, bool rl, int threads,
+                             size_t lds, hipStream_t s);
+bool launch_forward_core_1024(const CoreFwdArgs& a, int n_lif, int np, bool rl, int threads,
+                              size_t lds, hipStream_t s);
+hipError_t set_core_lds_limits_256(size_t bytes, int* bad);
+hipError_t set_core_lds_limits_1024(size_t bytes, int* bad);
+hipError_t set_backward_lds_limits(size_t bytes, int* bad);
