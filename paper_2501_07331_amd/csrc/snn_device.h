@@ -163,15 +163,37 @@ __device__ __forceinline__ void row_words(const unsigned long long* row, int NW,
     for (int w = 0; w < NWM; ++w) m[w] = uniform64(m[w]);
 }
 
+// Position of set bit number r (0-based, r < popcount) of a 64-bit word, by
+// halving: branch-free, per lane.
+__device__ __forceinline__ int nth_bit(unsigned long long word, int r) {
+    const unsigned lo = (unsigned)word, hi = (unsigned)(word >> 32);
+    int c = __popc(lo);
+    bool up = r >= c;
+    r -= up ? c : 0;
+    unsigned x = up ? hi : lo;
+    int pos = up ? 32 : 0;
+#pragma unroll
+    for (int h = 16; h >= 2; h >>= 1) {
+        const unsigned low = x & ((1u << h) - 1u);
+        c = __popc(low);
+        up = r >= c;
+        r -= up ? c : 0;
+        x = up ? (x >> h) : low;
+        pos += up ? h : 0;
+    }
+    return pos + ((r >= (int)(x & 1u)) ? 1 : 0);
+}
+
 // Set bits of a spike-mask row, ascending: skip the first `skip`, return the
-// next N (-1 past the end).  Up to four words the row's words m (uniform, in
-// registers) are walked fully unrolled; longer rows (row: the same words in
-// LDS, NW of them) are walked word by word at run time, which keeps the code
-// small.
+// next N (-1 past the end), uniform.  Up to four words (m: the row's words,
+// uniform) lane q finds set bit number skip + q branch-free and the ids are
+// read from lanes 0 .. N-1; longer rows (row: the same NW words in LDS) are
+// walked word by word at run time, which keeps the code small.
 template <int NWM, int N>
 __device__ __forceinline__ void word_ids(const unsigned long long (&m)[NWM],
                                          const unsigned long long* row, int NW, int skip,
                                          int (&ids)[N]) {
+    static_assert(N <= 64, "one lane per id");
     if constexpr (NWM > 4) {
         BitIter it = bits_begin(row, NW);
         for (;;) {
@@ -183,31 +205,21 @@ __device__ __forceinline__ void word_ids(const unsigned long long (&m)[NWM],
         for (; skip > 0 && it.cur; --skip) it.cur &= it.cur - 1;
         bits_chunk<N>(it, ids);
     } else {
-        unsigned long long rem[NWM];
+        const int q = (int)(threadIdx.x & 63) + skip;
+        int base = 0, wsel = -1, bsel = 0;
+        unsigned long long word = 0;
 #pragma unroll
-        for (int w = 0; w < NWM; ++w) rem[w] = m[w];
-        for (int k = 0; k < skip; ++k) {
-            bool done = false;
-#pragma unroll
-            for (int w = 0; w < NWM; ++w) {
-                if (!done && rem[w]) {
-                    rem[w] &= rem[w] - 1;
-                    done = true;
-                }
-            }
+        for (int w = 0; w < NWM; ++w) {
+            const int c = __popcll(m[w]);
+            const bool here = wsel < 0 && q < base + c;
+            word = here ? m[w] : word;
+            bsel = here ? base : bsel;
+            wsel = here ? w : wsel;
+            base += c;
         }
+        const int id = (wsel < 0) ? -1 : wsel * 64 + nth_bit(word, q - bsel);
 #pragma unroll
-        for (int q = 0; q < N; ++q) {
-            int id = -1;
-#pragma unroll
-            for (int w = 0; w < NWM; ++w) {
-                if (id < 0 && rem[w]) {
-                    id = w * 64 + __builtin_ctzll(rem[w]);
-                    rem[w] &= rem[w] - 1;
-                }
-            }
-            ids[q] = id;
-        }
+        for (int k = 0; k < N; ++k) ids[k] = __builtin_amdgcn_readlane(id, k);
     }
 }
 

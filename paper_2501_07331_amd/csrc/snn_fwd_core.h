@@ -1,7 +1,6 @@
 // The LIF forward core of libsnn (gfx950, wave64), as a template; its
 // instantiations for 256 and 1024 threads live in two sources so that they
-// compile in parallel. one workgroup per sample
-// runs the LIF layers over T steps (Table 1, forward dynamics with delayed
+// compile in parallel.  One workgroup per sample runs the LIF layers over T steps (Table 1, forward dynamics with delayed
 // current jumps).  Lane j owns neuron j of every LIF layer and column j of
 // every delay ring into that layer.
 //
@@ -15,12 +14,14 @@
 // slots of step n's spikes are loaded during step n and scattered at step
 // n + 1, so their load latency is hidden behind a whole step.  Arrivals with
 // delay 0 cannot wait: every lane keeps, for each LIF-post projection, the
-// presynaptic neurons with slot 0 into its post neuron (a bitmask) and their
-// weights, and adds those of step n's spikes to the arrival at step n, after
-// the ring cell (which by then holds every earlier step's weights): the same
-// fp32 sequence as adding in emission order.  With rings in HBM, more than
-// two (layer, LIF-post projection) pairs, 1024 threads, or a post neuron with
-// more than kZMax zero-delay synapses, the scatter is immediate.
+// presynaptic neurons with slot 0 into its post neuron (a bitmask in
+// registers; their weights in LDS, in ascending presynaptic order) and adds
+// those of step n's spikes to the arrival at step n, after the ring cell
+// (which by then holds every earlier step's weights): the same fp32 sequence
+// as adding in emission order.  With rings in HBM, more than two (layer,
+// LIF-post projection) pairs, 1024 threads, no LDS left for the weights, or
+// a post neuron with more than SNN_ZMAX zero-delay synapses, the scatter is
+// immediate.
 #pragma once
 
 #include <type_traits>
@@ -29,7 +30,7 @@
 
 namespace {
 
-constexpr int kZMax = 12;   // zero-delay synapses per lane and projection held in registers
+constexpr int kZMax = SNN_ZMAX;   // zero-delay synapses per lane and projection
 
 template <int MAXT, int NL, int NP, bool RL>
 struct FwdCore {
@@ -54,8 +55,6 @@ struct FwdCore {
         float V[NL], I[NL];
         int cnt[NL];                          // records so far (exact; may pass the capacity)
         unsigned long long zb[NL][NPA][NWM];  // presynaptic neurons with slot 0 into this lane's post
-        int zi[NL][NPA][kZMax];               // the same, as a list ascending (-1: unused)
-        float zw[NL][NPA][kZMax];             // their weights
     };
 
     template <typename Ptr>
@@ -249,6 +248,7 @@ struct FwdCore {
 
         // ---- arrivals at step n: per projection into the layer, in projection order
         const int n_mod = n % S;
+        const int lanes = NW * 64;
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
             const FwdLayer& y = a.ly[l];
@@ -273,19 +273,21 @@ struct FwdCore {
 #pragma unroll
                             for (int pq = 0; pq < NPA; ++pq) {
                                 if (pq != pp) continue;
-                                unsigned long long any = 0;
+                                // weights of this lane's zero-delay synapses, ascending
+                                const lds_f32* zw = (const lds_f32*)(reinterpret_cast<float*>(smem + a.zw_off)) +
+                                                    (size_t)(ll * NPA + pq) * kZMax * lanes + tid;
+                                int kbase = 0;
 #pragma unroll
-                                for (int w = 0; w < NWM; ++w) any |= mw[ll][w] & L.zb[ll][pq][w];
-                                if (any) {
-#pragma unroll
-                                    for (int k = 0; k < kZMax; ++k) {
-                                        const int i = L.zi[ll][pq][k];
-                                        unsigned long long word = 0;
-#pragma unroll
-                                        for (int w = 0; w < NWM; ++w) word = (w == (i >> 6)) ? mw[ll][w] : word;
-                                        const bool hit = i >= 0 && ((word >> (i & 63)) & 1ull);
-                                        add = hit ? __fadd_rn(add, L.zw[ll][pq][k]) : add;
+                                for (int w = 0; w < NWM; ++w) {
+                                    const unsigned long long z = L.zb[ll][pq][w];
+                                    unsigned long long h = mw[ll][w] & z;
+                                    while (h) {
+                                        const int bit = __builtin_ctzll(h);
+                                        const int k = kbase + __popcll(z & ((1ull << bit) - 1ull));
+                                        add = __fadd_rn(add, zw[k * lanes]);
+                                        h &= h - 1;
                                     }
+                                    kbase += __popcll(z);
                                 }
                             }
                         }
@@ -335,9 +337,11 @@ struct FwdCore {
             L.I[l] = 0.0f;
             L.cnt[l] = 0;
         }
-        bool defer = kDeferable;
+        bool defer = kDeferable && a.zw_off >= 0;
         if constexpr (kDeferable) {
-            // ---- delay-0 synapses into this lane's post, per LIF-post projection
+            // ---- delay-0 synapses into this lane's post, per LIF-post
+            // projection: bitmask in registers, weights in LDS ascending
+            const int lanes = a.NW * 64;
             bool over = false;
 #pragma unroll
             for (int l = 0; l < NL; ++l) {
@@ -345,11 +349,9 @@ struct FwdCore {
                 for (int pp = 0; pp < NPA; ++pp) {
 #pragma unroll
                     for (int w = 0; w < NWM; ++w) L.zb[l][pp][w] = 0ull;
-#pragma unroll
-                    for (int k = 0; k < kZMax; ++k) {
-                        L.zw[l][pp][k] = 0.0f;
-                        L.zi[l][pp][k] = -1;
-                    }
+                    if (!defer) continue;
+                    lds_f32* zw = (lds_f32*)(reinterpret_cast<float*>(smem + a.zw_off)) +
+                                  (size_t)(l * NPA + pp) * kZMax * lanes + tid;
                     const FwdLayer& y = a.ly[l];
                     if (pp >= NP || pp >= y.npost) continue;
                     const int nq = y.nq[pp];
@@ -372,13 +374,7 @@ struct FwdCore {
 #pragma unroll
                             for (int w = 0; w < NWM; ++w)
                                 if (w == (i >> 6)) L.zb[l][pp][w] |= 1ull << (i & 63);
-#pragma unroll
-                            for (int kk = 0; kk < kZMax; ++kk) {
-                                if (kk == cnt) {
-                                    L.zw[l][pp][kk] = __uint_as_float(e8[k].x);
-                                    L.zi[l][pp][kk] = i;
-                                }
-                            }
+                            if (cnt < kZMax) zw[cnt * lanes] = __uint_as_float(e8[k].x);
                             ++cnt;
                         }
                     }
@@ -394,7 +390,7 @@ struct FwdCore {
             __syncthreads();
             bool any = false;
             for (int w = 0; w < a.NW; ++w) any = any || vote[w] != 0ull;
-            defer = !any;
+            defer = defer && !any;
         } else {
             __syncthreads();
         }

@@ -59,6 +59,10 @@ struct InScanArgs {
 };
 
 // One LIF layer as seen by the forward core.
+// zero-delay synapses per post neuron and LIF-post projection that the
+// deferred forward scatter handles from LDS
+#define SNN_ZMAX 16
+
 struct FwdLayer {
     int n;
     int nin;                           // projections into the layer, in projection order:
@@ -92,6 +96,8 @@ struct CoreFwdArgs {
     float* If;
     DevStatus* st;
     int mask_off;                      // byte offset of the ballot masks [3][NL][NW] in LDS
+    int zw_off;                        // byte offset of the zero-delay weights [NL][NP][SNN_ZMAX][64 NW]
+                                       // in LDS, -1: none (no deferred scatter)
 };
 
 struct ReadoutArgs {

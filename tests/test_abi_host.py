@@ -83,7 +83,11 @@ def test_null_handles(lib):
     assert lib.snn_forward(None, None, None, None, None, None, None, None) == -1
     assert lib.snn_backward(None, None, None) == -1
     assert lib.snn_get_stats(None, None) == -1
-    assert lib.snn_last_error(None) == b"NULL handle"
+    # with no handle: the reason of the last failed snn_create ("" after an
+    # argument error, which needs no explanation beyond its code)
+    rc, h = _create(lib, GOOD, batch=0)
+    assert rc == -1 and not h.value
+    assert lib.snn_last_error(None) == b""
     lib.snn_destroy(None)
 
 
