@@ -26,7 +26,7 @@ struct snn_net {
     int core_threads;           // LIF-core workgroup size
     int read_threads;           // readout workgroup size
     size_t lds_core_f, lds_core_b, lds_scan, lds_read, lds_grad, lds_radj;
-    int mask_off, zw_off, scan_tw, table_lds;
+    int mask_off, zw_off, scan_tb, table_lds;
     int bpart_off;              // backward-core LDS plan
     int bring_mode[SNN_MAX_LAYERS];   // adjoint ring of a LIF layer: -2 none, -1 HBM, >= 0 LDS
     int radj_threads, radj_tab;
@@ -289,8 +289,11 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         net->lds_core_b = used;
     }
     // input scan: windows of 128 arrival steps (a [128][64] table per wave)
-    net->scan_tw = std::min(128, t.T);
-    net->lds_scan = (size_t)(net->scan_tw + 1) * 64 * sizeof(float);
+    // input scan ring: S + TB - 1 arrival steps and a dummy row per 64-post
+    // wave; TB as large as keeps four rings in one CU's LDS (40 KiB each),
+    // at least 8
+    net->scan_tb = std::max(8, std::min(64, 160 - t.S));
+    net->lds_scan = (size_t)(t.S + net->scan_tb) * 64 * sizeof(float);
     // readout forward: arrival table [T + 1][C] (row T: dummy) in LDS when it fits
     net->read_threads = ((C + 63) / 64) * 64;
     {
@@ -494,7 +497,7 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
     sa.S = t.S;
     sa.n_in = t.n_in;
     sa.n1 = t.n[1];
-    sa.TW = net->scan_tw;
+    sa.TB = net->scan_tb;
     sa.ws0 = net->ws;
     sa.in_neuron = in->neuron;
     sa.in_step = in->step;

@@ -85,32 +85,124 @@ __global__ void round_delays_kernel(RoundArgs a, uint8_t* slot, uint2* ws, DevSt
 
 // ------------------------------------------------------------------ input scan
 
-// Workgroup = (sample b, block of 64 posts of layer 1, window of TW arrival
-// steps), one wave: the input events that can arrive in the window (emitted
-// within S - 1 steps before it, or in it) are added in emission order into
-// an LDS table [TW][64], which then goes out as A_in rows.  No step-by-step
-// dependency: all windows run in parallel.
+// Workgroup = (sample b, block of 64 posts of layer 1), one wave; lane j owns
+// post j.  The sample's input events stream by once, in emission order, in
+// chunks of KB = 8, and each chunk's weights are added into an LDS ring of
+// R = S + TB - 1 arrival steps (row m % R; row R: dummy).  Rows of steps
+// before the first emission step of the next chunk are final (every later
+// event arrives at its emission step or after): they go out as A_in rows and
+// are cleared, at most two per chunk on the common path.  A chunk whose
+// arrivals fit the ring from the first row not yet written out (its steps
+// span less than TB past that row) is added at once; otherwise (a gap in the
+// input, or a sparse chunk) the rows up to the chunk go out first and its
+// events are added one by one, each after writing out the rows before it.  A
+// ring cell sums in emission order (column_add_all keeps the order of equal
+// rows).
+//
+// Loads run one chunk ahead, as in scatter_events: the ids and steps of a
+// pair of chunks (one event per lane), and the weights and slots of the next
+// chunk while a chunk is added, in two register sets; one explicit wait at
+// each chunk start.  The common path writes out at most two rows per chunk
+// and has no loop.
 __global__ void __launch_bounds__(64) input_scan_kernel(InScanArgs a) {
     if (a.st->bad_input) return;
-    const int n1 = a.n1, T = a.T, TW = a.TW;
-    const int nblk = (n1 + 63) / 64, nwin = (T + TW - 1) / TW;
-    const int g = blockIdx.x;
-    const int b = g / (nblk * nwin), rem = g % (nblk * nwin);
-    const int jb = rem / nwin, win = rem % nwin;
-    const int lane = threadIdx.x;
-    const int j = jb * 64 + lane;
+    const int n1 = a.n1, T = a.T, TB = a.TB, R = a.S + a.TB - 1;
+    const int nblk = (n1 + 63) >> 6;
+    const int b = blockIdx.x / nblk, jb = blockIdx.x - b * nblk;
+    const int lane = threadIdx.x, j = jb * 64 + lane;
     const bool live = j < n1;
-    const int m0 = win * TW, m_end = min(T, m0 + TW);
-    lds_f32* tab = (lds_f32*)smem + lane;                        // [TW + 1][64], row TW: dummy
-    for (int r = 0; r < TW; ++r) tab[r * 64] = 0.0f;
-    const int* idx = a.in_idx + (size_t)b * (T + 1);
-    const int e_lo = idx[max(0, m0 - (a.S - 1))], e_hi = idx[m_end];
-    scatter_events(a.in_neuron, a.in_step, e_lo, e_hi, a.ws0, a.n_in * n1 * 8, n1, j, live, m0, m_end,
-                   TW, tab, 64);
-    if (live) {
-        global_f32* out = (global_f32*)(a.A_in + ((size_t)b * T + m0) * n1 + j);
-        for (int r = 0; r < m_end - m0; ++r) out[(size_t)r * n1] = tab[r * 64];
+    const int jc = min(j, n1 - 1);
+    lds_f32* ring = (lds_f32*)smem + lane;                      // [R + 1][64]
+    for (int r = 0; r <= R; ++r) ring[r * 64] = 0.0f;
+    global_f32* out = (global_f32*)(a.A_in + (size_t)b * T * n1 + jc);
+    const int E0 = a.in_idx[(size_t)b * (T + 1)], E1 = a.in_idx[(size_t)b * (T + 1) + T];
+    int f = 0, fr = 0;                                           // rows < f written out; fr = f % R
+    auto flush_one = [&]() {
+        const float v = ring[fr * 64];
+        ring[fr * 64] = 0.0f;
+        if (live) out[(size_t)f * n1] = v;
+        ++f;
+        fr = (fr + 1 == R) ? 0 : fr + 1;
+    };
+    auto flush_to = [&](int m) {
+        while (f < m) flush_one();
+    };
+    if (E1 > E0) {
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)a.ws0, (short)0, a.n_in * n1 * 8, 0x00020000);
+        const int col8 = jc * 8, row8 = n1 * 8;
+        // events e0 + q for lanes q < 2 KB (clamped to the last event)
+        auto load_pair = [&](int e0, int& idv, int& stv) {
+            const int e = min(e0 + (lane & (2 * KB - 1)), E1 - 1);
+            idv = a.in_neuron[e];
+            stv = a.in_step[e];
+        };
+        auto load_ws = [&](int idv, int u8, uint2 (&w)[KB]) {
+#pragma unroll
+            for (int q = 0; q < KB; ++q) {
+                const int id = __builtin_amdgcn_readlane(idv, u8 + q);
+                const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, col8, id * row8, 0);
+                w[q] = make_uint2((unsigned)v[0], (unsigned)v[1]);
+            }
+        };
+        // chunk of events e0 .. e0 + KB - 1 (steps in lanes u8 .. u8 + KB - 1 of stv)
+        auto add_chunk = [&](int e0, int stv, int u8, const uint2 (&w)[KB]) {
+            const int nv = E1 - e0;                              // valid events (uniform)
+            if (nv <= 0) return;
+            int st[KB];
+#pragma unroll
+            for (int q = 0; q < KB; ++q) st[q] = __builtin_amdgcn_readlane(stv, u8 + q);
+            int last = st[0];
+#pragma unroll
+            for (int q = 1; q < KB; ++q) last = (q < nv) ? st[q] : last;
+            if (f < st[0]) flush_one();
+            if (f < st[0]) flush_one();
+            if (last - f < TB) {
+                int row[KB];
+                float wv[KB];
+#pragma unroll
+                for (int q = 0; q < KB; ++q) {
+                    const int s = (int)w[q].y;
+                    int r = fr + (st[q] - f) + s;
+                    r = (r >= R) ? r - R : r;
+                    row[q] = (q < nv && st[q] + s < T) ? r : R;
+                    wv[q] = __uint_as_float(w[q].x);
+                }
+                column_add_all(ring, 64, row, wv);
+            } else {
+                // rare: events one by one, reloaded
+                const int n = min(nv, KB);
+                for (int q = 0; q < n; ++q) {
+                    const int e = e0 + q;
+                    const int stq = a.in_step[e];
+                    flush_to(stq);
+                    const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, col8, a.in_neuron[e] * row8, 0);
+                    const int s = (int)v[1];
+                    int r = fr + s;
+                    r = (r >= R) ? r - R : r;
+                    if (stq + s < T) ring[r * 64] = __fadd_rn(ring[r * 64], __uint_as_float((unsigned)v[0]));
+                }
+            }
+        };
+        int idA, stA, idB, stB;
+        uint2 w0[KB], w1[KB];
+        load_pair(E0, idA, stA);
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        load_ws(idA, 0, w0);
+        for (int e0 = E0; e0 < E1; e0 += 2 * KB) {
+            __builtin_amdgcn_s_waitcnt(kWaitVm0);
+            load_pair(e0 + 2 * KB, idB, stB);
+            load_ws(idA, KB, w1);                                // second chunk of this pair
+            add_chunk(e0, stA, 0, w0);
+            if (e0 + KB >= E1) break;
+            __builtin_amdgcn_s_waitcnt(kWaitVm0);
+            load_ws(idB, 0, w0);                                 // first chunk of the next pair
+            add_chunk(e0 + KB, stA, KB, w1);
+            idA = idB;                                           // landed at the wait above
+            stA = stB;
+        }
     }
+    flush_to(T);
 }
 
 // ------------------------------------------------------------------ readout
@@ -259,8 +351,9 @@ hipError_t launch_round_delays(const float* const* D, const float* const* W, con
 }
 
 hipError_t launch_input_scan(const InScanArgs& a, size_t lds, hipStream_t s) {
-    const int nblk = (a.n1 + 63) / 64, nwin = (a.T + a.TW - 1) / a.TW;
-    hipLaunchKernelGGL(input_scan_kernel, dim3(a.B * nblk * nwin), dim3(64), lds, s, a);
+    const int nblk = (a.n1 + 63) / 64;
+    if (a.TB < 1 || a.S + a.TB - 1 < 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(input_scan_kernel, dim3(a.B * nblk), dim3(64), lds, s, a);
     return hipGetLastError();
 }
 

@@ -49,7 +49,8 @@ struct Topo {
 // Input projection arrivals: A_in[b][n][j] = sum, in emission order, of the
 // input-projection weights arriving at post j of layer 1 at step n.
 struct InScanArgs {
-    int B, T, S, n_in, n1, TW;         // TW: arrival steps per workgroup window
+    int B, T, S, n_in, n1, TB;         // TB: step span of an 8-event chunk on the fast path;
+                                       // the LDS ring holds S + TB - 1 arrival steps
     const uint2* ws0;                  // input projection (weight bits, slot) [n_in][n1]
     const int* in_neuron;
     const int* in_step;
