@@ -709,6 +709,7 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
                 if (t.pre[p] != l || t.kind[q] != SNN_LIF) continue;
                 y.ws[y.npost] = net->ws + t.woff[p];
                 y.nq[y.npost] = t.n[q];
+                y.npre[y.npost] = t.n[l];
                 y.qring_lds[y.npost] = net->bring_mode[q] >= 0 ? net->bring_mode[q] : -1;
                 y.qring[y.npost] = net->bring[q];
                 ++y.npost;
@@ -720,6 +721,7 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
                     if (t.pre[p] == 0 || t.kind[q] != SNN_LIF) continue;
                     y.ws[k] = net->ws + t.woff[p];
                     y.nq[k] = t.n[q];
+                    y.npre[k] = t.n[t.pre[p]];
                     y.qring_lds[k] = net->bring_mode[q] >= 0 ? net->bring_mode[q] : -1;
                     y.qring[k] = net->bring[q];
                 }

@@ -124,10 +124,17 @@ struct BwdCore {
     static constexpr int ROW4 = (2 + KP + 3) / 4;      // int4 loads of a spike-table row
     typedef BwdState<NL, KP, NPA> State;
 
-    // Spike-table row of step x: count, record index, first KP neurons.
+    // Spike-table row of step x: count, record index, first KP neurons.  The
+    // row is the same for every lane, but its address carries a per-lane zero
+    // that the compiler cannot see through: a load it knows to be uniform has
+    // its result moved to scalar registers right where it lands, which would
+    // wait for it there; these values are made scalar a step later, at use.
     static __device__ __forceinline__ void load_row(const BwdLayer& y, int b, int T, int x, int& cnt,
                                                     int& ri, int (&ids)[KP]) {
-        const int4* rp = reinterpret_cast<const int4*>(y.steptab + ((size_t)b * T + x) * SNN_STEP_ROW);
+        int zero;
+        asm volatile("v_mov_b32 %0, 0" : "=v"(zero));
+        const int4* rp =
+            reinterpret_cast<const int4*>(y.steptab + ((size_t)b * T + x) * SNN_STEP_ROW) + zero;
         int v[ROW4 * 4];
 #pragma unroll
         for (int k = 0; k < ROW4; ++k) {
@@ -163,11 +170,15 @@ struct BwdCore {
 #pragma unroll
             for (int pp = 0; pp < NP; ++pp) {
                 const int nq = y.nq[pp];
-                const unsigned col8 = (unsigned)min(tid, nq - 1) * 8u;
+                // rows past the entry's own (a stand-in entry may have fewer
+                // than y.n) read as zero; such entries are masked anyway
+                const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                    (void*)y.ws[pp], (short)0, y.npre[pp] * nq * 8, 0x00020000);
+                const int col8 = min(tid, nq - 1) * 8;
 #pragma unroll
                 for (int q = q0; q < q0 + 4; ++q) {
-                    const char* row = reinterpret_cast<const char*>(y.ws[pp] + (size_t)idc[q] * nq);
-                    ws[pp][q] = *reinterpret_cast<const uint2*>(row + col8);
+                    const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, col8, idc[q] * nq * 8, 0);
+                    ws[pp][q] = make_uint2((unsigned)v[0], (unsigned)v[1]);
                 }
             }
 #pragma unroll
@@ -187,11 +198,11 @@ struct BwdCore {
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
             load_row(a.ly[l], b, a.T, max(n - 2, 0), B.cnt2[l], B.ri2[l], B.id2[l]);
-            B.cnt3[l] = A.cnt2[l];
-            B.ri3[l] = A.ri2[l];
+            B.cnt3[l] = __builtin_amdgcn_readfirstlane(A.cnt2[l]);
+            B.ri3[l] = __builtin_amdgcn_readfirstlane(A.ri2[l]);
 #pragma unroll
             for (int q = 0; q < KP; ++q) B.id3[l][q] = A.id2[l][q];
-            load_step(a, b, tid, l, A.ri2[l], A.cnt2[l], A.id2[l], 0, B.ws[l], B.mine[l], B.I[l],
+            load_step(a, b, tid, l, B.ri3[l], B.cnt3[l], A.id2[l], 0, B.ws[l], B.mine[l], B.I[l],
                       B.A2[l]);
         }
     }
@@ -368,6 +379,8 @@ struct BwdCore {
         for (int l = 0; l < NL; ++l) {
             load_row(a.ly[l], b, T, T - 1, A.cnt3[l], A.ri3[l], A.id3[l]);
             load_row(a.ly[l], b, T, max(T - 2, 0), A.cnt2[l], A.ri2[l], A.id2[l]);
+            A.cnt3[l] = __builtin_amdgcn_readfirstlane(A.cnt3[l]);
+            A.ri3[l] = __builtin_amdgcn_readfirstlane(A.ri3[l]);
             load_step(a, b, tid, l, A.ri3[l], A.cnt3[l], A.id3[l], 0, A.ws[l], A.mine[l], A.I[l],
                       A.A2[l]);
         }

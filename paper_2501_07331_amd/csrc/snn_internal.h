@@ -144,6 +144,7 @@ struct BwdLayer {
                                        // entries past npost repeat a valid projection (loads stay
                                        // in bounds; their contributions are masked)
     int nq[2];                         // their post layer's neurons,
+    int npre[2];                       //   rows of ws (an entry past npost may have fewer than n),
     int qring_lds[2];                  //   adjoint ring (LDS float offset, or -1: global qring)
     float* qring[2];
     const uint2* ws[2];                //   (weight bits, slot) [n][nq]

@@ -223,3 +223,33 @@ def test_backward_before_forward_and_invalid_inputs():
             net.backward(dW, [x.clone() for x in dW])
         assert e.value.code == snn.SNN_ESTATE
     assert fwd() == 0      # the handle is still usable
+
+
+def test_parity_two_layers_of_unequal_width():
+    """A 32-neuron recurrent layer feeding a 96-neuron recurrent one: the
+    narrow layer has two LIF-post projections and the wide one a single one,
+    so the wide layer's unused projection entry stands in with the 32-row
+    recurrent matrix of the narrow layer (its loads must stay in its rows).
+    Both layers spike (about 15 and 20 spikes per neuron and sample)."""
+    import dataclasses
+
+    from workloads import Workload
+    from workloads.configs import CONFIGS
+    from workloads.generators import input_spikes, labels
+
+    cfg = dataclasses.replace(CONFIGS[3], name="uneven-12-32rec-96rec-27",
+                              layers=((12, 0, 0), (32, 1, 1), (96, 1, 1), (27, 2, 0)),
+                              delay_range=(25, 25, 25, 25, 25))
+    B, T = 6, 300
+    off, st, ne = input_spikes(cfg, B, T=T)
+    shapes = [(12, 32), (32, 32), (32, 96), (96, 96), (96, 27)]
+    mus = (1.4, 0.0, 0.25, 0.0, 0.05)
+    rng = np.random.default_rng(77)
+    W = [rng.normal(m, 0.3 if p in (0, 2) else 0.05, size=s).astype(np.float32)
+         for p, (m, s) in enumerate(zip(mus, shapes))]
+    D = [rng.uniform(0.0, 25.0, size=s).astype(np.float32) for s in shapes]
+    wl = Workload(cfg, B, T, off, st, ne, W, D, labels(cfg, B))
+    import paper_2501_07331_amd as snn
+    gpu, orc = _parity(wl)
+    assert all(int(c.sum()) > 0 for c in orc["fwd"].count)
+    _parity(wl, flags=snn.SNN_FLAG_HBM_RINGS)
