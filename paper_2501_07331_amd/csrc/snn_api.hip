@@ -30,7 +30,7 @@ struct snn_net {
     int bpart_off;              // backward-core LDS plan
     int bring_mode[SNN_MAX_LAYERS];   // adjoint ring of a LIF layer: -2 none, -1 HBM, >= 0 LDS
     int radj_threads, radj_tab;
-    int grad_J, grad_threads, grad_SB, grad_bs, grad_nblk, grad_ngroups;
+    int grad_J, grad_KL, grad_threads, grad_SB, grad_bs, grad_nblk, grad_ngroups, grad_spcap;
     GradGroup grad_grp[SNN_MAX_LAYERS];
     hipStream_t stream;
     long long n_params;
@@ -312,9 +312,13 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     net->lds_radj = net->radj_tab ? (size_t)t.T * C * sizeof(float) : 0;
     // gradients: one group per post layer (its projections in projection
     // order), J posts per workgroup, samples split into SB blocks so that the
-    // grid has about 512 workgroups; workgroups in units of 4 J-blocks
+    // grid has about 512 workgroups; workgroups in units of 4 J-blocks.  LDS:
+    // the J trajectories of a sample [J][T] float2 (J = 8, 4 or 1: the
+    // largest within 64 KiB), then room for the sample's spike steps (16-bit)
+    // up to 96 KiB in all, when that leaves any
     {
-        net->grad_J = ((size_t)8 * t.T * 2 * sizeof(float) <= kLds) ? 8 : 1;
+        const size_t tj = (size_t)t.T * 2 * sizeof(float);
+        net->grad_J = (8 * tj <= 64 * 1024) ? 8 : (4 * tj <= 64 * 1024) ? 4 : 1;
         const int J = net->grad_J;
         int ng = 0, jblocks = 0, maxpre = 64;
         for (int q = 1; q < n_layers; ++q) {
@@ -349,8 +353,14 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         net->grad_SB = SB;
         net->grad_bs = bs;
         net->grad_nblk = blk;
-        net->grad_threads = std::min(1024, ((maxpre + 63) / 64) * 64);
-        net->lds_grad = (size_t)J * t.T * 2 * sizeof(float);
+        // synapses of a block: J x maxpre, dealt KL per lane (one pass when they fit)
+        const int pairs = J * maxpre;
+        net->grad_KL = (pairs <= 4 * 1024) ? 4 : 8;
+        net->grad_threads = std::min(1024, ((pairs + net->grad_KL - 1) / net->grad_KL + 63) / 64 * 64);
+        const size_t traj = (size_t)J * t.T * 2 * sizeof(float);
+        const size_t room = (traj < 96 * 1024) ? 96 * 1024 - traj : 0;
+        net->grad_spcap = (int)(room / sizeof(unsigned short)) & ~7;
+        net->lds_grad = traj + (size_t)net->grad_spcap * sizeof(unsigned short);
     }
 
     // ---- device scratch
@@ -772,6 +782,7 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
     ga.B = t.B;
     ga.T = t.T;
     ga.SB = net->grad_SB;
+    ga.spcap = net->grad_spcap;
     ga.bs = net->grad_bs;
     ga.lif_total = t.lif_total;
     ga.C = C;
@@ -801,7 +812,7 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
     for (int g = 0; g < net->grad_ngroups; ++g) ga.grp[g] = net->grad_grp[g];
     ga.part = net->gpart;
     if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GRAD], s));
-    HIP_TRY(net, launch_gradients(ga, net->grad_J, net->grad_threads, net->lds_grad, s));
+    HIP_TRY(net, launch_gradients(ga, net->grad_J, net->grad_KL, net->grad_threads, net->lds_grad, s));
     if (ga.SB > 1) HIP_TRY(net, launch_grad_reduce(ga, t.P, s));
     if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GRAD + 1], s));
     int rc = read_status(net);

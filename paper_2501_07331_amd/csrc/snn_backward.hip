@@ -465,11 +465,22 @@ __global__ void __launch_bounds__(1024) group_kernel(GroupArgs a) {
 // dL/dw_ij = -tau_s sum_spikes lambda_I,j(t + d_ij) and dL/dd_ij = -w_ij
 // sum_spikes (lambda_I - lambda_V)_j(t + d_ij), per step of delay (x dt).
 //
-// Workgroups come in units of four J-post blocks that share 128-byte lines of
-// the [B][T][N] trajectories; a unit's four blocks have indices 8 apart, so
-// with round-robin dispatch over the 8 XCDs they run on one XCD and share its
-// L2.
-template <int J>
+// Workgroup = (post layer, block of J posts, block of samples).  The J x V
+// synapses into the block (V presynaptic neurons over the layer's
+// projections) are dealt to lanes: lane l owns pairs p = l + nt k, post
+// p % J of presynaptic neuron p / J.  Within a wave the neurons are adjacent
+// (similar spike counts, little divergence) and a lane's neurons lie nt / J
+// apart, so every lane sums about the same number of spikes however the
+// input concentrates on some channels.  Per sample the J post trajectories
+// and the sample's grouped spike steps are staged in LDS; each lane sums, per
+// synapse and in spike order, lambda_I and w (lambda_I - lambda_V) at the
+// delayed arrivals in fp32, then adds the sample's sums in fp64.  Sample
+// blocks are reduced in a fixed order: no atomics, deterministic.
+//
+// Workgroups come in units of four J-post blocks that share lines of the
+// [B][T][N] trajectories; a unit's four blocks have indices 8 apart, so with
+// round-robin dispatch over the 8 XCDs they run on one XCD and share its L2.
+template <int J, int KL>
 __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
     const int tid = threadIdx.x, nt = blockDim.x;
     int g = 0;
@@ -483,91 +494,105 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
     if (jb >= G.jb) return;
     const int nq = G.nq, j0 = jb * J, nj = min(J, nq - j0);
     const int T = a.T;
-    float2* st = reinterpret_cast<float2*>(smem);              // [J][T]: random steps spread banks
+    float2* st = reinterpret_cast<float2*>(smem);              // [J][T]
+    unsigned short* sp = reinterpret_cast<unsigned short*>(smem + (size_t)J * T * sizeof(float2));
     const float* tu = G.out ? a.tu_out : a.tu_lif;
     const float* td = G.out ? a.td_out : a.td_lif;
     const int LN = G.out ? a.C : a.lif_total;
-    const int vtot = G.npre[0] + (G.np > 1 ? G.npre[1] : 0);
+    const int n0 = G.npre[0], n1 = (G.np > 1) ? G.npre[1] : 0;
+    const int vtot = n0 + n1;
+    const int* go0 = a.g_off[G.pre[0]];
+    const int* go1 = a.g_off[G.pre[G.np > 1 ? 1 : 0]];
+    const int* gs0 = a.g_step[G.pre[0]];
+    const int* gs1 = a.g_step[G.pre[G.np > 1 ? 1 : 0]];
     const int b0 = sb * a.bs, b1 = min(a.B, b0 + a.bs);
-    for (int v0 = 0; v0 < vtot; v0 += nt) {
-        const int v = v0 + tid;
-        const bool live = v < vtot;
-        const int pi = (live && v >= G.npre[0]) ? 1 : 0;
-        const int i = v - (pi ? G.npre[0] : 0);
-        const int p = G.p[pi], pre = G.pre[pi], npre = G.npre[pi];
-        float w[J];
-        int s[J];
+    for (int pbase = 0; pbase < J * vtot; pbase += nt * KL) {
+        // this lane's synapses, one word each: presynaptic index (bits 0-15),
+        // post within the block (16-19), projection part (20), slot (21-28);
+        // -1: none
+        int dsc[KL];
+        float w[KL];
 #pragma unroll
-        for (int jj = 0; jj < J; ++jj) {
-            w[jj] = 0.0f;
-            s[jj] = T;                                         // never arrives
-            if (live && jj < nj) {
-                const uint2 e = a.ws[a.woff[p] + (size_t)i * nq + j0 + jj];
-                w[jj] = __uint_as_float(e.x);
-                s[jj] = (int)e.y;
+        for (int k = 0; k < KL; ++k) {
+            const int p = pbase + tid + nt * k;
+            const int v = p / J, q = p % J;
+            dsc[k] = -1;
+            w[k] = 0.0f;
+            if (p < J * vtot && q < nj) {
+                const int pi = (v >= n0) ? 1 : 0, i = v - (pi ? n0 : 0);
+                const uint2 e = a.ws[a.woff[G.p[pi]] + (size_t)i * nq + j0 + q];
+                w[k] = __uint_as_float(e.x);
+                dsc[k] = i | (q << 16) | (pi << 20) | ((int)e.y << 21);
             }
         }
-        double su[J], sd[J];
+        double su[KL], sd[KL];
 #pragma unroll
-        for (int jj = 0; jj < J; ++jj) {
-            su[jj] = 0.0;
-            sd[jj] = 0.0;
+        for (int k = 0; k < KL; ++k) {
+            su[k] = 0.0;
+            sd[k] = 0.0;
         }
         for (int b = b0; b < b1; ++b) {
             __syncthreads();
+            // spike lists of this lane's neurons (offsets into g_step)
+            int lo[KL], hi[KL];
+#pragma unroll
+            for (int k = 0; k < KL; ++k) {
+                const int i = dsc[k] & 0xFFFF, pi = (dsc[k] >> 20) & 1;
+                const int* go = pi ? go1 + (size_t)b * (n1 + 1) : go0 + (size_t)b * (n0 + 1);
+                lo[k] = (dsc[k] >= 0) ? go[i] : 0;
+                hi[k] = (dsc[k] >= 0) ? go[i + 1] : 0;
+            }
+            // the sample's grouped spike steps of both presynaptic layers
+            const int s0 = go0[(size_t)b * (n0 + 1)], e0 = go0[(size_t)b * (n0 + 1) + n0];
+            const int s1 = n1 ? go1[(size_t)b * (n1 + 1)] : 0, e1 = n1 ? go1[(size_t)b * (n1 + 1) + n1] : 0;
+            const int c0 = e0 - s0, c1 = e1 - s1;
+            const bool in_lds = c0 + c1 <= a.spcap;
+            if (in_lds) {
+                for (int x = tid; x < c0 + c1; x += nt)
+                    sp[x] = (unsigned short)((x < c0) ? gs0[s0 + x] : gs1[s1 + x - c0]);
+            }
+            // the J post trajectories of the sample
             const size_t base = (size_t)b * T * LN + G.off + j0;
             for (int e = tid; e < T * J; e += nt) {
-                const int m = e / J, jj = e % J;
+                const int m = e / J, q = e % J;
                 float2 x = make_float2(0.0f, 0.0f);
-                if (jj < nj) x = make_float2(tu[base + (size_t)m * LN + jj], td[base + (size_t)m * LN + jj]);
-                st[jj * T + m] = x;
+                if (q < nj) x = make_float2(tu[base + (size_t)m * LN + q], td[base + (size_t)m * LN + q]);
+                st[q * T + m] = x;
             }
             __syncthreads();
-            if (!live) continue;
-            const int* go = a.g_off[pre] + (size_t)b * (npre + 1) + i;
-            const int lo = go[0], hi = go[1];
-            const int* gs = a.g_step[pre];
-            float pu[J], pd[J];
 #pragma unroll
-            for (int jj = 0; jj < J; ++jj) {
-                pu[jj] = 0.0f;
-                pd[jj] = 0.0f;
-            }
-            for (int x = lo; x < hi; x += 4) {
-                int nn[4];
-#pragma unroll
-                for (int k = 0; k < 4; ++k) nn[k] = (x + k < hi) ? gs[x + k] : T;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-#pragma unroll
-                    for (int jj = 0; jj < J; ++jj) {
-                        const int m = nn[k] + s[jj];
-                        if (m <= T - 1) {
-                            const float2 ud = st[jj * T + m];
-                            pu[jj] = __fadd_rn(pu[jj], ud.x);
-                            pd[jj] = __fadd_rn(pd[jj], __fmul_rn(w[jj], ud.y));
-                        }
+            for (int k = 0; k < KL; ++k) {
+                if (dsc[k] < 0) continue;
+                const int pi = (dsc[k] >> 20) & 1, sl = (dsc[k] >> 21) & 0xFF;
+                const float2* stk = st + ((dsc[k] >> 16) & 0xF) * T;
+                const int* gs = pi ? gs1 : gs0;
+                const int off = pi ? c0 - s1 : -s0;                 // LDS index = x + off
+                float pu = 0.0f, pd = 0.0f;
+                for (int x = lo[k]; x < hi[k]; ++x) {
+                    const int t = in_lds ? (int)sp[x + off] : gs[x];
+                    const int m = t + sl;
+                    if (m <= T - 1) {
+                        const float2 ud = stk[m];
+                        pu = __fadd_rn(pu, ud.x);
+                        pd = __fadd_rn(pd, __fmul_rn(w[k], ud.y));
                     }
                 }
-            }
-#pragma unroll
-            for (int jj = 0; jj < J; ++jj) {
-                su[jj] += (double)pu[jj];
-                sd[jj] += (double)pd[jj];
+                su[k] += (double)pu;
+                sd[k] += (double)pd;
             }
         }
-        if (!live) continue;
 #pragma unroll
-        for (int jj = 0; jj < J; ++jj) {
-            if (jj >= nj) continue;
-            const size_t kk = (size_t)i * nq + j0 + jj;
+        for (int k = 0; k < KL; ++k) {
+            if (dsc[k] < 0) continue;
+            const int p = G.p[(dsc[k] >> 20) & 1];
+            const size_t kk = (size_t)(dsc[k] & 0xFFFF) * nq + j0 + ((dsc[k] >> 16) & 0xF);
             if (a.SB == 1) {
-                a.dW[p][kk] = (float)(-(double)a.tau_s * su[jj]);
-                a.dD[p][kk] = (float)(-(double)a.dt * sd[jj]);
+                a.dW[p][kk] = (float)(-(double)a.tau_s * su[k]);
+                a.dD[p][kk] = (float)(-(double)a.dt * sd[k]);
             } else {
                 const size_t gi = (size_t)a.woff[p] + kk;
-                a.part[((size_t)sb * 2 + 0) * a.nparams + gi] = su[jj];
-                a.part[((size_t)sb * 2 + 1) * a.nparams + gi] = sd[jj];
+                a.part[((size_t)sb * 2 + 0) * a.nparams + gi] = su[k];
+                a.part[((size_t)sb * 2 + 1) * a.nparams + gi] = sd[k];
             }
         }
     }
@@ -648,14 +673,20 @@ hipError_t launch_group(const GroupArgs& a, int B, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_gradients(const GradArgs& a, int J, int threads, size_t lds, hipStream_t s) {
-    if (J == 8)
-        hipLaunchKernelGGL(gradients_kernel<8>, dim3(a.nblk), dim3(threads), lds, s, a);
-    else if (J == 1)
-        hipLaunchKernelGGL(gradients_kernel<1>, dim3(a.nblk), dim3(threads), lds, s, a);
-    else
-        return hipErrorInvalidValue;
-    return hipGetLastError();
+hipError_t launch_gradients(const GradArgs& a, int J, int KL, int threads, size_t lds, hipStream_t s) {
+#define SNN_GRAD(JJ, KK)                                                                         \
+    if (J == JJ && KL == KK) {                                                                   \
+        hipLaunchKernelGGL((gradients_kernel<JJ, KK>), dim3(a.nblk), dim3(threads), lds, s, a); \
+        return hipGetLastError();                                                                \
+    }
+    SNN_GRAD(8, 4)
+    SNN_GRAD(8, 8)
+    SNN_GRAD(4, 4)
+    SNN_GRAD(4, 8)
+    SNN_GRAD(1, 4)
+    SNN_GRAD(1, 8)
+#undef SNN_GRAD
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_grad_reduce(const GradArgs& a, int P, hipStream_t s) {
@@ -672,8 +703,10 @@ hipError_t launch_grad_reduce(const GradArgs& a, int P, hipStream_t s) {
 
 hipError_t set_backward_lds_limits(size_t bytes, int* bad) {
     const void* fns[] = {(const void*)readout_adjoint_kernel, CORE_FNS(256), CORE_FNS(1024),
-                         (const void*)group_kernel, (const void*)gradients_kernel<8>,
-                         (const void*)gradients_kernel<1>};
+                         (const void*)group_kernel, (const void*)gradients_kernel<8, 4>,
+                         (const void*)gradients_kernel<8, 8>, (const void*)gradients_kernel<4, 4>,
+                         (const void*)gradients_kernel<4, 8>, (const void*)gradients_kernel<1, 4>,
+                         (const void*)gradients_kernel<1, 8>};
     for (int i = 0; i < (int)(sizeof(fns) / sizeof(fns[0])); ++i) {
         const hipError_t e =
             hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);

@@ -227,25 +227,25 @@ __device__ __forceinline__ void word_ids(const unsigned long long (&m)[NWM],
 constexpr int kWaitVm0 = 0x0F70;
 
 // Adds w[k] to cell row[k] of one lane's column (cell r at col[r * stride])
-// for k = 0 .. KB-1 in order, where every row is valid (out-of-range entries
+// for k = 0 .. K-1 in order, where every row is valid (out-of-range entries
 // point at a dummy row that is never read out).  Reads first, equal rows
 // merged in registers, then the writes: the same fp32 result as one
 // read-modify-write per entry in order, without branches.
-template <typename Ptr>
-__device__ __forceinline__ void column_add_all(Ptr col, int stride, const int (&row)[KB],
-                                               const float (&w)[KB]) {
-    float v[KB];
+template <typename Ptr, int K>
+__device__ __forceinline__ void column_add_all(Ptr col, int stride, const int (&row)[K],
+                                               const float (&w)[K]) {
+    float v[K];
 #pragma unroll
-    for (int k = 0; k < KB; ++k) v[k] = col[row[k] * stride];
+    for (int k = 0; k < K; ++k) v[k] = col[row[k] * stride];
 #pragma unroll
-    for (int k = 0; k < KB; ++k) {
+    for (int k = 0; k < K; ++k) {
         float base = v[k];
 #pragma unroll
         for (int j = 0; j < k; ++j) base = (row[j] == row[k]) ? v[j] : base;
         v[k] = __fadd_rn(base, w[k]);
     }
 #pragma unroll
-    for (int k = 0; k < KB; ++k) col[row[k] * stride] = v[k];
+    for (int k = 0; k < K; ++k) col[row[k] * stride] = v[k];
 }
 
 // Delayed scatter of a sorted event list into a table, one column per lane:

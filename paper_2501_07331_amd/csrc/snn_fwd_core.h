@@ -5,9 +5,9 @@
 // every delay ring into that layer.
 //
 // Per step n: free dynamics, threshold and reset, wave ballots into LDS, one
-// barrier, spike records, the delayed scatter of the spikes into the rings of
-// the LIF-post projections, and the arrivals (ring row n, projection by
-// projection in projection order).  A ring cell sums its weights in emission
+// barrier, the delayed scatter of the spikes into the rings of the LIF-post
+// projections, the spike records, and the arrivals (ring row n, projection
+// by projection in projection order).  A ring cell sums its weights in emission
 // order (step, then presynaptic neuron).
 //
 // Deferred scatter (rings in LDS, few zero-delay synapses): the weights and
@@ -35,7 +35,8 @@ constexpr int kZMax = SNN_ZMAX;   // zero-delay synapses per lane and projection
 template <int MAXT, int NL, int NP, bool RL>
 struct FwdCore {
     static constexpr int NWM = MAXT / 64;
-    static constexpr int KP = (NL == 1) ? 16 : 4;    // spikes per step with prefetched weights
+    static constexpr int KP = (NL == 1) ? 8 : 4;     // spikes per step with prefetched weights
+    static constexpr int KS = 4;                      // spikes per column_add_all of the deferred scatter
     static constexpr int NPA = NP > 0 ? NP : 1;
     // the deferred scatter's register lists fit without spills for one LIF
     // layer, or two with one LIF-post projection each, at 256 threads (and it
@@ -93,8 +94,9 @@ struct FwdCore {
     }
 
     // Adds the weights of spikes 0 .. N) (valid below cnt) emitted at step e to
-    // the ring cells of their arrivals, slots >= smin, arrivals before T.
-    template <int N>
+    // the ring cells of their arrivals, slots >= smin, arrivals before T, in
+    // chunks of C.
+    template <int N, int C>
     static __device__ __forceinline__ void scatter(const CoreFwdArgs& a, int b, int l, int pp, int tid,
                                                    int e, int cnt, int smin, const uint2 (&w)[N]) {
         const FwdLayer& y = a.ly[l];
@@ -103,12 +105,12 @@ struct FwdCore {
         const int e_mod = e % S;
         RingPtr col = ring_col<RingPtr>(a, b, l, pp, min(tid, nq - 1));
 #pragma unroll
-        for (int q0 = 0; q0 < N; q0 += KB) {
+        for (int q0 = 0; q0 < N; q0 += C) {
             if (cnt <= q0) continue;
-            int row[KB];
-            float wv[KB];
+            int row[C];
+            float wv[C];
 #pragma unroll
-            for (int k = 0; k < KB; ++k) {
+            for (int k = 0; k < C; ++k) {
                 const int q = q0 + k;
                 const int s = (int)w[q].y;
                 int r = e_mod + s;
@@ -136,7 +138,7 @@ struct FwdCore {
                 if (pp >= y.npost) continue;
                 uint2 w[KB];
                 load_ws<KB>(a, l, pp, tid, ids, w);
-                scatter<KB>(a, b, l, pp, tid, e, total - q0, smin, w);
+                scatter<KB, KB>(a, b, l, pp, tid, e, total - q0, smin, w);
             }
         }
     }
@@ -148,8 +150,6 @@ struct FwdCore {
         const int T = a.T, S = a.S, NW = a.NW;
         unsigned long long* masks = reinterpret_cast<unsigned long long*>(smem + a.mask_off);
         const int par = n % 3;
-        // loads issued a step ago (P) have landed
-        __builtin_amdgcn_s_waitcnt(kWaitVm0);
 
         // ---- free dynamics over one step, threshold, reset, ballots
         bool spk[NL];
@@ -168,13 +168,13 @@ struct FwdCore {
         }
         __syncthreads();
 
-        // ---- spike records (ascending neuron order) and the step's first KP spikes
+        // ---- counts, this lane's rank among the step's spikes (ascending
+        // neuron order) and the step's first KP spikes
         unsigned long long mw[NL][NWM];
         int ids[NL][KP];
-        int tot[NL];
+        int tot[NL], rank[NL], cnt0[NL];
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
-            const FwdLayer& y = a.ly[l];
             row_words<NWM>(masks + (size_t)(par * NL + l) * NW, NW, mw[l]);
             int before = 0, total = 0;
             unsigned long long own = 0;
@@ -185,32 +185,17 @@ struct FwdCore {
                 before += (w < wave) ? c : 0;
                 own = (w == wave) ? mw[l][w] : own;
             }
-            int* row = y.steptab + ((size_t)b * T + n) * SNN_STEP_ROW;
-            if (tid == 0) {
-                // internal record indices never pass the capacity (the
-                // caller's count stays exact)
-                y.rec_idx[(size_t)b * (T + 1) + n] = min(L.cnt[l], a.cap);
-                row[0] = total;
-                row[1] = min(L.cnt[l], a.cap);
-            }
-            if (spk[l]) {
-                const int rank = before + lanes_below(own);
-                if (rank < SNN_STEP_IDS) row[2 + rank] = tid;
-                const int pos = L.cnt[l] + rank;
-                if (pos < a.cap) {
-                    const size_t r = (size_t)b * a.cap + pos;
-                    y.rec_n[r] = tid;
-                    y.rec_s[r] = n;
-                    y.rec_I[r] = L.I[l];
-                    y.out_step[r] = n;
-                    y.out_neuron[r] = tid;
-                }
-            }
-            if (tid == 0 && L.cnt[l] + total > a.cap) a.st->overflow = 1;
+            rank[l] = before + lanes_below(own);
+            cnt0[l] = L.cnt[l];
             L.cnt[l] += total;
             tot[l] = total;
             word_ids<NWM, KP>(mw[l], masks + (size_t)(par * NL + l) * NW, NW, 0, ids[l]);
         }
+
+        // loads issued a step ago (P) have landed; waiting here, not at the
+        // step start, lets the dynamics, the barrier and the ids above cover
+        // their latency (no stores of this step are in flight yet)
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
 
         if constexpr (DEFER) {
             // ---- step n - 1's spikes into the rings (delays >= 1), weights loaded then
@@ -219,7 +204,8 @@ struct FwdCore {
                 for (int l = 0; l < NL; ++l) {
 #pragma unroll
                     for (int pp = 0; pp < NP; ++pp) {
-                        if (pp < a.ly[l].npost) scatter<KP>(a, b, l, pp, tid, n - 1, P.cnt[l], 1, P.ws[l][pp]);
+                        if (pp < a.ly[l].npost)
+                            scatter<KP, KS>(a, b, l, pp, tid, n - 1, P.cnt[l], 1, P.ws[l][pp]);
                     }
                     if (P.cnt[l] > KP) {
                         const unsigned long long* prow = masks + (size_t)(((n - 1) % 3) * NL + l) * NW;
@@ -245,6 +231,33 @@ struct FwdCore {
                 scatter_rest(a, b, l, tid, n, mw[l], masks + (size_t)(par * NL + l) * NW, 0, tot[l], 0);
         }
         N.ain = a.A_in[((size_t)b * T + min(n + 1, T - 1)) * a.n1 + min(tid, a.n1 - 1)];
+
+        // ---- spike records (I- of this step), step table, overflow
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            const FwdLayer& y = a.ly[l];
+            int* row = y.steptab + ((size_t)b * T + n) * SNN_STEP_ROW;
+            if (tid == 0) {
+                // internal record indices never pass the capacity (the
+                // caller's count stays exact)
+                y.rec_idx[(size_t)b * (T + 1) + n] = min(cnt0[l], a.cap);
+                row[0] = tot[l];
+                row[1] = min(cnt0[l], a.cap);
+            }
+            if (spk[l]) {
+                if (rank[l] < SNN_STEP_IDS) row[2 + rank[l]] = tid;
+                const int pos = cnt0[l] + rank[l];
+                if (pos < a.cap) {
+                    const size_t r = (size_t)b * a.cap + pos;
+                    y.rec_n[r] = tid;
+                    y.rec_s[r] = n;
+                    y.rec_I[r] = L.I[l];
+                    y.out_step[r] = n;
+                    y.out_neuron[r] = tid;
+                }
+            }
+            if (tid == 0 && cnt0[l] + tot[l] > a.cap) a.st->overflow = 1;
+        }
 
         // ---- arrivals at step n: per projection into the layer, in projection order
         const int n_mod = n % S;

@@ -195,6 +195,7 @@ struct GradGroup {
 
 struct GradArgs {
     int B, T, SB, bs, lif_total, C, ngroups, nblk;
+    int spcap;                         // LDS capacity for a sample's spike steps (16-bit), 0: none
     float tau_s, dt;
     long long nparams;
     const float* tu_lif;               // [B][T][lif_total]
@@ -232,7 +233,7 @@ hipError_t launch_readout_adjoint(const ReadoutBwdArgs& a, int threads, size_t l
 hipError_t launch_backward_core(const CoreBwdArgs& a, int n_lif, int threads, size_t lds,
                                 hipStream_t s);
 hipError_t launch_group(const GroupArgs& a, int B, hipStream_t s);
-hipError_t launch_gradients(const GradArgs& a, int J, int threads, size_t lds, hipStream_t s);
+hipError_t launch_gradients(const GradArgs& a, int J, int KL, int threads, size_t lds, hipStream_t s);
 hipError_t launch_grad_reduce(const GradArgs& a, int P, hipStream_t s);
 hipError_t set_forward_lds_limits(size_t bytes, int* bad);
 hipError_t set_core_lds_limits(size_t bytes, int* bad);
