@@ -295,7 +295,12 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     net->scan_tb = std::max(8, std::min(64, 160 - t.S));
     net->lds_scan = (size_t)(t.S + net->scan_tb) * 64 * sizeof(float);
     // readout forward: arrival table [T + 1][C] (row T: dummy) in LDS when it fits
-    net->read_threads = ((C + 63) / 64) * 64;
+    // readout: groups of ceil(C / 64) waves, each building a window of the
+    // arrival table; up to 1024 threads
+    {
+        const int ob = (C + 63) / 64;
+        net->read_threads = 64 * ob * std::max(1, 16 / ob);
+    }
     {
         const size_t tab = align16((size_t)(t.T + 1) * C * sizeof(float));
         if (!hbm && tab <= kLds) {

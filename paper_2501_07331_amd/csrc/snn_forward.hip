@@ -207,37 +207,51 @@ __global__ void __launch_bounds__(64) input_scan_kernel(InScanArgs a) {
 
 // ------------------------------------------------------------------ readout
 
-// One workgroup per sample, lane k owns output neuron k.  table_lds >= 0:
-// the arrival table [T + 1][C] (row T: dummy) lives in LDS; else in global
-// memory ([B][T + 1][C], sized by the host for this case).
+// One workgroup per sample.  Waves come in groups of OB = ceil(C / 64), lane
+// k of a group owning output neuron k; group g builds rows [g W, (g + 1) W)
+// of the arrival table [T + 1][C] (row T: dummy), scattering the records
+// emitted in its rows or in the S - 1 steps before them, in emission order,
+// so the groups work on disjoint rows in parallel.  Then group 0 runs the LI
+// layer over the T steps.  table_lds >= 0: the table lives in LDS; else in
+// global memory ([B][T + 1][C], sized by the host for this case).
 __global__ void __launch_bounds__(1024) readout_forward_kernel(ReadoutArgs a) {
     const Topo& t = a.t;
     if (a.st->bad_input) return;
-    const int b = blockIdx.x, k = threadIdx.x;
+    const int b = blockIdx.x, tid = threadIdx.x;
     const int C = t.n[t.out_l], T = t.T;
+    const int OB = (C + 63) >> 6, ngrp = max(1, (int)(blockDim.x >> 6) / OB);
+    const int wave = tid >> 6, grp = wave / OB;
+    const int k = (wave % OB) * 64 + (tid & 63);
     const int pa = t.pre[t.out_p];
     float* lds = reinterpret_cast<float*>(smem);
     const bool in_lds = a.table_lds >= 0;
-    // table [T + 1][C] (row T: dummy); lanes past C share column C - 1's
-    // dummy cell and touch nothing else
+    // lanes past C share column C - 1's dummy cell and touch nothing else
     const int kc = min(k, C - 1);
     lds_f32* lcol = (lds_f32*)(lds + (in_lds ? a.table_lds : 0)) + kc;
     global_f32* gcol = in_lds ? nullptr : (global_f32*)(a.table + (size_t)b * (T + 1) * C) + kc;
     if (pa != 0) {
-        // arrival table of the feeding layer's spikes, in emission order
-        if (k < C) {
-            for (int m = 0; m < T; ++m) {
-                if (in_lds) lcol[m * C] = 0.0f; else gcol[m * C] = 0.0f;
+        const int W = (T + ngrp - 1) / ngrp;
+        const int m0 = min(T, grp * W), m1 = min(T, m0 + W);
+        if (grp < ngrp && m0 < m1) {
+            if (k < C) {
+                for (int m = m0; m < m1; ++m) {
+                    if (in_lds) lcol[m * C] = 0.0f; else gcol[m * C] = 0.0f;
+                }
             }
+            const size_t base = ((size_t)t.lif[pa] * t.B + b) * t.cap;
+            const int* idx = a.rec_idx + ((size_t)t.lif[pa] * t.B + b) * (T + 1);
+            const int e_lo = idx[max(0, m0 - (t.S - 1))], e_hi = idx[m1];
+            const int wsb = t.n[pa] * C * 8;
+            if (in_lds)
+                scatter_events(a.rec_n + base, a.rec_s + base, e_lo, e_hi, a.ws, wsb, C, k, k < C, m0, m1,
+                               T - m0, lcol + m0 * C, C);
+            else
+                scatter_events(a.rec_n + base, a.rec_s + base, e_lo, e_hi, a.ws, wsb, C, k, k < C, m0, m1,
+                               T - m0, gcol + (size_t)m0 * C, C);
         }
-        const size_t base = ((size_t)t.lif[pa] * t.B + b) * t.cap;
-        const int cnt = a.rec_idx[((size_t)t.lif[pa] * t.B + b) * (T + 1) + T];
-        const int wsb = t.n[pa] * C * 8;
-        if (in_lds)
-            scatter_events(a.rec_n + base, a.rec_s + base, 0, cnt, a.ws, wsb, C, k, k < C, 0, T, T, lcol, C);
-        else
-            scatter_events(a.rec_n + base, a.rec_s + base, 0, cnt, a.ws, wsb, C, k, k < C, 0, T, T, gcol, C);
+        __syncthreads();
     }
+    if (grp != 0) return;
     if (k >= C) return;
     const global_f32* ain = (const global_f32*)(a.A_in + (size_t)b * T * C) + k;
     float V = 0.0f, I = 0.0f, acc = 0.0f, best = 0.0f;
