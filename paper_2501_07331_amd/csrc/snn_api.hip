@@ -267,7 +267,7 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         if (t.pre[p] != 0 && t.kind[t.post[p]] == SNN_LIF) read_by_lif[t.post[p]] = true;
     {
         const int NL = std::max(t.n_lif, 1);
-        const int KP = (NL == 1) ? 16 : 4;
+        const int KP = bwd_prefetch(NL);
         net->bpart_off = 0;
         const size_t part = align16((size_t)2 * NL * KP * 4 * nwaves * sizeof(double));
         size_t used = part;

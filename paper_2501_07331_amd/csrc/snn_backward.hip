@@ -625,7 +625,7 @@ hipError_t launch_readout_adjoint(const ReadoutBwdArgs& a, int threads, size_t l
 
 template <int MAXT, int NL, int NP>
 static void launch_core3(const CoreBwdArgs& a, bool rl, int threads, size_t lds, hipStream_t s) {
-    constexpr int KP = (NL == 1) ? 16 : 4;
+    constexpr int KP = bwd_prefetch(NL);
     if (rl)
         hipLaunchKernelGGL((backward_core_kernel<MAXT, NL, KP, NP, true>), dim3(a.B), dim3(threads),
                            lds, s, a);
@@ -695,7 +695,7 @@ hipError_t launch_grad_reduce(const GradArgs& a, int P, hipStream_t s) {
 }
 
 #define CORE_FNS2(M, R)                                                                          \
-    (const void*)backward_core_kernel<M, 1, 16, 0, R>, (const void*)backward_core_kernel<M, 1, 16, 1, R>, \
+    (const void*)backward_core_kernel<M, 1, bwd_prefetch(1), 0, R>, (const void*)backward_core_kernel<M, 1, bwd_prefetch(1), 1, R>, \
     (const void*)backward_core_kernel<M, 2, 4, 1, R>, (const void*)backward_core_kernel<M, 2, 4, 2, R>, \
     (const void*)backward_core_kernel<M, 3, 4, 1, R>, (const void*)backward_core_kernel<M, 3, 4, 2, R>, \
     (const void*)backward_core_kernel<M, 4, 4, 1, R>, (const void*)backward_core_kernel<M, 4, 4, 2, R>

@@ -60,6 +60,12 @@ struct InScanArgs {
 };
 
 // One LIF layer as seen by the forward core.
+// spikes per step of a LIF layer whose data the backward core prefetches a
+// step ahead (more are loaded in further rounds), by LIF layer count; 16
+// covers nearly every step of a 256-neuron layer at 14 spikes per neuron
+// while its input is active (8 left a quarter of them to an extra round)
+constexpr int bwd_prefetch(int n_lif) { return n_lif == 1 ? 16 : 4; }
+
 // zero-delay synapses per post neuron and LIF-post projection that the
 // deferred forward scatter handles from LDS
 #define SNN_ZMAX 16
