@@ -33,6 +33,8 @@ struct snn_net {
     int grad_J, grad_KL, grad_threads, grad_SB, grad_bs, grad_nblk, grad_ngroups, grad_spcap;
     GradGroup grad_grp[SNN_MAX_LAYERS];
     hipStream_t stream;
+    hipStream_t aux;                   // second stream: spike grouping beside the backward sweep
+    hipEvent_t fork, join;             // its start after the caller's work, its end before gradients
     long long n_params;
     long long cnt[SNN_MAXP];
     int n_state;
@@ -114,6 +116,9 @@ static void free_all(snn_net* n) {
     if (n->st_host) (void)hipHostFree(n->st_host);
     for (int i = 0; i < 2 * K_N; ++i)
         if (n->ev[i]) (void)hipEventDestroy(n->ev[i]);
+    if (n->fork) (void)hipEventDestroy(n->fork);
+    if (n->join) (void)hipEventDestroy(n->join);
+    if (n->aux) (void)hipStreamDestroy(n->aux);
 }
 
 template <typename T>
@@ -422,6 +427,12 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         what = "backward LDS limits";
         e = set_backward_lds_limits(kLds, &bad);
     }
+    if (e == hipSuccess) {
+        what = "auxiliary stream";
+        e = hipStreamCreateWithFlags(&net->aux, hipStreamNonBlocking);
+    }
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&net->fork, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&net->join, hipEventDisableTiming);
     net->timing = (opts->flags & SNN_FLAG_TIMING) ? 1 : 0;
     if (e == hipSuccess) what = "timing events";
     for (int i = 0; i < 2 * K_N && net->timing && e == hipSuccess; ++i) e = hipEventCreate(&net->ev[i]);
@@ -671,6 +682,41 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
                         hipGetErrorString(e));
         net->in_gstep_cap = net->in_nnz;
     }
+    // spikes grouped by presynaptic neuron (inputs, then every LIF layer) on
+    // the second stream: they depend on the forward only, and run beside the
+    // latency-bound adjoint sweeps; the gradients wait for them
+    const hipStream_t g_s = net->aux;
+    HIP_TRY(net, hipEventRecord(net->fork, s));
+    HIP_TRY(net, hipStreamWaitEvent(g_s, net->fork, 0));
+    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GROUP], g_s));
+    {
+        GroupArgs g{};
+        g.off = net->in_off;
+        g.end = net->in_off;
+        g.step = net->in_step;
+        g.neuron = net->in_neuron;
+        g.n = t.n_in;
+        g.g_off = net->in_goff;
+        g.g_step = net->in_gstep;
+        g.st = net->st;
+        HIP_TRY(net, launch_group(g, t.B, g_s));
+    }
+    for (int l = 1; l < t.L; ++l) {
+        if (t.kind[l] != SNN_LIF) continue;
+        const size_t li = (size_t)t.lif[l];
+        GroupArgs g{};
+        g.cnt = net->rec_cnt + li * t.B;
+        g.off_stride = t.cap;
+        g.step = net->rec_s + li * t.B * t.cap;
+        g.neuron = net->rec_n + li * t.B * t.cap;
+        g.n = t.n[l];
+        g.g_off = net->rec_goff + li * t.B * (t.maxn + 1);
+        g.g_step = net->rec_gstep + li * t.B * t.cap;
+        g.st = net->st;
+        HIP_TRY(net, launch_group(g, t.B, g_s));
+    }
+    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GROUP + 1], g_s));
+    HIP_TRY(net, hipEventRecord(net->join, g_s));
     const int C = t.n[t.out_l];
     const int feed = t.pre[t.out_p];
     const size_t B = t.B, cap = t.cap;
@@ -754,35 +800,7 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
         TIMED(net, K_BCORE,
               launch_backward_core(a, t.n_lif, net->core_threads, net->lds_core_b, s));
     }
-    // spikes grouped by presynaptic neuron: inputs, then every LIF layer
-    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GROUP], s));
-    {
-        GroupArgs g{};
-        g.off = net->in_off;
-        g.end = net->in_off;
-        g.step = net->in_step;
-        g.neuron = net->in_neuron;
-        g.n = t.n_in;
-        g.g_off = net->in_goff;
-        g.g_step = net->in_gstep;
-        g.st = net->st;
-        HIP_TRY(net, launch_group(g, t.B, s));
-    }
-    for (int l = 1; l < t.L; ++l) {
-        if (t.kind[l] != SNN_LIF) continue;
-        const size_t li = (size_t)t.lif[l];
-        GroupArgs g{};
-        g.cnt = net->rec_cnt + li * t.B;
-        g.off_stride = t.cap;
-        g.step = net->rec_s + li * t.B * t.cap;
-        g.neuron = net->rec_n + li * t.B * t.cap;
-        g.n = t.n[l];
-        g.g_off = net->rec_goff + li * t.B * (t.maxn + 1);
-        g.g_step = net->rec_gstep + li * t.B * t.cap;
-        g.st = net->st;
-        HIP_TRY(net, launch_group(g, t.B, s));
-    }
-    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GROUP + 1], s));
+    HIP_TRY(net, hipStreamWaitEvent(s, net->join, 0));
     GradArgs ga{};
     ga.B = t.B;
     ga.T = t.T;
@@ -852,6 +870,7 @@ extern "C" const char* snn_last_error(const snn_net* net) { return net ? net->er
 extern "C" void snn_destroy(snn_net* net) {
     if (!net) return;
     (void)hipStreamSynchronize(net->stream);
+    if (net->aux) (void)hipStreamSynchronize(net->aux);
     free_all(net);
     free(net);
 }
