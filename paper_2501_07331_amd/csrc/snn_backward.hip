@@ -216,6 +216,40 @@ struct BwdCore {
         const BwdLayer& y = a.ly[l];
         const int lane = tid & 63, wave = tid >> 6;
         float* lds = reinterpret_cast<float*>(smem);
+        // the reads of the chunk, all in bounds (masked terms read row 0,
+        // column 0), issued together; the empty asm takes them as operands so
+        // that the compiler keeps them unconditional (it would otherwise move
+        // each read behind its own mask branch and wait for it there) and one
+        // wait covers all of them; a masked term is then 0 x 0
+        float d[4][NPA];
+        bool ok[4][NPA];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int q = q0 + k;
+#pragma unroll
+            for (int pp = 0; pp < NPA; ++pp) {
+                d[k][pp] = 0.0f;
+                ok[k][pp] = false;
+                if (pp >= NP) continue;
+                const int nq = y.nq[pp];
+                const int sq = (int)ws[pp][q].y;
+                int row = n_mod + sq;
+                row = (row >= a.S) ? row - a.S : row;
+                ok[k][pp] = pp < y.npost && q < cnt && tid < nq && n + sq <= a.T - 1;
+                if (RL)
+                    d[k][pp] = ((lds_f32*)(lds + y.qring_lds[pp]))[(ok[k][pp] ? row : 0) * nq +
+                                                                  (ok[k][pp] ? tid : 0)];
+                else
+                    d[k][pp] = ((global_f32*)(y.qring[pp] +
+                                              ((size_t)b * a.S + (ok[k][pp] ? row : 0)) * nq))[ok[k][pp] ? tid : 0];
+            }
+        }
+        if constexpr (NPA == 1) {
+            asm volatile("" : "+v"(d[0][0]), "+v"(d[1][0]), "+v"(d[2][0]), "+v"(d[3][0]));
+        } else {
+            asm volatile("" : "+v"(d[0][0]), "+v"(d[1][0]), "+v"(d[2][0]), "+v"(d[3][0]),
+                              "+v"(d[0][1]), "+v"(d[1][1]), "+v"(d[2][1]), "+v"(d[3][1]));
+        }
         double v[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
@@ -223,17 +257,9 @@ struct BwdCore {
             v[k] = 0.0;
 #pragma unroll
             for (int pp = 0; pp < NP; ++pp) {
-                const int nq = y.nq[pp];
-                const int sq = (int)ws[pp][q].y;
-                int row = n_mod + sq;
-                row = (row >= a.S) ? row - a.S : row;
-                const bool ok = pp < y.npost && q < cnt && tid < nq && n + sq <= a.T - 1;
-                float d;
-                if (RL)
-                    d = ((lds_f32*)(lds + y.qring_lds[pp]))[(ok ? row : 0) * nq + (ok ? tid : 0)];
-                else
-                    d = ((global_f32*)(y.qring[pp] + ((size_t)b * a.S + (ok ? row : 0)) * nq))[ok ? tid : 0];
-                v[k] -= ok ? (double)__fmul_rn(__uint_as_float(ws[pp][q].x), d) : 0.0;
+                const float wm = ok[k][pp] ? __uint_as_float(ws[pp][q].x) : 0.0f;
+                const float dm = ok[k][pp] ? d[k][pp] : 0.0f;
+                v[k] -= (double)__fmul_rn(wm, dm);
             }
         }
         const double x = row_sum4(v, lane);
