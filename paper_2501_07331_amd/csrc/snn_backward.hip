@@ -283,7 +283,18 @@ struct BwdCore {
         if (NP > 0) {
             const double* pq = part_l + (size_t)q * (4 * a.NW);
             double Ap = 0.0;
-            for (int i = 0; i < 4 * a.NW; ++i) Ap += pq[i];
+            if constexpr (MAXT <= 256) {
+                // the 4 NW partials read together, then added in order
+                constexpr int NPART = 4 * (MAXT / 64);
+                const int np = 4 * a.NW;
+                double pv[NPART];
+#pragma unroll
+                for (int i = 0; i < NPART; ++i) pv[i] = pq[min(i, np - 1)];
+#pragma unroll
+                for (int i = 0; i < NPART; ++i) Ap = (i < np) ? Ap + pv[i] : Ap;
+            } else {
+                for (int i = 0; i < 4 * a.NW; ++i) Ap += pq[i];
+            }
             A += Ap;
         }
         const float den = __fsub_rn(I, a.theta);
