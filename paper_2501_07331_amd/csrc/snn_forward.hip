@@ -99,11 +99,14 @@ __global__ void round_delays_kernel(RoundArgs a, uint8_t* slot, uint2* ws, DevSt
 // ring cell sums in emission order (column_add_all keeps the order of equal
 // rows).
 //
-// Loads run one chunk ahead, as in scatter_events: the ids and steps of a
-// pair of chunks (one event per lane), and the weights and slots of the next
-// chunk while a chunk is added, in two register sets; one explicit wait at
-// each chunk start.  The common path writes out at most two rows per chunk
-// and has no loop.
+// Loads run two chunks ahead: the ids and steps of a pair of chunks (one
+// event per lane) at least two chunks before use, and the weights and slots
+// of chunk c + 2 while chunk c is added, in three register sets (the loop
+// body covers six chunks, so every set and pair vector has a fixed
+// register).  A chunk writes out its final rows before issuing loads, so the
+// wait at the next chunk start lets exactly the newest 8 operations (chunk
+// c + 1's weights) stay in flight.  The common path writes out at most two
+// rows per chunk and has no loop.
 __global__ void __launch_bounds__(64) input_scan_kernel(InScanArgs a) {
     if (a.st->bad_input) return;
     const int n1 = a.n1, T = a.T, TB = a.TB, R = a.S + a.TB - 1;
@@ -145,6 +148,16 @@ __global__ void __launch_bounds__(64) input_scan_kernel(InScanArgs a) {
                 w[q] = make_uint2((unsigned)v[0], (unsigned)v[1]);
             }
         };
+        // before the chunk of events e0 ..: write out up to two rows that are
+        // final (steps before the chunk's first); issued before the next loads
+        // so that the stores are never among the newest operations a chunk
+        // start waits past
+        auto flush_before = [&](int e0, int stv, int u8) {
+            if (E1 - e0 <= 0) return;
+            const int st0 = __builtin_amdgcn_readlane(stv, u8);
+            if (f < st0) flush_one();
+            if (f < st0) flush_one();
+        };
         // chunk of events e0 .. e0 + KB - 1 (steps in lanes u8 .. u8 + KB - 1 of stv)
         auto add_chunk = [&](int e0, int stv, int u8, const uint2 (&w)[KB]) {
             const int nv = E1 - e0;                              // valid events (uniform)
@@ -155,8 +168,6 @@ __global__ void __launch_bounds__(64) input_scan_kernel(InScanArgs a) {
             int last = st[0];
 #pragma unroll
             for (int q = 1; q < KB; ++q) last = (q < nv) ? st[q] : last;
-            if (f < st[0]) flush_one();
-            if (f < st[0]) flush_one();
             if (last - f < TB) {
                 int row[KB];
                 float wv[KB];
@@ -184,22 +195,48 @@ __global__ void __launch_bounds__(64) input_scan_kernel(InScanArgs a) {
                 }
             }
         };
-        int idA, stA, idB, stB;
-        uint2 w0[KB], w1[KB];
-        load_pair(E0, idA, stA);
+        // vmcnt(8): all but the newest eight operations (chunk c + 1's weight
+        // loads) have landed
+        constexpr int kWaitVm8 = 0x0F70 | 8;
+        int idX, stX, idY, stY, idZ, stZ;
+        uint2 w0[KB], w1[KB], w2[KB];
+        load_pair(E0, idX, stX);
+        load_pair(E0 + 2 * KB, idY, stY);
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
-        load_ws(idA, 0, w0);
-        for (int e0 = E0; e0 < E1; e0 += 2 * KB) {
-            __builtin_amdgcn_s_waitcnt(kWaitVm0);
-            load_pair(e0 + 2 * KB, idB, stB);
-            load_ws(idA, KB, w1);                                // second chunk of this pair
-            add_chunk(e0, stA, 0, w0);
-            if (e0 + KB >= E1) break;
-            __builtin_amdgcn_s_waitcnt(kWaitVm0);
-            load_ws(idB, 0, w0);                                 // first chunk of the next pair
-            add_chunk(e0 + KB, stA, KB, w1);
-            idA = idB;                                           // landed at the wait above
-            stA = stB;
+        load_ws(idX, 0, w0);
+        load_ws(idX, KB, w1);
+        // per chunk: wait, write out, next pair's ids, weights of chunk c + 2,
+        // add chunk c; pairs X, Y, Z hold events e0 .., e0 + 16 .., e0 + 32 ..
+        for (int e0 = E0; e0 < E1; e0 += 6 * KB) {
+            __builtin_amdgcn_s_waitcnt(kWaitVm8);
+            flush_before(e0, stX, 0);
+            load_pair(e0 + 4 * KB, idZ, stZ);
+            load_ws(idY, 0, w2);
+            add_chunk(e0, stX, 0, w0);
+            __builtin_amdgcn_s_waitcnt(kWaitVm8);
+            flush_before(e0 + KB, stX, KB);
+            load_ws(idY, KB, w0);
+            add_chunk(e0 + KB, stX, KB, w1);
+            if (e0 + 2 * KB >= E1) break;
+            __builtin_amdgcn_s_waitcnt(kWaitVm8);
+            flush_before(e0 + 2 * KB, stY, 0);
+            load_pair(e0 + 6 * KB, idX, stX);
+            load_ws(idZ, 0, w1);
+            add_chunk(e0 + 2 * KB, stY, 0, w2);
+            __builtin_amdgcn_s_waitcnt(kWaitVm8);
+            flush_before(e0 + 3 * KB, stY, KB);
+            load_ws(idZ, KB, w2);
+            add_chunk(e0 + 3 * KB, stY, KB, w0);
+            if (e0 + 4 * KB >= E1) break;
+            __builtin_amdgcn_s_waitcnt(kWaitVm8);
+            flush_before(e0 + 4 * KB, stZ, 0);
+            load_pair(e0 + 8 * KB, idY, stY);
+            load_ws(idX, 0, w0);
+            add_chunk(e0 + 4 * KB, stZ, 0, w1);
+            __builtin_amdgcn_s_waitcnt(kWaitVm8);
+            flush_before(e0 + 5 * KB, stZ, KB);
+            load_ws(idX, KB, w1);
+            add_chunk(e0 + 5 * KB, stZ, KB, w2);
         }
     }
     flush_to(T);
