@@ -584,17 +584,42 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
             const int s1 = n1 ? go1[(size_t)b * (n1 + 1)] : 0, e1 = n1 ? go1[(size_t)b * (n1 + 1) + n1] : 0;
             const int c0 = e0 - s0, c1 = e1 - s1;
             const bool in_lds = c0 + c1 <= a.spcap;
+            // (loads of eight iterations issued before their stores, so that a
+            // sample's staging costs a few memory round trips, not one each)
+            constexpr int U = 8;
             if (in_lds) {
-                for (int x = tid; x < c0 + c1; x += nt)
-                    sp[x] = (unsigned short)((x < c0) ? gs0[s0 + x] : gs1[s1 + x - c0]);
+                for (int x0 = tid; x0 < c0 + c1; x0 += U * nt) {
+                    int v[U];
+#pragma unroll
+                    for (int u = 0; u < U; ++u) {
+                        const int x = x0 + u * nt;
+                        const int xc = min(x, c0 + c1 - 1);
+                        v[u] = (xc < c0) ? gs0[s0 + xc] : gs1[s1 + xc - c0];
+                    }
+#pragma unroll
+                    for (int u = 0; u < U; ++u)
+                        if (x0 + u * nt < c0 + c1) sp[x0 + u * nt] = (unsigned short)v[u];
+                }
             }
             // the J post trajectories of the sample
             const size_t base = (size_t)b * T * LN + G.off + j0;
-            for (int e = tid; e < T * J; e += nt) {
-                const int m = e / J, q = e % J;
-                float2 x = make_float2(0.0f, 0.0f);
-                if (q < nj) x = make_float2(tu[base + (size_t)m * LN + q], td[base + (size_t)m * LN + q]);
-                st[q * T + m] = x;
+            for (int e0 = tid; e0 < T * J; e0 += U * nt) {
+                float2 x[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int e = min(e0 + u * nt, T * J - 1);
+                    const int m = e / J, q = e % J;
+                    const int qc = min(q, nj - 1);
+                    x[u] = make_float2(tu[base + (size_t)m * LN + qc], td[base + (size_t)m * LN + qc]);
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int e = e0 + u * nt;
+                    if (e < T * J) {
+                        const int m = e / J, q = e % J;
+                        st[q * T + m] = (q < nj) ? x[u] : make_float2(0.0f, 0.0f);
+                    }
+                }
             }
             __syncthreads();
 #pragma unroll
