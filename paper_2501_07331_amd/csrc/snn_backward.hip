@@ -630,13 +630,25 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
                 const int* gs = pi ? gs1 : gs0;
                 const int off = pi ? c0 - s1 : -s0;                 // LDS index = x + off
                 float pu = 0.0f, pd = 0.0f;
-                for (int x = lo[k]; x < hi[k]; ++x) {
-                    const int t = in_lds ? (int)sp[x + off] : gs[x];
-                    const int m = t + sl;
-                    if (m <= T - 1) {
-                        const float2 ud = stk[m];
-                        pu = __fadd_rn(pu, ud.x);
-                        pd = __fadd_rn(pd, __fmul_rn(w[k], ud.y));
+                // four spikes at a time: their reads issued together, their
+                // terms added in spike order
+                for (int x = lo[k]; x < hi[k]; x += 4) {
+                    int m[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int xc = min(x + u, hi[k] - 1);
+                        const int t = in_lds ? (int)sp[xc + off] : gs[xc];
+                        m[u] = (x + u < hi[k]) ? t + sl : T;             // T: no arrival
+                    }
+                    float2 ud[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) ud[u] = stk[(m[u] <= T - 1) ? m[u] : 0];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        if (m[u] <= T - 1) {
+                            pu = __fadd_rn(pu, ud[u].x);
+                            pd = __fadd_rn(pd, __fmul_rn(w[k], ud[u].y));
+                        }
                     }
                 }
                 su[k] += (double)pu;
