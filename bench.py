@@ -180,11 +180,31 @@ def main():
                 kt.setdefault(k, []).append(bwd[k])
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t0
-    s = net.stats()
+        s = net.stats()
+        S_lif = int(recs[0][0].sum().item())
+        # the training iteration: the same step plus one Adam update of every
+        # weight and delay (on copies, after the timed region above)
+        Wt = [w.clone() for w in W]
+        Dt = [d.clone() for d in D]
+        opt_ms = []
+        n_train = max(1, min(args.steps, 10))
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(n_train):
+            net.forward(off, st, ne, Wt, Dt, labels, recs, loss, z)
+            net.backward(dW, dD)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            net.optimizer_step(Wt, Dt, dW, dD, kind=snn.SNN_OPT_ADAM, lr_w=1e-3, lr_d=0.1)
+            e1.record(stream)
+            e1.synchronize()
+            opt_ms.append(e0.elapsed_time(e1))
+        torch.cuda.synchronize()
+        train_ms = 1e3 * (time.perf_counter() - t1) / n_train
+    n_params = sum(w.numel() for w in W)
     E = s["events"]
     ms = 1e3 * elapsed / args.steps
     # units of work, from the spike counts of this batch (one LIF layer)
-    S_lif = int(recs[0][0].sum().item())
     n_in, n_h, C = c.layers[0][0], c.layers[1][0], c.layers[2][0]
     u = {"E_in": s["input_spikes"] * n_h, "E_ll": S_lif * n_h, "E_ro": S_lif * C,
          "NS_lif": wl.B * wl.T * n_h, "NS_li": wl.B * wl.T * C, "S_lif": S_lif,
@@ -217,7 +237,12 @@ def main():
                    "kernel_ms": {k: round(v, 4) for k, v in avg.items()},
                    "kernel_hbm_frac": kernel_frac,
                    "step_alg_bytes": step_bytes(u),
-                   "step_hbm_frac": round(step_bytes(u) / (elapsed / args.steps) / 1e9 / HBM_PEAK_GBS, 4)},
+                   "step_hbm_frac": round(step_bytes(u) / (elapsed / args.steps) / 1e9 / HBM_PEAK_GBS, 4),
+                   "train_step_ms": round(train_ms, 4),
+                   "optimizer": {"kind": "adam", "params": 2 * n_params,
+                                 "ms": round(float(np.mean(opt_ms)), 4),
+                                 "hbm_frac": round(56 * n_params / (np.mean(opt_ms) * 1e-3) / 1e9
+                                                   / HBM_PEAK_GBS, 4)}},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": ach, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": ach / HBM_PEAK_GBS, "traffic": measured_traffic(dom),
                      "alg_bytes_per_launch": kb[dom]},

@@ -199,6 +199,50 @@ int snn_forward(snn_net* net, const snn_spikes_in* in, const float* const* W, co
  */
 int snn_backward(snn_net* net, float* const* dW, float* const* dD);
 
+/*
+ * Parameter update after snn_backward: one optimiser step on every W and D,
+ * then the delay clamp.  The paper trains weights and delays with separate
+ * learning rates and schedules (Methods / "Implementation" and its
+ * hyper-parameter tables) and keeps delays non-negative (Fig. 3 caption); it
+ * does not name the optimiser, so two are offered:
+ *   SNN_OPT_SGD:   x <- x - lr * g                 (fp32, one rounding each op)
+ *   SNN_OPT_ADAM:  m <- b1 m + (1 - b1) g,  v <- b2 v + (1 - b2) g g,
+ *                  x <- x - lr * (m c1) / (sqrt(v c2) + eps),
+ *                  c1 = 1 / (1 - b1^k), c2 = 1 / (1 - b2^k) at the k-th Adam
+ *                  step of the handle (bias corrections computed in fp64 on
+ *                  the host, rounded to fp32)
+ * with g = dW (lr = lr_w * lr_scale_w[p]) for weights and g = dD (lr = lr_d *
+ * lr_scale_d[p]) for delays, which are then clamped to [d_min, d_max] (in
+ * steps; d_min <= d_max).  Learning-rate schedules are the caller's: it
+ * passes this step's lr_w and lr_d.
+ *   W, D:     host arrays of P device pointers, updated in place
+ *   dW, dD:   host arrays of P device pointers (as written by snn_backward)
+ *   lr_scale_w, lr_scale_d: host arrays of P factors per projection, or NULL
+ *             (all 1); 0 freezes that projection's weights or delays
+ * The Adam moments (4 fp32 per parameter) are owned by the handle, allocated
+ * by its first Adam step, zero at that point and after snn_optimizer_reset.
+ * Enqueued on the handle's stream; returns after it has been enqueued (no
+ * read-back).  Errors: SNN_EINVAL (NULL pointers, unknown kind, non-finite
+ * or negative rates, d_min > d_max, b1 or b2 outside [0, 1), eps <= 0),
+ * SNN_ENOMEM, SNN_EDEVICE.
+ */
+enum { SNN_OPT_SGD = 0, SNN_OPT_ADAM = 1 };
+
+typedef struct {
+    int32_t kind;
+    float lr_w, lr_d;
+    float beta1, beta2, eps;      /* Adam only */
+    float d_min, d_max;
+    const float* lr_scale_w;      /* host [P] or NULL */
+    const float* lr_scale_d;      /* host [P] or NULL */
+} snn_optim;
+
+int snn_optimizer_step(snn_net* net, const snn_optim* o, float* const* W, float* const* D,
+                       const float* const* dW, const float* const* dD);
+
+/* Zero the Adam moments and the Adam step count of the handle. */
+int snn_optimizer_reset(snn_net* net);
+
 /* Copy the final V and I of non-input layer `layer` after the last forward
  * into (dev) [batch][n_layer] buffers. */
 int snn_get_state(const snn_net* net, int32_t layer, float* V, float* I);

@@ -12,6 +12,7 @@ SNN_INPUT, SNN_LIF, SNN_LI = 0, 1, 2
 SNN_LOSS_CE_SUM, SNN_LOSS_CE_MAX = 0, 1
 SNN_FLAG_HBM_RINGS = 1
 SNN_FLAG_TIMING = 2
+SNN_OPT_SGD, SNN_OPT_ADAM = 0, 1
 _NAMES = {0: "SNN_OK", -1: "SNN_EINVAL", -2: "SNN_ENOMEM", -3: "SNN_ESTATE", -4: "SNN_EOVERFLOW",
           -5: "SNN_EDEVICE"}
 
@@ -52,6 +53,13 @@ class snn_stats(C.Structure):
                 ("kernel_ms", C.c_float * 8)]
 
 
+class snn_optim(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("lr_w", C.c_float), ("lr_d", C.c_float),
+                ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float),
+                ("d_min", C.c_float), ("d_max", C.c_float),
+                ("lr_scale_w", C.c_void_p), ("lr_scale_d", C.c_void_p)]
+
+
 # order of snn_stats.kernel_ms
 KERNELS = ("input_scan", "forward_core", "readout_forward", "readout_adjoint", "backward_core",
            "group", "gradients")
@@ -82,6 +90,9 @@ def load_library():
     lib.snn_forward.argtypes = [P, C.POINTER(snn_spikes_in), C.POINTER(P), C.POINTER(P), P,
                                 C.POINTER(snn_spikes_out), P, P]
     lib.snn_backward.argtypes = [P, C.POINTER(P), C.POINTER(P)]
+    lib.snn_optimizer_step.argtypes = [P, C.POINTER(snn_optim), C.POINTER(P), C.POINTER(P),
+                                       C.POINTER(P), C.POINTER(P)]
+    lib.snn_optimizer_reset.argtypes = [P]
     lib.snn_get_state.argtypes = [P, C.c_int32, P, P]
     lib.snn_get_stats.argtypes = [P, C.POINTER(snn_stats)]
     lib.snn_last_error.argtypes = [P]
@@ -89,7 +100,8 @@ def load_library():
     lib.snn_destroy.argtypes = [P]
     lib.snn_destroy.restype = None
     for f in ("snn_create", "snn_num_projections", "snn_projection_info", "snn_forward",
-              "snn_backward", "snn_get_state", "snn_get_stats"):
+              "snn_backward", "snn_optimizer_step", "snn_optimizer_reset", "snn_get_state",
+              "snn_get_stats"):
         getattr(lib, f).restype = C.c_int
     _lib = lib
     return lib
@@ -127,6 +139,7 @@ class Network:
         self.layers = [tuple(int(x) for x in l) for l in layers]
         self.batch, self.T = int(batch), int(T)
         self.record_capacity = int(record_capacity)
+        self.max_delay = int(max_delay)
         if stream is None:
             stream = torch.cuda.current_stream()
         self.stream = stream
@@ -203,6 +216,37 @@ class Network:
                 raise ValueError(f"dW/dD[{p}] must hold {npre}x{npost} elements")
         rc = self._lib.snn_backward(self._h, _ptr_array(dW, f32, "dW"), _ptr_array(dD, f32, "dD"))
         return self._check(rc)
+
+    def optimizer_step(self, W, D, dW, dD, kind: int = SNN_OPT_ADAM, lr_w: float = 1e-3,
+                       lr_d: float = 0.1, beta1: float = 0.9, beta2: float = 0.999,
+                       eps: float = 1e-8, d_min: float = 0.0, d_max: Optional[float] = None,
+                       lr_scale_w: Optional[Sequence[float]] = None,
+                       lr_scale_d: Optional[Sequence[float]] = None):
+        """One SGD or Adam step on W and D in place, then D clamped to
+        [d_min, d_max] (default d_max: the handle's max_delay)."""
+        import torch
+        f32 = torch.float32
+        P_ = len(self.projections)
+        for nm, ts in (("W", W), ("D", D), ("dW", dW), ("dD", dD)):
+            if len(ts) != P_:
+                raise ValueError(f"one {nm} tensor per projection")
+        for p, (_, _, npre, npost) in enumerate(self.projections):
+            for t_ in (W[p], D[p], dW[p], dD[p]):
+                if t_.numel() != npre * npost:
+                    raise ValueError(f"parameters of projection {p} must hold {npre}x{npost} elements")
+        sw = (C.c_float * P_)(*lr_scale_w) if lr_scale_w is not None else None
+        sd = (C.c_float * P_)(*lr_scale_d) if lr_scale_d is not None else None
+        o = snn_optim(int(kind), float(lr_w), float(lr_d), float(beta1), float(beta2), float(eps),
+                      float(d_min), float(self.max_delay if d_max is None else d_max),
+                      C.cast(sw, C.c_void_p) if sw is not None else None,
+                      C.cast(sd, C.c_void_p) if sd is not None else None)
+        rc = self._lib.snn_optimizer_step(self._h, C.byref(o), _ptr_array(W, f32, "W"),
+                                          _ptr_array(D, f32, "D"), _ptr_array(dW, f32, "dW"),
+                                          _ptr_array(dD, f32, "dD"))
+        return self._check(rc)
+
+    def optimizer_reset(self):
+        return self._check(self._lib.snn_optimizer_reset(self._h))
 
     def state(self, layer: int, V, I):
         import torch

@@ -66,6 +66,8 @@ struct snn_net {
     float* td_out;
     double* A2;
     double* gpart;
+    float* mom;                 // Adam moments [4][n_params], allocated by the first Adam step
+    long long adam_steps;
     int* in_goff;
     int* in_gstep;
     long long in_gstep_cap;
@@ -106,7 +108,7 @@ static void free_all(snn_net* n) {
                     n->rec_idx, n->rec_cnt, n->rec_goff, n->rec_gstep, n->z,      n->nstar,
                     n->src,     n->Vf,      n->If,       n->table,     n->tu_lif, n->td_lif,
                     n->tu_out,  n->td_out,  n->A2,       n->in_goff,   n->in_gstep, n->st,
-                    n->gpart,   n->ws,      n->steptab};
+                    n->gpart,   n->ws,      n->steptab, n->mom};
     for (void* p : bufs)
         if (p) (void)hipFree(p);
     for (int p = 0; p < SNN_MAXP; ++p)
@@ -843,6 +845,79 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
     rc = collect_times(net, K_RADJ, K_N, t.n_lif > 0);
     if (rc) return rc;
     net->stats.degenerate_jumps = (int64_t)net->st_host->degenerate;
+    return SNN_OK;
+}
+
+extern "C" int snn_optimizer_step(snn_net* net, const snn_optim* o, float* const* W, float* const* D,
+                                  const float* const* dW, const float* const* dD) {
+    if (!net) return SNN_EINVAL;
+    net->err[0] = 0;
+    const Topo& t = net->t;
+    if (!o || !W || !D || !dW || !dD) return fail(net, SNN_EINVAL, "NULL optimiser, W, D, dW or dD");
+    if (o->kind != SNN_OPT_SGD && o->kind != SNN_OPT_ADAM)
+        return fail(net, SNN_EINVAL, "unknown optimiser kind %d", o->kind);
+    if (!(o->lr_w >= 0.0f) || !(o->lr_d >= 0.0f) || isinf(o->lr_w) || isinf(o->lr_d))
+        return fail(net, SNN_EINVAL, "learning rates must be finite and >= 0");
+    if (!(o->d_min <= o->d_max)) return fail(net, SNN_EINVAL, "d_min > d_max (or NaN)");
+    if (o->kind == SNN_OPT_ADAM &&
+        (!(o->beta1 >= 0.0f && o->beta1 < 1.0f) || !(o->beta2 >= 0.0f && o->beta2 < 1.0f) ||
+         !(o->eps > 0.0f)))
+        return fail(net, SNN_EINVAL, "Adam needs 0 <= beta1, beta2 < 1 and eps > 0");
+    OptArgs a{};
+    a.P = t.P;
+    a.kind = o->kind;
+    a.nparams = net->n_params;
+    for (int p = 0; p < t.P; ++p) {
+        if (!W[p] || !D[p] || !dW[p] || !dD[p])
+            return fail(net, SNN_EINVAL, "NULL W, D, dW or dD of projection %d", p);
+        const float sw = o->lr_scale_w ? o->lr_scale_w[p] : 1.0f;
+        const float sd = o->lr_scale_d ? o->lr_scale_d[p] : 1.0f;
+        if (!(sw >= 0.0f) || !(sd >= 0.0f) || isinf(sw) || isinf(sd))
+            return fail(net, SNN_EINVAL, "learning-rate factors of projection %d must be finite and >= 0", p);
+        a.woff[p] = t.woff[p];
+        a.W[p] = W[p];
+        a.D[p] = D[p];
+        a.dW[p] = dW[p];
+        a.dD[p] = dD[p];
+        a.lr_w[p] = (float)((double)o->lr_w * sw);
+        a.lr_d[p] = (float)((double)o->lr_d * sd);
+    }
+    a.d_min = o->d_min;
+    a.d_max = o->d_max;
+    if (o->kind == SNN_OPT_ADAM) {
+        if (!net->mom) {
+            const size_t bytes = (size_t)4 * std::max<long long>(net->n_params, 1) * sizeof(float);
+            const hipError_t e = hipMalloc((void**)&net->mom, bytes);
+            if (e != hipSuccess) {
+                net->mom = nullptr;
+                return fail(net, e == hipErrorOutOfMemory ? SNN_ENOMEM : SNN_EDEVICE, "hipMalloc: %s",
+                            hipGetErrorString(e));
+            }
+            HIP_TRY(net, hipMemsetAsync(net->mom, 0, bytes, net->stream));
+            net->adam_steps = 0;
+        }
+        const long long k = ++net->adam_steps;
+        a.b1 = o->beta1;
+        a.b2 = o->beta2;
+        a.one_m_b1 = (float)(1.0 - (double)o->beta1);
+        a.one_m_b2 = (float)(1.0 - (double)o->beta2);
+        a.eps = o->eps;
+        a.c1 = (float)(1.0 / (1.0 - pow((double)o->beta1, (double)k)));
+        a.c2 = (float)(1.0 / (1.0 - pow((double)o->beta2, (double)k)));
+        a.mom = net->mom;
+    }
+    HIP_TRY(net, launch_optimizer(a, net->stream));
+    return SNN_OK;
+}
+
+extern "C" int snn_optimizer_reset(snn_net* net) {
+    if (!net) return SNN_EINVAL;
+    net->err[0] = 0;
+    net->adam_steps = 0;
+    if (net->mom)
+        HIP_TRY(net, hipMemsetAsync(net->mom, 0,
+                                    (size_t)4 * std::max<long long>(net->n_params, 1) * sizeof(float),
+                                    net->stream));
     return SNN_OK;
 }
 

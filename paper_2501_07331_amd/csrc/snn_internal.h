@@ -218,7 +218,23 @@ struct GradArgs {
     float* dD[SNN_MAXP];
 };
 
-// Kernel launchers (snn_forward.hip, snn_backward.hip).
+// One optimiser step (snn_optimizer_step): rates per projection, constants
+// rounded to fp32 on the host.
+struct OptArgs {
+    int P, kind;
+    long long nparams;
+    long long woff[SNN_MAXP];
+    float* W[SNN_MAXP];
+    float* D[SNN_MAXP];
+    const float* dW[SNN_MAXP];
+    const float* dD[SNN_MAXP];
+    float lr_w[SNN_MAXP], lr_d[SNN_MAXP];
+    float b1, b2, one_m_b1, one_m_b2, eps, c1, c2;
+    float d_min, d_max;
+    float* mom;                        // Adam: [4][nparams] (m_w, v_w, m_d, v_d)
+};
+
+// Kernel launchers (snn_forward.hip, snn_backward.hip, snn_optim.hip).
 hipError_t launch_reset_status(DevStatus* st, hipStream_t s);
 hipError_t launch_validate(const int* off, const int* step, const int* neuron, int nnz, int B, int T,
                            int n_in, const int* labels, int C, DevStatus* st, hipStream_t s);
@@ -241,6 +257,7 @@ hipError_t launch_backward_core(const CoreBwdArgs& a, int n_lif, int threads, si
 hipError_t launch_group(const GroupArgs& a, int B, hipStream_t s);
 hipError_t launch_gradients(const GradArgs& a, int J, int KL, int threads, size_t lds, hipStream_t s);
 hipError_t launch_grad_reduce(const GradArgs& a, int P, hipStream_t s);
+hipError_t launch_optimizer(const OptArgs& a, hipStream_t s);
 hipError_t set_forward_lds_limits(size_t bytes, int* bad);
 hipError_t set_core_lds_limits(size_t bytes, int* bad);
 bool launch_forward_core_256(const CoreFwdArgs& a, int n_lif, int np, bool rl, int threads,

@@ -37,6 +37,8 @@ def test_struct_layouts_match_header():
     assert C.sizeof(b.snn_spikes_in) == 32
     assert C.sizeof(b.snn_spikes_out) == 24
     assert C.sizeof(b.snn_stats) == 80
+    # int32 + 7 floats; 2 pointers
+    assert C.sizeof(b.snn_optim) == 48
 
 
 def _create(lib, layers, tau_m=20.0, tau_s=5.0, theta=1.0, dt=1.0, max_delay=10, **opt):
@@ -83,6 +85,8 @@ def test_null_handles(lib):
     assert lib.snn_forward(None, None, None, None, None, None, None, None) == -1
     assert lib.snn_backward(None, None, None) == -1
     assert lib.snn_get_stats(None, None) == -1
+    assert lib.snn_optimizer_step(None, None, None, None, None, None) == -1
+    assert lib.snn_optimizer_reset(None) == -1
     # with no handle: the reason of the last failed snn_create ("" after an
     # argument error, which needs no explanation beyond its code)
     rc, h = _create(lib, GOOD, batch=0)
