@@ -114,6 +114,77 @@ def copy_calibration(mib):
     print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "launches": 5}), flush=True)
 
 
+def sweep(args):
+    """Step time against the maximum delay (the delay-buffer size the paper's
+    timing comparison varies, Results / "Computational performance") and
+    against the grid step at fixed trial length.  Delay sweep: every
+    feed-forward projection U[0, max_delay], the recurrent one U[0,
+    min(max_delay, 50)] steps, dt 1 ms, T 1000.  dt sweep: delays U[0, 25.5]
+    ms feed-forward and U[0, 5] ms recurrent, T = 1000 ms / dt."""
+    import torch
+    import paper_2501_07331_amd as snn
+    from workloads import make_variant
+    assert torch.cuda.is_available(), "the sweep needs a GPU"
+    if args.sweep == "delay":
+        pts = [int(x) for x in args.points.split(",")] if args.points else [0, 25, 50, 100, 150, 200, 255]
+        cases = [dict(delay_range=(m, min(m, 50), m)) for m in pts]
+    else:
+        pts = [float(x) for x in args.points.split(",")] if args.points else [1.0, 0.5, 0.25, 0.1]
+        cases = []
+        for dt in pts:
+            T = int(round(1000.0 / dt))
+            cases.append(dict(dt=dt, T=T, delay_range=(int(round(25.5 / dt)), int(round(5.0 / dt)),
+                                                     int(round(25.5 / dt)))))
+    dev = torch.device("cuda")
+    cap = 64 * 256
+    for kw in cases:
+        wl = make_variant(4, **kw)
+        c = wl.cfg
+        stream = torch.cuda.Stream()
+        with torch.cuda.stream(stream):
+            t = lambda a, dt_: torch.from_numpy(np.ascontiguousarray(a)).to(dev, dt_)
+            off, st, ne = t(wl.in_off, torch.int32), t(wl.in_step, torch.int32), t(wl.in_neuron, torch.int32)
+            W = [t(w, torch.float32) for w in wl.W]
+            D = [t(d, torch.float32) for d in wl.D]
+            labels = t(wl.labels, torch.int32)
+            recs = [(torch.zeros(wl.B, dtype=torch.int32, device=dev),
+                     torch.zeros(wl.B, cap, dtype=torch.int32, device=dev),
+                     torch.zeros(wl.B, cap, dtype=torch.int32, device=dev))]
+            loss = torch.zeros(wl.B + 1, device=dev)
+            dW = [torch.zeros_like(w) for w in W]
+            dD = [torch.zeros_like(w) for w in W]
+            net = snn.Network(c.layers, c.tau_m, c.tau_s, c.theta, c.dt, c.max_delay, wl.B, wl.T,
+                              c.loss, c.readout_scale, cap, flags=snn.SNN_FLAG_TIMING, stream=stream)
+            for _ in range(args.warmup):
+                net.forward(off, st, ne, W, D, labels, recs, loss)
+                net.backward(dW, dD)
+            torch.cuda.synchronize()
+            kt = {}
+            t0 = time.perf_counter()
+            for _ in range(args.steps):
+                net.forward(off, st, ne, W, D, labels, recs, loss)
+                fwd = net.stats()["kernel_ms"]
+                net.backward(dW, dD)
+                bwd = net.stats()["kernel_ms"]
+                for k in ("input_scan", "forward_core", "readout_forward"):
+                    kt.setdefault(k, []).append(fwd[k])
+                for k in ("readout_adjoint", "backward_core", "group", "gradients"):
+                    kt.setdefault(k, []).append(bwd[k])
+            torch.cuda.synchronize()
+            el = (time.perf_counter() - t0) / args.steps
+            s = net.stats()
+            net.close()
+        print(json.dumps({"sweep": args.sweep, "max_delay": c.max_delay, "delay_range": list(c.delay_range),
+                          "dt_ms": c.dt, "T": wl.T, "B": wl.B, "ms_per_step": round(1e3 * el, 4),
+                          "events": s["events"], "events_per_s": s["events"] / el,
+                          "lif_spikes_per_neuron": round(s["lif_spikes"] / wl.B / 256, 2),
+                          "lds_rings": s["lds_rings"],
+                          "kernel_ms": {k: round(float(np.mean(v)), 4) for k, v in kt.items()}}),
+              flush=True)
+        del net, W, D, dW, dD, recs
+        torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -124,7 +195,16 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (the reference "
                          "kernel the HBM byte counters are scaled by) and exit")
+    ap.add_argument("--sweep", choices=("delay", "dt"), default=None,
+                    help="instead of the single line: time the 700-256rec-20 step over a range "
+                         "of maximum delays (dt 1 ms) or of time steps (the same 1 s trials), "
+                         "one JSON line per point")
+    ap.add_argument("--points", type=str, default=None,
+                    help="comma-separated sweep points (max delays in steps, or dt in ms)")
     args = ap.parse_args()
+    if args.sweep:
+        sweep(args)
+        return
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
         return

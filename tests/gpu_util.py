@@ -129,9 +129,12 @@ def assert_forward_bitexact(gpu, orc, wl):
     assert np.array_equal(gpu["I"].view(np.uint32), f.I_final.view(np.uint32)), "final I differs"
 
 
-def assert_backward_close(gpu, orc, rtol=1e-4, atol_rel=1e-6, f64_bound=1e-4):
+def assert_backward_close(gpu, orc, rtol=1e-4, atol_rel=1e-6, f64_bound=1e-4, model_gap=False):
     """GPU vs the fp32 kernel-precision model at the stated tolerance, and vs
-    the fp64 definition within f64_bound of each tensor's scale."""
+    the fp64 definition within f64_bound of each tensor's scale.  With
+    model_gap, the fp64 bound of a tensor is at least twice the distance of
+    the oracle's own fp32 model from its fp64 definition (fp32 adjoints lose
+    accuracy over long, spike-dense trials: about 1e-3 of scale at T = 10^4)."""
     dW32, dD32, deg32 = orc["f32"]
     assert gpu["stats"]["degenerate_jumps"] == deg32
     for p in range(len(dW32)):
@@ -144,4 +147,8 @@ def assert_backward_close(gpu, orc, rtol=1e-4, atol_rel=1e-6, f64_bound=1e-4):
             for nm, g, r in (("dW", gpu["dW"][p], dW64[p]), ("dD", gpu["dD"][p], dD64[p])):
                 scale = np.abs(r).max()
                 err = np.abs(g.astype(np.float64) - r).max()
-                assert err <= f64_bound * scale + 1e-30, f"{nm}[{p}] vs fp64: {err / scale:.3g} of scale"
+                bound = f64_bound
+                if model_gap:
+                    m32 = (dW32 if nm == "dW" else dD32)[p]
+                    bound = max(bound, 2.0 * np.abs(m32.astype(np.float64) - r).max() / scale)
+                assert err <= bound * scale + 1e-30, f"{nm}[{p}] vs fp64: {err / scale:.3g} of scale"

@@ -253,3 +253,37 @@ def test_parity_two_layers_of_unequal_width():
     gpu, orc = _parity(wl)
     assert all(int(c.sum()) > 0 for c in orc["fwd"].count)
     _parity(wl, flags=snn.SNN_FLAG_HBM_RINGS)
+
+
+# ------------------------------------------------- long delays, fine grids
+
+
+@pytest.mark.parametrize("cid,B,rng_,flags", [
+    (4, 4, (255, 255, 255), 0),          # S = 256: delay and adjoint rings in device memory
+    (4, 4, (255, 50, 255), 0),
+    (4, 4, (0, 0, 0), 0),                # every delay zero (plain EventProp)
+    (3, 16, (255, 255, 255), 0),         # 128 posts: S = 256 rings still fit in LDS
+    (3, 16, (255, 255, 255), 1),
+])
+def test_parity_max_delay_sweep_shapes(cid, B, rng_, flags):
+    from workloads import make_variant
+    wl = make_variant(cid, B=B, delay_range=rng_)
+    gpu, orc = _parity(wl, flags=flags)
+    assert orc["fwd"].count.sum() > 0
+
+
+def test_parity_fine_dt_long_T():
+    """dt = 0.1 ms, T = 10^4 steps (the same 1 s trials at ten times the
+    resolution), delays up to 255 steps: the gradient kernel's trajectories
+    no longer fit 8 or 4 posts per workgroup, the readout tables leave LDS."""
+    from workloads import make_variant
+    wl = make_variant(4, B=2, T=10000, dt=0.1, delay_range=(255, 50, 255))
+    print(f"[parity] fine dt B={wl.B} T={wl.T}", flush=True)
+    gpu = run_gpu(wl)
+    orc = run_oracle(wl)
+    assert gpu["rc"] == 0 and orc["fwd"].count.sum() > 0
+    assert_forward_bitexact(gpu, orc, wl)
+    assert np.allclose(gpu["loss"], orc["loss"], rtol=1e-6, atol=1e-7)
+    # vs the fp32 model at the usual tolerance; vs fp64 within twice the
+    # model's own distance from it (about 1.3e-3 of scale here)
+    assert_backward_close(gpu, orc, model_gap=True)

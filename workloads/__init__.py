@@ -6,9 +6,10 @@ none of the method's arithmetic (no neuron dynamics, no loss, no gradients) and
 imports neither the HIP library nor the oracle.
 """
 from .configs import CONFIGS, INPUT, LIF, LI, LOSS_CE_SUM, LOSS_CE_MAX, projections, Config
-from .generators import Workload, make_workload, input_spikes, weights_and_delays, labels
+from .generators import (Workload, make_workload, make_variant, input_spikes,
+                         weights_and_delays, labels)
 
 __all__ = [
     "CONFIGS", "INPUT", "LIF", "LI", "LOSS_CE_SUM", "LOSS_CE_MAX", "projections", "Config",
-    "Workload", "make_workload", "input_spikes", "weights_and_delays", "labels",
+    "Workload", "make_workload", "make_variant", "input_spikes", "weights_and_delays", "labels",
 ]

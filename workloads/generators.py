@@ -137,3 +137,27 @@ def make_workload(cid: int, B: Optional[int] = None, T: Optional[int] = None,
     if weight_scale != 1.0:
         W = [(w * np.float32(weight_scale)).astype(np.float32) for w in W]
     return Workload(cfg, B, T, off, st, ne, W, D, labels(cfg, B))
+
+
+def make_variant(cid: int, B: Optional[int] = None, T: Optional[int] = None,
+                 dt: Optional[float] = None, delay_range: Optional[Sequence[int]] = None,
+                 name: Optional[str] = None) -> Workload:
+    """Config `cid` with another grid (dt, T) or other delay ranges (in steps),
+    drawn from the same seeds and weight means; the input generator keeps its
+    rates and times in ms, so a finer dt resolves the same spike trains."""
+    import dataclasses
+    base = CONFIGS[cid]
+    kw = {}
+    if dt is not None:
+        kw["dt"] = float(dt)
+    if T is not None:
+        kw["T"] = int(T)
+    if delay_range is not None:
+        if len(delay_range) != len(base.delay_range):
+            raise ValueError("one delay range per projection")
+        kw["delay_range"] = tuple(int(x) for x in delay_range)
+    cfg = dataclasses.replace(base, name=name or base.name, **kw)
+    B = cfg.B if B is None else B
+    off, st, ne = input_spikes(cfg, B, T=cfg.T)
+    W, D = weights_and_delays(cfg, mus=weight_means(base))
+    return Workload(cfg, B, cfg.T, off, st, ne, W, D, labels(cfg, B))
