@@ -12,6 +12,8 @@ library never imports it.
   system of Table 1 for tiny networks, with the exact EventProp backward and
   a finite-difference check; it pins the grid oracle.
 """
-from .grid import (OracleNet, constants, forward, loss, backward, lib_path, ForwardResult)
+from .grid import (OracleNet, constants, forward, loss, loss_dmse, first_spike_dlp, backward,
+                   lib_path, ForwardResult, LOSS_DMSE)
 
-__all__ = ["OracleNet", "constants", "forward", "loss", "backward", "lib_path", "ForwardResult"]
+__all__ = ["OracleNet", "constants", "forward", "loss", "loss_dmse", "first_spike_dlp", "backward",
+           "lib_path", "ForwardResult", "LOSS_DMSE"]

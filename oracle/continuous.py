@@ -8,9 +8,16 @@ time step shrinks.
 Model (Table 1): tau_m V' = -V + I, tau_s I' = -I between events; a LIF neuron
 spikes when V reaches theta from below and is reset to 0; a spike of neuron n
 at t_k makes I_m jump by w_mn at t_k + d_mn (real-valued delays >= 0).  The
-readout layer is LI (no threshold).  Loss, with per-readout weights c_k:
+readout layer is LI (no threshold), or LIF for the spike-time loss.  Loss,
+with per-readout weights c_k:
   "integral":  L = sum_k c_k * integral_0^T V_k dt   (a voltage loss l_V)
   "max":       L = sum_k c_k * max_t V_k(t)          (source at t_max)
+  "dmse":      L = 1/2 sum_{i != c} (t_i - t_c - Delta)^2 on the first spike
+               times t_i of a LIF output layer (T if none; c the label), the
+               time-invariant MSE of the Methods (a spike-time loss l_p)
+and optionally a spike-time term coef_l * t_k for every spike of a chosen
+LIF layer l (lp_lin = {l: coef_l}).  A spike-time loss adds dl_p/dt_k to the
+numerator of the jump at spike k (Table 1 backward transition).
 
 Backward (Table 1 and the Methods): between events the adjoints obey
 tau_m lambda_V' = -lambda_V - dl_V/dV and tau_s lambda_I' = -lambda_I + lambda_V
@@ -53,6 +60,7 @@ class ContNet:
     tau_s: float = 5.0
     theta: float = 1.0
     T: float = 60.0
+    out_lif: bool = False
 
     def __post_init__(self):
         self.L = len(self.sizes)
@@ -100,9 +108,12 @@ class ContNet:
 
     # ----- forward --------------------------------------------------------------------
     def forward(self, in_spikes: Sequence[Tuple[float, int]], loss: str = "integral",
-                c: Sequence[float] = None):
+                c: Sequence[float] = None, label: int = 0, delta: float = 0.0,
+                lp_lin: Dict[int, float] = None):
         """in_spikes: (time, input neuron).  Returns (L, record) with record the
         spike list [(t, layer, neuron, I_minus)] and the readout t_max list."""
+        assert (loss == "dmse") == self.out_lif
+        lp_lin = {} if lp_lin is None else dict(lp_lin)
         L_ = self.L
         out = L_ - 1
         c = [1.0] * self.sizes[out] if c is None else list(c)
@@ -133,7 +144,7 @@ class ContNet:
             t_next = min(t_next, self.T)
             # earliest threshold crossing in (t, t_next]
             tc, who = None, None
-            for l in range(1, L_ - 1):
+            for l in range(1, L_ if self.out_lif else L_ - 1):
                 for j in range(self.sizes[l]):
                     x = self._crossing(V[l][j], I[l][j], t_next - t)
                     if x is not None and (tc is None or x < tc):
@@ -160,11 +171,20 @@ class ContNet:
                 I[q][j] += w
             if t >= self.T:
                 break
+        first = [self.T] * self.sizes[out]
+        for (ts_, l, j, _) in spikes:
+            if l == out and first[j] == self.T:
+                first[j] = ts_
         if loss == "integral":
             Lval = sum(ck * v for ck, v in zip(c, integ))
-        else:
+        elif loss == "max":
             Lval = sum(ck * v for ck, v in zip(c, vmax))
-        return Lval, {"spikes": spikes, "tmax": tmax, "c": c, "loss": loss}
+        else:
+            Lval = 0.5 * sum((first[i] - first[label] - delta) ** 2
+                             for i in range(self.sizes[out]) if i != label)
+        Lval += sum(lp_lin.get(l, 0.0) * ts_ for (ts_, l, _, _) in spikes)
+        return Lval, {"spikes": spikes, "tmax": tmax, "c": c, "loss": loss, "first": first,
+                      "label": label, "delta": delta, "lp_lin": lp_lin}
 
     # ----- backward -------------------------------------------------------------------
     def backward(self, in_spikes, rec):
@@ -195,6 +215,22 @@ class ContNet:
         dW = [[[0.0] * self.sizes[q] for _ in range(self.sizes[a])] for (a, q, _, _) in self.proj]
         dD = [[[0.0] * self.sizes[q] for _ in range(self.sizes[a])] for (a, q, _, _) in self.proj]
         jsum = [0.0] * len(allspk)
+        # dl_p / dt_k of every spike: the time-invariant MSE at the first
+        # spike of each output neuron, and the linear spike-time terms
+        dlp = [0.0] * len(allspk)
+        lp_lin = rec.get("lp_lin", {})
+        seen = set()
+        for k, (tk, l, i, _) in enumerate(allspk):
+            if l == 0:
+                continue
+            dlp[k] += lp_lin.get(l, 0.0)
+            if loss == "dmse" and l == out and i not in seen:
+                seen.add(i)
+                f, lab, dl = rec["first"], rec["label"], rec["delta"]
+                if i != lab:
+                    dlp[k] += f[i] - f[lab] - dl
+                else:
+                    dlp[k] -= sum(f[m] - f[lab] - dl for m in range(self.sizes[out]) if m != lab)
         t = self.T
 
         def propagate(s):
@@ -218,15 +254,15 @@ class ContNet:
                 jsum[k] += W[i][j] * (lv[q][j] - li[q][j])
             elif kind == "spike":
                 k = pl
-                _, l, i, Im = allspk[k]
-                lv[l][i] += (th * lv[l][i] + jsum[k]) / (Im - th)
+                tk, l, i, Im = allspk[k]
+                lv[l][i] += (th * lv[l][i] + jsum[k] + dlp[k]) / (Im - th)
             else:
                 lv[out][pl] -= c[pl] / tm
         propagate(t)
         return dW, dD
 
     # ----- finite differences ---------------------------------------------------------
-    def fd(self, in_spikes, loss="integral", c=None, h=1e-6):
+    def fd(self, in_spikes, loss="integral", c=None, h=1e-6, **kw):
         dW = [[[0.0] * self.sizes[q] for _ in range(self.sizes[a])] for (a, q, _, _) in self.proj]
         dD = [[[0.0] * self.sizes[q] for _ in range(self.sizes[a])] for (a, q, _, _) in self.proj]
         for p, (a, q, W, D) in enumerate(self.proj):
@@ -235,9 +271,9 @@ class ContNet:
                     for M, G in ((W, dW), (D, dD)):
                         x0 = M[i][j]
                         M[i][j] = x0 + h
-                        lp, _ = self.forward(in_spikes, loss, c)
+                        lp, _ = self.forward(in_spikes, loss, c, **kw)
                         M[i][j] = x0 - h
-                        lm, _ = self.forward(in_spikes, loss, c)
+                        lm, _ = self.forward(in_spikes, loss, c, **kw)
                         M[i][j] = x0
                         G[p][i][j] = (lp - lm) / (2 * h)
         return dW, dD

@@ -31,11 +31,13 @@ def _load():
              C.c_int, C.c_int, C.c_int, C.c_float, ip, ip, ip, fp, fp, C.c_int,
              ip, ip, ip, fp, fp, ip, fp, fp, fp, lp])
         lib.oracle_loss.argtypes = [C.c_int, C.c_int, fp, ip, fp, fp]
+        lib.oracle_loss_dmse.argtypes = [C.c_int, C.c_int, fp, ip, C.c_float, fp, dp]
         lib.oracle_backward.argtypes = (
             [C.c_int, ip, ip, ip, C.c_float, C.c_float, C.c_float, C.c_float, C.c_int,
              C.c_int, C.c_int, C.c_int, C.c_float, ip, ip, ip, fp, fp, C.c_int,
-             ip, ip, ip, fp, fp, ip, C.c_int, dp, dp, lp])
-        for f in (lib.oracle_constants, lib.oracle_forward, lib.oracle_loss, lib.oracle_backward):
+             ip, ip, ip, fp, fp, ip, dp, C.c_int, dp, dp, lp])
+        for f in (lib.oracle_constants, lib.oracle_forward, lib.oracle_loss, lib.oracle_loss_dmse,
+                  lib.oracle_backward):
             f.restype = C.c_int
         _lib = lib
     return _lib
@@ -92,6 +94,11 @@ class OracleNet:
         return sum(1 for l in self.layers if l[1] == 1)
 
     @property
+    def cap_layers(self):
+        """Layers whose spikes are recorded (every LIF layer, output included)."""
+        return [l for l in self.layers[1:] if l[1] == 1]
+
+    @property
     def n_state(self):
         return sum(l[0] for l in self.layers[1:])
 
@@ -128,7 +135,7 @@ def forward(net: OracleNet, in_off, in_step, in_neuron, W: Sequence[np.ndarray],
     B = in_off.size - 1
     C_ = net.layers[-1][0]
     if cap is None:
-        cap = net.T * max([l[0] for l in net.layers[1:-1]] + [1])
+        cap = net.T * max([l[0] for l in net.cap_layers] + [1])
     nl = max(net.n_lif, 1)
     cnt = np.zeros((nl, B), np.int32)
     st = np.zeros((nl, B, cap), np.int32)
@@ -167,9 +174,49 @@ def loss(z: np.ndarray, labels) -> tuple:
     return lo, g
 
 
+LOSS_DMSE = 2
+
+
+def loss_dmse(z: np.ndarray, labels, delta: float) -> tuple:
+    """Time-invariant MSE on first output spike times z [B][C] (ms): per-sample
+    and mean loss [B+1] (fp32) and dL/dt_k of the batch mean [B][C] (fp64)."""
+    z = _f32(z)
+    labels = _i32(labels)
+    B, C_ = z.shape
+    lo = np.zeros(B + 1, np.float32)
+    dl = np.zeros((B, C_), np.float64)
+    rc = _load().oracle_loss_dmse(B, C_, _p(z, C.c_float), _p(labels, C.c_int), float(delta),
+                                  _p(lo, C.c_float), _p(dl, C.c_double))
+    if rc:
+        raise ValueError(f"oracle_loss_dmse rc={rc}")
+    return lo, dl
+
+
+def first_spike_dlp(net: OracleNet, fwd: ForwardResult, dl: np.ndarray) -> np.ndarray:
+    """Per-record dl_p/dt_k [n_lif][B][cap] for the time-invariant MSE: the
+    first spike of output neuron k in sample b carries dl[b][k], every other
+    record 0 (later spikes do not enter the loss)."""
+    nl = max(net.n_lif, 1)
+    B, cap = fwd.count.shape[1], fwd.cap
+    out = np.zeros((nl, B, cap), np.float64)
+    li = net.n_lif - 1                       # the output layer is the last LIF layer
+    for b in range(B):
+        seen = set()
+        for r in range(min(int(fwd.count[li, b]), cap)):
+            k = int(fwd.neuron[li, b, r])
+            if k not in seen:
+                seen.add(k)
+                out[li, b, r] = dl[b, k]
+    return out
+
+
 def backward(net: OracleNet, in_off, in_step, in_neuron, W: Sequence[np.ndarray],
-             D: Sequence[np.ndarray], fwd: ForwardResult, g: np.ndarray, mode: str = "f64"):
-    """Returns (dW list, dD list, degenerate count); fp64 arrays shaped like W."""
+             D: Sequence[np.ndarray], fwd: ForwardResult, g: np.ndarray, mode: str = "f64",
+             dlp: Optional[np.ndarray] = None):
+    """Returns (dW list, dD list, degenerate count); fp64 arrays shaped like W.
+    g: dL/dz of the voltage readout (CE losses; ignored for the spike-time
+    loss).  dlp: per-record dl_p/dt_k [n_lif][B][cap] (fp64) added to the
+    jump of every recorded spike, or None."""
     lib = _load()
     n, k, r = net.arrays()
     in_off, in_step, in_neuron = _i32(in_off), _i32(in_step), _i32(in_neuron)
@@ -179,6 +226,9 @@ def backward(net: OracleNet, in_off, in_step, in_neuron, W: Sequence[np.ndarray]
     dD = np.zeros(Wf.size, np.float64)
     stats = np.zeros(4, np.int64)
     g = _f32(g)
+    if dlp is not None:
+        dlp = np.ascontiguousarray(dlp, dtype=np.float64)
+        assert dlp.shape == (max(net.n_lif, 1), B, fwd.cap)
     rc = lib.oracle_backward(net.L, _p(n, C.c_int), _p(k, C.c_int), _p(r, C.c_int),
                              net.tau_m, net.tau_s, net.theta, net.dt, net.max_delay,
                              B, net.T, net.loss, net.readout_scale,
@@ -186,7 +236,7 @@ def backward(net: OracleNet, in_off, in_step, in_neuron, W: Sequence[np.ndarray]
                              _p(Wf, C.c_float), _p(Df, C.c_float), fwd.cap,
                              _p(fwd.count, C.c_int), _p(fwd.step, C.c_int), _p(fwd.neuron, C.c_int),
                              _p(fwd.I_minus, C.c_float), _p(g, C.c_float), _p(fwd.nstar, C.c_int),
-                             {"f64": 0, "f32": 1}[mode],
+                             _p(dlp, C.c_double), {"f64": 0, "f32": 1}[mode],
                              _p(dW, C.c_double), _p(dD, C.c_double), _p(stats, C.c_long))
     if rc:
         raise ValueError(f"oracle_backward rc={rc}")

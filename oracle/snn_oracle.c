@@ -24,6 +24,10 @@
  *        layer, in projection order; those cells are cleared.
  *     5. readout of the LI layer: sum  acc_k += V_k;  max  first argmax.
  *   z_k = s * acc_k (sum) or max_n V_k (max); CE loss; g = dL/dz.
+ *   With the spike-time loss (OR_LOSS_DMSE) the last layer is LIF instead:
+ *   z_k is the first spike time of output neuron k in ms (n dt; T dt when
+ *   it never fires) and the loss is the time-invariant MSE of the Methods,
+ *   L_b = 1/2 sum_{i != c} (t_i - t_c - Delta)^2 with c the label.
  *
  *   Backward, n = T-1 .. 0, lambda = 0, trajectory H[n][j] of (lambda_V,
  *   lambda_I):
@@ -38,7 +42,10 @@
  *        tau_m V-dot^- = I- - theta at a crossing, so
  *        lambda_V <- lambda_V + (theta lambda_V + A_i) / (I- - theta)
  *        (the lambda_V jump of Table 1 with the delayed postsynaptic sum);
- *        skipped and counted as degenerate if I- - theta <= 0.
+ *        skipped and counted as degenerate if I- - theta <= 0.  A
+ *        spike-time loss l_p adds its derivative dl_p/dt_k to the numerator
+ *        (Table 1 backward transition; Methods, time-invariant MSE): given
+ *        per record in rec_dlp.  There is no LI source then.
  *   Then the gradient sums over every presynaptic spike (n, i) (inputs and
  *   LIF records), in spike order, and post j with m = n + slot <= T-1:
  *     SU_ij += u,  SD_ij += w_ij (u - v),   (v, u) = H[m][j];
@@ -65,6 +72,7 @@
 #define OR_LI 2
 #define OR_LOSS_CE_SUM 0
 #define OR_LOSS_CE_MAX 1
+#define OR_LOSS_DMSE 2
 
 #define OR_OK 0
 #define OR_EINVAL (-1)
@@ -98,7 +106,7 @@ static int build_topo(topo_t* t, int L, const int* n, const int* kind, const int
         if (n[l] <= 0) return OR_EINVAL;
         if (l == 0 && kind[l] != OR_INPUT) return OR_EINVAL;
         if (l > 0 && l < L - 1 && kind[l] != OR_LIF) return OR_EINVAL;
-        if (l == L - 1 && kind[l] != OR_LI) return OR_EINVAL;
+        if (l == L - 1 && kind[l] != OR_LI && kind[l] != OR_LIF) return OR_EINVAL;
         if (rec[l] && kind[l] != OR_LIF) return OR_EINVAL;
     }
     t->P = 0;
@@ -184,7 +192,8 @@ int oracle_forward(int L, const int* n, const int* kind, const int* rec,
     int rc = build_topo(&t, L, n, kind, rec);
     if (rc) return rc;
     if (max_delay < 0 || max_delay > 255 || cap < 0) return OR_EINVAL;
-    if (loss != OR_LOSS_CE_SUM && loss != OR_LOSS_CE_MAX) return OR_EINVAL;
+    if (loss != OR_LOSS_CE_SUM && loss != OR_LOSS_CE_MAX && loss != OR_LOSS_DMSE) return OR_EINVAL;
+    if ((loss == OR_LOSS_DMSE) != (t.kind[L - 1] == OR_LIF)) return OR_EINVAL;
     rc = check_inputs(&t, B, T, in_off, in_step, in_neuron);
     if (rc) return rc;
     float k4[4];
@@ -210,8 +219,9 @@ int oracle_forward(int L, const int* n, const int* kind, const int* rec,
     int spk_n[OR_MAXL];
     float* acc = (float*)malloc(sizeof(float) * C);
     float* best = (float*)malloc(sizeof(float) * C);
-    if (!slot || !V || !I || !ring || !spk || !acc || !best) {
-        free(slot); free(V); free(I); free(ring); free(spk); free(acc); free(best);
+    int* first = (int*)malloc(sizeof(int) * C);
+    if (!slot || !V || !I || !ring || !spk || !acc || !best || !first) {
+        free(slot); free(V); free(I); free(ring); free(spk); free(acc); free(best); free(first);
         return OR_ENOMEM;
     }
     for (long k = 0; k < t.n_params; ++k) slot[k] = (unsigned char)delay_slot(D[k], max_delay, &clamped);
@@ -223,6 +233,7 @@ int oracle_forward(int L, const int* n, const int* kind, const int* rec,
         memset(ring, 0, sizeof(float) * (size_t)S * ring_w);
         for (int l = 0; l < L; ++l)
             if (t.lif_idx[l] >= 0) rec_count[(size_t)t.lif_idx[l] * B + b] = 0;
+        for (int k = 0; k < C; ++k) first[k] = -1;
         int cur = in_off[b];
         const int end = in_off[b + 1];
         for (int n_ = 0; n_ < T; ++n_) {
@@ -286,7 +297,14 @@ int oracle_forward(int L, const int* n, const int* kind, const int* rec,
                     *cell = 0.0f;
                 }
             }
-            /* 5. readout */
+            /* 5. readout: first spikes of a LIF output layer, or the LI voltages */
+            if (loss == OR_LOSS_DMSE) {
+                for (int q = 0; q < spk_n[out_l]; ++q) {
+                    const int k = spk[t.st_off[out_l] + q];
+                    if (first[k] < 0) first[k] = n_;
+                }
+                continue;
+            }
             for (int k = 0; k < C; ++k) {
                 const float v = V[t.st_off[out_l] + k];
                 if (loss == OR_LOSS_CE_SUM) {
@@ -297,15 +315,24 @@ int oracle_forward(int L, const int* n, const int* kind, const int* rec,
                 }
             }
         }
-        for (int k = 0; k < C; ++k)
-            z[(size_t)b * C + k] = (loss == OR_LOSS_CE_SUM) ? readout_scale * acc[k] : best[k];
-        if (loss == OR_LOSS_CE_SUM)
-            for (int k = 0; k < C; ++k) nstar[(size_t)b * C + k] = -1;
+        if (loss == OR_LOSS_DMSE) {
+            /* first spike times in ms, T dt for a neuron that never fires */
+            for (int k = 0; k < C; ++k) {
+                const int n0 = first[k] >= 0 ? first[k] : T;
+                z[(size_t)b * C + k] = (float)((double)n0 * (double)dt);
+                nstar[(size_t)b * C + k] = first[k];
+            }
+        } else {
+            for (int k = 0; k < C; ++k)
+                z[(size_t)b * C + k] = (loss == OR_LOSS_CE_SUM) ? readout_scale * acc[k] : best[k];
+            if (loss == OR_LOSS_CE_SUM)
+                for (int k = 0; k < C; ++k) nstar[(size_t)b * C + k] = -1;
+        }
         if (V_final) memcpy(V_final + (size_t)b * t.n_state, V, sizeof(float) * t.n_state);
         if (I_final) memcpy(I_final + (size_t)b * t.n_state, I, sizeof(float) * t.n_state);
     }
     if (stats) stats[0] = clamped;
-    free(slot); free(V); free(I); free(ring); free(spk); free(acc); free(best);
+    free(slot); free(V); free(I); free(ring); free(spk); free(acc); free(best); free(first);
     return overflow ? OR_EOVERFLOW : OR_OK;
 }
 
@@ -334,6 +361,35 @@ int oracle_loss(int B, int C, const float* z, const int* labels, float* loss_out
     return OR_OK;
 }
 
+/* Time-invariant MSE on first output spike times (Methods): t_k = z[b][k]
+ * in ms, c = labels[b]; L_b = 1/2 sum_{i != c} (t_i - t_c - delta)^2 in
+ * fp64; loss_out[b] = L_b, loss_out[B] = mean; dl[b][k] = dL/dt_k of the
+ * batch mean: (t_k - t_c - delta)/B for k != c and -sum_{i != c} (t_i - t_c
+ * - delta)/B for k = c. */
+int oracle_loss_dmse(int B, int C, const float* z, const int* labels, float delta, float* loss_out,
+                     double* dl) {
+    if (B <= 0 || C <= 0) return OR_EINVAL;
+    double total = 0.0;
+    for (int b = 0; b < B; ++b) {
+        const int c = labels[b];
+        if (c < 0 || c >= C) return OR_EINVAL;
+        const float* tb = z + (size_t)b * C;
+        double L = 0.0, sc = 0.0;
+        for (int k = 0; k < C; ++k) {
+            if (k == c) continue;
+            const double e = (double)tb[k] - (double)tb[c] - (double)delta;
+            L += 0.5 * e * e;
+            sc += e;
+            dl[(size_t)b * C + k] = e / (double)B;
+        }
+        dl[(size_t)b * C + c] = -sc / (double)B;
+        loss_out[b] = (float)L;
+        total += L;
+    }
+    loss_out[B] = (float)(total / (double)B);
+    return OR_OK;
+}
+
 /* fp32 rounding of a double that holds the exact result of one operation on
  * fp32 operands: equals the correctly rounded fp32 operation. */
 static inline double rnd(int f32, double x) { return f32 ? (double)(float)x : x; }
@@ -349,12 +405,15 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
                     const int* in_off, const int* in_step, const int* in_neuron,
                     const float* W, const float* D, int cap,
                     const int* rec_count, const int* rec_step, const int* rec_neuron,
-                    const float* rec_I, const float* g, const int* nstar, int mode,
+                    const float* rec_I, const float* g, const int* nstar,
+                    const double* rec_dlp, int mode,
                     double* dW, double* dD, long* stats) {
     topo_t t;
     int rc = build_topo(&t, L, n, kind, rec);
     if (rc) return rc;
     if (max_delay < 0 || max_delay > 255 || cap < 0 || (mode != 0 && mode != 1)) return OR_EINVAL;
+    if (loss != OR_LOSS_CE_SUM && loss != OR_LOSS_CE_MAX && loss != OR_LOSS_DMSE) return OR_EINVAL;
+    if ((loss == OR_LOSS_DMSE) != (t.kind[L - 1] == OR_LIF)) return OR_EINVAL;
     rc = check_inputs(&t, B, T, in_off, in_step, in_neuron);
     if (rc) return rc;
     for (int li = 0; li < t.n_lif; ++li)
@@ -403,7 +462,7 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
     for (int b = 0; b < B; ++b) {
         memset(lv, 0, sizeof(double) * t.n_state);
         memset(lI, 0, sizeof(double) * t.n_state);
-        for (int k = 0; k < C; ++k) {
+        for (int k = 0; k < C && loss != OR_LOSS_DMSE; ++k) {
             const double gk = (double)g[(size_t)b * C + k];
             const double sk = (loss == OR_LOSS_CE_SUM) ? (double)readout_scale * gk / (double)tau_m
                                                        : gk / (double)tau_m;
@@ -427,7 +486,7 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
                 h[2 * s + 1] = lI[s];
             }
             /* 3. loss source on the LI readout */
-            for (int k = 0; k < C; ++k) {
+            for (int k = 0; k < C && loss != OR_LOSS_DMSE; ++k) {
                 const int s = t.st_off[out_l] + k;
                 if (loss == OR_LOSS_CE_SUM || nstar[(size_t)b * C + k] == n_)
                     lv[s] = rnd(f32, lv[s] - src[k]);
@@ -468,7 +527,8 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
                     const int s = t.st_off[l] + rec_neuron[base + k];
                     const double den = rnd(f32, (double)rec_I[base + k] - (double)theta);
                     if (den > 0.0) {
-                        const double num = (double)theta * lv[s] + A[s];
+                        double num = (double)theta * lv[s] + A[s];
+                        if (rec_dlp) num += rec_dlp[base + k];
                         lv[s] = rnd(f32, lv[s] + rnd(f32, num / den));
                     } else {
                         ++degenerate;
