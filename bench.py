@@ -125,6 +125,9 @@ def sweep(args):
     import paper_2501_07331_amd as snn
     from workloads import make_variant
     assert torch.cuda.is_available(), "the sweep needs a GPU"
+    if args.sweep == "losses":
+        losses_bench(args)
+        return
     if args.sweep == "delay":
         pts = [int(x) for x in args.points.split(",")] if args.points else [0, 25, 50, 100, 150, 200, 255]
         cases = [dict(delay_range=(m, min(m, 50), m)) for m in pts]
@@ -185,6 +188,73 @@ def sweep(args):
         torch.cuda.empty_cache()
 
 
+def _time_steps(net, fwd_args, dW, dD, steps, warmup, dlp=None):
+    import torch
+    for _ in range(warmup):
+        net.forward(*fwd_args)
+        net.backward(dW, dD, dlp)
+    torch.cuda.synchronize()
+    kt = {}
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        net.forward(*fwd_args)
+        fwd = net.stats()["kernel_ms"]
+        net.backward(dW, dD, dlp)
+        bwd = net.stats()["kernel_ms"]
+        for k in ("input_scan", "forward_core", "readout_forward"):
+            kt.setdefault(k, []).append(fwd[k])
+        for k in ("readout_adjoint", "backward_core", "group", "gradients"):
+            kt.setdefault(k, []).append(bwd[k])
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / steps, {k: round(float(np.mean(v)), 4) for k, v in kt.items()}
+
+
+def losses_bench(args):
+    """Steps with spike-time loss terms: the time-invariant MSE on the first
+    spikes of a LIF output layer (the latency-coded 4-200-3 network, B = 256,
+    dt 0.1 ms, T 600), and the 700-256rec-20 step with a dl_p/dt_k term on
+    every hidden record (snn_backward_lp) beside the plain step."""
+    import torch
+    import paper_2501_07331_amd as snn
+    from workloads import LOSS_DMSE, make_variant, make_workload
+    dev = torch.device("cuda")
+    cases = [("latency-4-200-3lif dmse", make_variant(2, B=256, layers=((4, 0, 0), (200, 1, 0), (3, 1, 0)),
+                                                     loss=LOSS_DMSE, dmse_delta=1.0), False),
+             ("audio-700-256rec-20 plain", make_workload(4), False),
+             ("audio-700-256rec-20 + hidden dl_p/dt", make_workload(4), True)]
+    for name, wl, hidden_lp in cases:
+        c = wl.cfg
+        cap = 64 * max(l[0] for l in c.layers[1:] if l[1] == snn.SNN_LIF)
+        stream = torch.cuda.Stream()
+        with torch.cuda.stream(stream):
+            t = lambda a, dt_: torch.from_numpy(np.ascontiguousarray(a)).to(dev, dt_)
+            off, st, ne = t(wl.in_off, torch.int32), t(wl.in_step, torch.int32), t(wl.in_neuron, torch.int32)
+            W = [t(w, torch.float32) for w in wl.W]
+            D = [t(d, torch.float32) for d in wl.D]
+            labels = t(wl.labels, torch.int32)
+            nl = sum(1 for l in c.layers if l[1] == snn.SNN_LIF)
+            recs = [(torch.zeros(wl.B, dtype=torch.int32, device=dev),
+                     torch.zeros(wl.B, cap, dtype=torch.int32, device=dev),
+                     torch.zeros(wl.B, cap, dtype=torch.int32, device=dev)) for _ in range(nl)]
+            loss = torch.zeros(wl.B + 1, device=dev)
+            dW = [torch.zeros_like(w) for w in W]
+            dD = [torch.zeros_like(w) for w in W]
+            net = snn.Network(c.layers, c.tau_m, c.tau_s, c.theta, c.dt, c.max_delay, wl.B, wl.T,
+                              c.loss, c.readout_scale, cap, flags=snn.SNN_FLAG_TIMING, stream=stream,
+                              dmse_delta=c.dmse_delta)
+            dlp = None
+            if hidden_lp:
+                dlp = [torch.full((wl.B, cap), 1e-4, device=dev)]
+            el, kt = _time_steps(net, (off, st, ne, W, D, labels, recs, loss), dW, dD, args.steps,
+                                 args.warmup, dlp)
+            s = net.stats()
+            net.close()
+        print(json.dumps({"sweep": "losses", "workload": name, "B": wl.B, "T": wl.T, "dt_ms": c.dt,
+                          "ms_per_step": round(1e3 * el, 4), "events": s["events"],
+                          "events_per_s": s["events"] / el, "loss": float(loss[-1].item()),
+                          "kernel_ms": kt}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -195,10 +265,10 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (the reference "
                          "kernel the HBM byte counters are scaled by) and exit")
-    ap.add_argument("--sweep", choices=("delay", "dt"), default=None,
+    ap.add_argument("--sweep", choices=("delay", "dt", "losses"), default=None,
                     help="instead of the single line: time the 700-256rec-20 step over a range "
-                         "of maximum delays (dt 1 ms) or of time steps (the same 1 s trials), "
-                         "one JSON line per point")
+                         "of maximum delays (dt 1 ms) or of time steps (the same 1 s trials), or "
+                         "the steps with spike-time loss terms; one JSON line per point")
     ap.add_argument("--points", type=str, default=None,
                     help="comma-separated sweep points (max delays in steps, or dt in ms)")
     args = ap.parse_args()

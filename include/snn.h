@@ -9,7 +9,8 @@
  *
  * Model.  Layer 0 is an input layer of spike sources, layers 1 .. L-2 are LIF
  * layers (optionally recurrent), layer L-1 is a leaky-integrator (LI) readout,
- * i.e. a LIF layer with an infinite threshold (Table 1 caption).  Between
+ * i.e. a LIF layer with an infinite threshold (Table 1 caption), or, with the
+ * spike-time loss, a spiking LIF output layer.  Between
  * events tau_m V' = -V + I and tau_s I' = -I; a LIF neuron spikes when V
  * reaches theta and is reset to 0; a spike of neuron i at step n makes the
  * current of post neuron j jump by w_ij at step n + d_ij (Table 1, forward).
@@ -73,7 +74,7 @@ enum {
 };
 
 enum { SNN_INPUT = 0, SNN_LIF = 1, SNN_LI = 2 };                /* layer kinds */
-enum { SNN_LOSS_CE_SUM = 0, SNN_LOSS_CE_MAX = 1 };               /* readout losses */
+enum { SNN_LOSS_CE_SUM = 0, SNN_LOSS_CE_MAX = 1, SNN_LOSS_DMSE = 2 };   /* losses */
 
 #define SNN_MAX_LAYERS 6
 #define SNN_MAX_NEURONS 1024   /* per non-input layer */
@@ -93,7 +94,15 @@ typedef struct {
  * loss:             SNN_LOSS_CE_SUM: z_k = readout_scale * sum_n V_k,n;
  *                   SNN_LOSS_CE_MAX: z_k = max_n V_k,n (first maximiser);
  *                   softmax cross-entropy on z, mean over the batch
- *                   (voltage-based readouts of Fig. 1 and the Results)
+ *                   (voltage-based readouts of Fig. 1 and the Results);
+ *                   SNN_LOSS_DMSE: the last layer is LIF (not recurrent) and
+ *                   z_k is the first spike time of output neuron k in ms
+ *                   (n dt in fp64, rounded to fp32; T dt if it never fires);
+ *                   the loss is the time-invariant mean squared error of the
+ *                   Methods, L_b = 1/2 sum_{i != c} (z_i - z_c - dmse_delta)^2
+ *                   with c = labels[b], mean over the batch; it enters the
+ *                   backward pass as dL/dt_k at the first spike of each
+ *                   output neuron (a neuron that never fires carries none)
  * readout_scale:    s above (sum readout only)
  * record_capacity:  spike records kept per sample and LIF layer
  * flags:            bitwise OR of
@@ -103,6 +112,7 @@ typedef struct {
  *                   SNN_FLAG_TIMING: time the main kernels with HIP events
  *                   on hip_stream (reported by snn_get_stats)
  * hip_stream:       hipStream_t to enqueue on (NULL: default stream)
+ * dmse_delta:       Delta_t of the spike-time loss, in ms (SNN_LOSS_DMSE)
  */
 #define SNN_FLAG_HBM_RINGS 1
 #define SNN_FLAG_TIMING 2
@@ -113,6 +123,7 @@ typedef struct {
     int32_t record_capacity;
     int32_t flags;
     void* hip_stream;
+    float dmse_delta;
 } snn_opts;
 
 /* Input spikes, CSR over samples (dev): offsets [batch+1] with offsets[0] = 0
@@ -153,8 +164,10 @@ typedef struct {
 
 /*
  * Build a network handle: validates the topology (layer 0 SNN_INPUT, layers
- * 1 .. L-2 SNN_LIF, last layer SNN_LI, 2 <= L <= SNN_MAX_LAYERS, non-input
- * layers of 1 .. SNN_MAX_NEURONS neurons, only LIF layers recurrent),
+ * 1 .. L-2 SNN_LIF, last layer SNN_LI, or a non-recurrent SNN_LIF with
+ * SNN_LOSS_DMSE, 2 <= L <= SNN_MAX_LAYERS, at most SNN_MAX_LAYERS - 2 LIF
+ * layers, non-input layers of 1 .. SNN_MAX_NEURONS neurons, only LIF layers
+ * recurrent),
  * computes the fp32 constants on the host in fp64, and allocates the device
  * scratch for opts->batch samples.  dt > 0, tau_m != tau_s, both > 0,
  * 0 <= max_delay <= SNN_MAX_DELAY.  No device compute.  *out receives the
@@ -174,9 +187,11 @@ int snn_projection_info(const snn_net* net, int32_t p, int32_t* pre_layer, int32
  *   W, D:     host arrays of P device pointers, projection p [n_pre][n_post]
  *             fp32; D in steps
  *   labels:   (dev) [batch] class indices in [0, C)
- *   records:  host array of one snn_spikes_out per LIF layer (dev buffers)
- *   loss:     (dev) [batch + 1] per-sample CE, then the batch mean
- *   z:        (dev) [batch][C] readout values, or NULL
+ *   records:  host array of one snn_spikes_out per LIF layer (dev buffers;
+ *             the LIF output layer of SNN_LOSS_DMSE included, last)
+ *   loss:     (dev) [batch + 1] per-sample loss, then the batch mean
+ *   z:        (dev) [batch][C] readout values (first spike times for
+ *             SNN_LOSS_DMSE), or NULL
  * The library keeps in, W, D and labels for snn_backward: the caller keeps
  * them alive and unmodified until the matching snn_backward returns.
  * Errors: SNN_EINVAL (NULL pointers, bad input spikes, bad labels),
@@ -198,6 +213,22 @@ int snn_forward(snn_net* net, const snn_spikes_in* in, const float* const* W, co
  * SNN_EOVERFLOW (the forward overflowed its records), SNN_EINVAL, SNN_EDEVICE.
  */
 int snn_backward(snn_net* net, float* const* dW, float* const* dD);
+
+/*
+ * snn_backward with a spike-time loss term on any LIF layer: the derivative
+ * dl_p/dt_k of an extra loss l_p(spike times) with respect to the time (in
+ * ms) of each recorded spike is added to the numerator of that spike's
+ * lambda_V jump (Table 1 backward transition; Methods, the jump with
+ * dl_p/dt_k), on top of the loss chosen at creation.
+ *   dlp:      host array of one device pointer per LIF layer (in layer
+ *             order, as the records), each [batch][record_capacity] fp32 in
+ *             the order of that layer's records of the last forward, or
+ *             NULL (no term on that layer); dlp itself may be NULL.  Entries
+ *             past a sample's count are ignored.  For the gradient of a
+ *             batch-mean loss the caller includes the 1/batch.
+ * The term is added in fp64.  Errors as snn_backward.
+ */
+int snn_backward_lp(snn_net* net, const float* const* dlp, float* const* dW, float* const* dD);
 
 /*
  * Parameter update after snn_backward: one optimiser step on every W and D,

@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 
 SNN_OK, SNN_EINVAL, SNN_ENOMEM, SNN_ESTATE, SNN_EOVERFLOW, SNN_EDEVICE = 0, -1, -2, -3, -4, -5
 SNN_INPUT, SNN_LIF, SNN_LI = 0, 1, 2
-SNN_LOSS_CE_SUM, SNN_LOSS_CE_MAX = 0, 1
+SNN_LOSS_CE_SUM, SNN_LOSS_CE_MAX, SNN_LOSS_DMSE = 0, 1, 2
 SNN_FLAG_HBM_RINGS = 1
 SNN_FLAG_TIMING = 2
 SNN_OPT_SGD, SNN_OPT_ADAM = 0, 1
@@ -34,7 +34,7 @@ class snn_layer(C.Structure):
 class snn_opts(C.Structure):
     _fields_ = [("batch", C.c_int32), ("T", C.c_int32), ("loss", C.c_int32),
                 ("readout_scale", C.c_float), ("record_capacity", C.c_int32),
-                ("flags", C.c_int32), ("hip_stream", C.c_void_p)]
+                ("flags", C.c_int32), ("hip_stream", C.c_void_p), ("dmse_delta", C.c_float)]
 
 
 class snn_spikes_in(C.Structure):
@@ -90,6 +90,7 @@ def load_library():
     lib.snn_forward.argtypes = [P, C.POINTER(snn_spikes_in), C.POINTER(P), C.POINTER(P), P,
                                 C.POINTER(snn_spikes_out), P, P]
     lib.snn_backward.argtypes = [P, C.POINTER(P), C.POINTER(P)]
+    lib.snn_backward_lp.argtypes = [P, C.POINTER(P), C.POINTER(P), C.POINTER(P)]
     lib.snn_optimizer_step.argtypes = [P, C.POINTER(snn_optim), C.POINTER(P), C.POINTER(P),
                                        C.POINTER(P), C.POINTER(P)]
     lib.snn_optimizer_reset.argtypes = [P]
@@ -100,7 +101,7 @@ def load_library():
     lib.snn_destroy.argtypes = [P]
     lib.snn_destroy.restype = None
     for f in ("snn_create", "snn_num_projections", "snn_projection_info", "snn_forward",
-              "snn_backward", "snn_optimizer_step", "snn_optimizer_reset", "snn_get_state",
+              "snn_backward", "snn_backward_lp", "snn_optimizer_step", "snn_optimizer_reset", "snn_get_state",
               "snn_get_stats"):
         getattr(lib, f).restype = C.c_int
     _lib = lib
@@ -133,7 +134,8 @@ class Network:
 
     def __init__(self, layers: Sequence[Tuple[int, int, int]], tau_m: float, tau_s: float,
                  theta: float, dt: float, max_delay: int, batch: int, T: int, loss: int,
-                 readout_scale: float, record_capacity: int, flags: int = 0, stream=None):
+                 readout_scale: float, record_capacity: int, flags: int = 0, stream=None,
+                 dmse_delta: float = 0.0):
         import torch
         self._lib = load_library()
         self.layers = [tuple(int(x) for x in l) for l in layers]
@@ -145,7 +147,7 @@ class Network:
         self.stream = stream
         arr = (snn_layer * len(layers))(*[snn_layer(*l) for l in self.layers])
         opts = snn_opts(self.batch, self.T, int(loss), float(readout_scale), self.record_capacity,
-                        int(flags), C.c_void_p(stream.cuda_stream))
+                        int(flags), C.c_void_p(stream.cuda_stream), float(dmse_delta))
         h = C.c_void_p()
         rc = self._lib.snn_create(arr, len(layers), tau_m, tau_s, theta, dt, int(max_delay),
                                   C.byref(opts), C.byref(h))
@@ -208,13 +210,26 @@ class Network:
                                    _ptr(loss, f32, "loss"), _ptr(z, f32, "z") if z is not None else None)
         return self._check(rc)
 
-    def backward(self, dW, dD):
+    def backward(self, dW, dD, dlp=None):
+        """dlp: None, or one entry per LIF layer: None or an fp32 [B][cap]
+        device tensor of dl_p/dt_k per record (snn_backward_lp)."""
         import torch
         f32 = torch.float32
         for p, (_, _, npre, npost) in enumerate(self.projections):
             if dW[p].numel() != npre * npost or dD[p].numel() != npre * npost:
                 raise ValueError(f"dW/dD[{p}] must hold {npre}x{npost} elements")
-        rc = self._lib.snn_backward(self._h, _ptr_array(dW, f32, "dW"), _ptr_array(dD, f32, "dD"))
+        if dlp is None:
+            rc = self._lib.snn_backward(self._h, _ptr_array(dW, f32, "dW"), _ptr_array(dD, f32, "dD"))
+            return self._check(rc)
+        if len(dlp) != len(self.lif_layers):
+            raise ValueError("one dlp entry (or None) per LIF layer")
+        arr = (C.c_void_p * max(len(dlp), 1))()
+        for i, x in enumerate(dlp):
+            if x is not None and x.numel() != self.batch * self.record_capacity:
+                raise ValueError("dlp entries must be [B][record_capacity]")
+            arr[i] = _ptr(x, f32, f"dlp[{i}]") if x is not None else None
+        rc = self._lib.snn_backward_lp(self._h, arr, _ptr_array(dW, f32, "dW"),
+                                       _ptr_array(dD, f32, "dD"))
         return self._check(rc)
 
     def optimizer_step(self, W, D, dW, dD, kind: int = SNN_OPT_ADAM, lr_w: float = 1e-3,

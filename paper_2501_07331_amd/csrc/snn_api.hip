@@ -22,6 +22,7 @@ size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
 struct snn_net {
     Topo t;
     float tau_m, tau_s, theta, dt;
+    float dmse_delta;
     int max_delay;
     int core_threads;           // LIF-core workgroup size
     int read_threads;           // readout workgroup size
@@ -67,6 +68,9 @@ struct snn_net {
     double* A2;
     double* gpart;
     float* mom;                 // Adam moments [4][n_params], allocated by the first Adam step
+    double* xlp_out;            // spike-time loss: jump terms of the output layer's records [B][cap]
+    double* jx[SNN_MAX_LIF];    // per LIF layer: jump terms with the caller's dl_p/dt [B][cap]
+    int ran[K_N];               // kernels enqueued (and timed) by the last call
     long long adam_steps;
     int* in_goff;
     int* in_gstep;
@@ -108,13 +112,15 @@ static void free_all(snn_net* n) {
                     n->rec_idx, n->rec_cnt, n->rec_goff, n->rec_gstep, n->z,      n->nstar,
                     n->src,     n->Vf,      n->If,       n->table,     n->tu_lif, n->td_lif,
                     n->tu_out,  n->td_out,  n->A2,       n->in_goff,   n->in_gstep, n->st,
-                    n->gpart,   n->ws,      n->steptab, n->mom};
+                    n->gpart,   n->ws,      n->steptab, n->mom,   n->xlp_out};
     for (void* p : bufs)
         if (p) (void)hipFree(p);
     for (int p = 0; p < SNN_MAXP; ++p)
         if (n->fring[p]) (void)hipFree(n->fring[p]);
     for (int l = 0; l < SNN_MAX_LAYERS; ++l)
         if (n->bring[l]) (void)hipFree(n->bring[l]);
+    for (int l = 0; l < SNN_MAX_LIF; ++l)
+        if (n->jx[l]) (void)hipFree(n->jx[l]);
     if (n->st_host) (void)hipHostFree(n->st_host);
     for (int i = 0; i < 2 * K_N; ++i)
         if (n->ev[i]) (void)hipEventDestroy(n->ev[i]);
@@ -145,17 +151,25 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     if (!(theta == theta)) return SNN_EINVAL;
     if (max_delay < 0 || max_delay > SNN_MAX_DELAY) return SNN_EINVAL;
     if (opts->batch < 1 || opts->T < 1 || opts->record_capacity < 0) return SNN_EINVAL;
-    if (opts->loss != SNN_LOSS_CE_SUM && opts->loss != SNN_LOSS_CE_MAX) return SNN_EINVAL;
+    if (opts->loss != SNN_LOSS_CE_SUM && opts->loss != SNN_LOSS_CE_MAX &&
+        opts->loss != SNN_LOSS_DMSE)
+        return SNN_EINVAL;
+    const bool dmse = opts->loss == SNN_LOSS_DMSE;
+    if (dmse && (!(opts->dmse_delta == opts->dmse_delta) || isinf(opts->dmse_delta) ||
+                 opts->record_capacity < 1))
+        return SNN_EINVAL;
     if (opts->flags & ~(SNN_FLAG_HBM_RINGS | SNN_FLAG_TIMING)) return SNN_EINVAL;
     for (int l = 0; l < n_layers; ++l) {
         const snn_layer& y = layers[l];
         if (y.n < 1) return SNN_EINVAL;
         if (l == 0 && (y.kind != SNN_INPUT || y.n > SNN_MAX_INPUT)) return SNN_EINVAL;
         if (l > 0 && l < n_layers - 1 && y.kind != SNN_LIF) return SNN_EINVAL;
-        if (l == n_layers - 1 && y.kind != SNN_LI) return SNN_EINVAL;
-        if (y.recurrent && y.kind != SNN_LIF) return SNN_EINVAL;
+        if (l == n_layers - 1 && y.kind != (dmse ? SNN_LIF : SNN_LI)) return SNN_EINVAL;
+        if (y.recurrent && (y.kind != SNN_LIF || l == n_layers - 1)) return SNN_EINVAL;
         if (l > 0 && y.n > SNN_MAX_NEURONS) return SNN_EINVAL;
     }
+    // the kernels hold per-LIF-layer state for at most SNN_MAX_LIF layers
+    if (dmse && n_layers - 1 > SNN_MAX_LIF) return SNN_EINVAL;
     // the gradient kernel stages (lambda_I, lambda_I - lambda_V) of T steps in LDS
     if ((size_t)opts->T * 2 * sizeof(float) > kLds) return SNN_EINVAL;
     if ((long long)opts->batch * (opts->T + 1) > (1LL << 31)) return SNN_EINVAL;
@@ -186,6 +200,7 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     net->theta = theta;
     net->dt = dt;
     net->max_delay = max_delay;
+    net->dmse_delta = opts->dmse_delta;
     net->stream = (hipStream_t)opts->hip_stream;
     const bool hbm = (opts->flags & SNN_FLAG_HBM_RINGS) != 0;
 
@@ -209,6 +224,7 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     }
     net->n_state = so;
     t.out_l = n_layers - 1;
+    t.out_lif = dmse ? 1 : 0;
     long long off = 0;
     for (int l = 1; l < n_layers; ++l) {
         for (int r = 0; r < 1 + (layers[l].recurrent ? 1 : 0); ++r) {
@@ -338,7 +354,7 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
             g = GradGroup{};
             g.nq = t.n[q];
             g.jb = (g.nq + J - 1) / J;
-            g.out = (q == t.out_l) ? 1 : 0;
+            g.out = (q == t.out_l && !t.out_lif) ? 1 : 0;
             g.off = g.out ? 0 : t.lif_off[q];
             for (int p = 0; p < t.P; ++p) {
                 if (t.post[p] != q) continue;
@@ -410,7 +426,8 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     ALLOC(net->tu_out, B * T * C);
     ALLOC(net->td_out, B * T * C);
     if (net->grad_SB > 1) ALLOC(net->gpart, (size_t)net->grad_SB * 2 * (size_t)net->n_params);
-    if (feed != 0) ALLOC(net->A2, B * cap);
+    if (feed != 0 && !t.out_lif) ALLOC(net->A2, B * cap);
+    if (t.out_lif) ALLOC(net->xlp_out, B * cap);
     ALLOC(net->in_goff, B * (t.n_in + 1));
     ALLOC(net->st, 1);
 #undef ALLOC
@@ -475,17 +492,18 @@ static int read_status(snn_net* net) {
 
 #define TIMED(net, k, expr)                                                                 \
     do {                                                                                    \
+        (net)->ran[k] = 1;                                                                  \
         if ((net)->timing) HIP_TRY(net, hipEventRecord((net)->ev[2 * (k)], (net)->stream)); \
         HIP_TRY(net, expr);                                                                 \
         if ((net)->timing)                                                                  \
             HIP_TRY(net, hipEventRecord((net)->ev[2 * (k) + 1], (net)->stream));           \
     } while (0)
 
-static int collect_times(snn_net* net, int k0, int k1, bool has_core) {
+static int collect_times(snn_net* net, int k0, int k1) {
     if (!net->timing) return SNN_OK;
     for (int k = k0; k < k1; ++k) {
         net->stats.kernel_ms[k] = 0.0f;
-        if (!has_core && (k == K_CORE || k == K_BCORE)) continue;
+        if (!net->ran[k]) continue;
         HIP_TRY(net, hipEventElapsedTime(&net->stats.kernel_ms[k], net->ev[2 * k], net->ev[2 * k + 1]));
     }
     return SNN_OK;
@@ -512,6 +530,7 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
     }
     hipStream_t s = net->stream;
     const int C = t.n[t.out_l];
+    for (int k = K_SCAN; k < K_RADJ; ++k) net->ran[k] = 0;
     HIP_TRY(net, launch_reset_status(net->st, s));
     HIP_TRY(net, launch_validate(in->offsets, in->step, in->neuron, in->nnz, t.B, t.T, t.n_in, labels,
                                  C, net->st, s));
@@ -610,23 +629,31 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
         a.zw_off = net->zw_off;
         TIMED(net, K_CORE, launch_forward_core(a, t.n_lif, net->core_threads, net->lds_core_f, s));
     }
-    ReadoutArgs r{};
-    r.t = t;
-    r.ws = net->ws + t.woff[t.out_p];
-    r.A_in = net->A_in;
-    r.rec_n = net->rec_n;
-    r.rec_s = net->rec_s;
-    r.rec_idx = net->rec_idx;
-    r.table = net->table;
-    r.table_lds = net->table_lds;
-    r.z = net->z;
-    r.nstar = net->nstar;
-    r.Vf = net->Vf;
-    r.If = net->If;
-    r.st = net->st;
-    TIMED(net, K_READ, launch_readout_forward(r, net->read_threads, net->lds_read, s));
-    HIP_TRY(net, launch_loss(net->z, labels, t.B, C, t.loss, t.rscale, net->tau_m, loss, net->src,
-                             net->st, s));
+    if (t.out_lif) {
+        // spike-time loss on the first spikes of the LIF output layer
+        const size_t li = (size_t)t.lif[t.out_l], B = t.B, cap = t.cap;
+        HIP_TRY(net, launch_dmse_loss(net->rec_cnt + li * B, net->rec_s + li * B * cap,
+                                      net->rec_n + li * B * cap, t.cap, labels, t.B, C, t.T, t.dt,
+                                      net->dmse_delta, net->z, loss, net->xlp_out, net->st, s));
+    } else {
+        ReadoutArgs r{};
+        r.t = t;
+        r.ws = net->ws + t.woff[t.out_p];
+        r.A_in = net->A_in;
+        r.rec_n = net->rec_n;
+        r.rec_s = net->rec_s;
+        r.rec_idx = net->rec_idx;
+        r.table = net->table;
+        r.table_lds = net->table_lds;
+        r.z = net->z;
+        r.nstar = net->nstar;
+        r.Vf = net->Vf;
+        r.If = net->If;
+        r.st = net->st;
+        TIMED(net, K_READ, launch_readout_forward(r, net->read_threads, net->lds_read, s));
+        HIP_TRY(net, launch_loss(net->z, labels, t.B, C, t.loss, t.rscale, net->tau_m, loss,
+                                 net->src, net->st, s));
+    }
     if (z)
         HIP_TRY(net, hipMemcpyAsync(z, net->z, sizeof(float) * t.B * C, hipMemcpyDeviceToDevice, s));
     int rc = read_status(net);
@@ -635,7 +662,7 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
     if (h.bad_input)
         return fail(net, SNN_EINVAL, "input spikes or labels invalid (offsets, range, order)");
     memset(&net->stats, 0, sizeof(net->stats));
-    rc = collect_times(net, K_SCAN, K_RADJ, t.n_lif > 0);
+    rc = collect_times(net, K_SCAN, K_RADJ);
     if (rc) return rc;
     net->stats.input_spikes = in->nnz;
     net->stats.clamped_delays = (int64_t)h.clamped;
@@ -662,6 +689,11 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
 }
 
 extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
+    return snn_backward_lp(net, nullptr, dW, dD);
+}
+
+extern "C" int snn_backward_lp(snn_net* net, const float* const* dlp, float* const* dW,
+                               float* const* dD) {
     if (!net) return SNN_EINVAL;
     net->err[0] = 0;
     Topo& t = net->t;
@@ -672,6 +704,21 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
     for (int p = 0; p < t.P; ++p)
         if (!dW[p] || !dD[p]) return fail(net, SNN_EINVAL, "NULL dW or dD of projection %d", p);
     hipStream_t s = net->stream;
+    for (int k = K_RADJ; k < K_N; ++k) net->ran[k] = 0;
+    // per-record jump terms from the caller on a LIF layer: device room for
+    // their fp64 sums (first use of the layer)
+    bool has_lp[SNN_MAX_LIF] = {false};
+    for (int li = 0; dlp && li < t.n_lif; ++li) {
+        if (!dlp[li] || t.cap < 1) continue;
+        has_lp[li] = true;
+        if (net->jx[li]) continue;
+        const hipError_t e = hipMalloc((void**)&net->jx[li], (size_t)t.B * t.cap * sizeof(double));
+        if (e != hipSuccess) {
+            net->jx[li] = nullptr;
+            return fail(net, e == hipErrorOutOfMemory ? SNN_ENOMEM : SNN_EDEVICE, "hipMalloc: %s",
+                        hipGetErrorString(e));
+        }
+    }
     // the grouped input steps need one slot per input spike of the last forward
     if (net->in_nnz > net->in_gstep_cap) {
         HIP_TRY(net, hipStreamSynchronize(s));
@@ -690,6 +737,7 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
     const hipStream_t g_s = net->aux;
     HIP_TRY(net, hipEventRecord(net->fork, s));
     HIP_TRY(net, hipStreamWaitEvent(g_s, net->fork, 0));
+    net->ran[K_GROUP] = 1;
     if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GROUP], g_s));
     {
         GroupArgs g{};
@@ -722,7 +770,7 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
     const int C = t.n[t.out_l];
     const int feed = t.pre[t.out_p];
     const size_t B = t.B, cap = t.cap;
-    {
+    if (!t.out_lif) {
         ReadoutBwdArgs r{};
         r.B = t.B;
         r.T = t.T;
@@ -746,6 +794,22 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
         r.A2 = net->A2;
         r.tab_lds = net->radj_tab;
         TIMED(net, K_RADJ, launch_readout_adjoint(r, net->radj_threads, net->lds_radj, s));
+    }
+    // extra jump numerators per LIF layer: the readout part of the jump sums
+    // (the layer feeding an LI readout), the spike-time loss's terms (LIF
+    // output layer), plus the caller's dl_p/dt
+    const double* jump_x[SNN_MAX_LIF] = {nullptr};
+    for (int l = 1; l < t.L; ++l) {
+        if (t.kind[l] != SNN_LIF) continue;
+        const int li = t.lif[l];
+        const double* own = (!t.out_lif && l == feed) ? net->A2 : (t.out_lif && l == t.out_l) ? net->xlp_out : nullptr;
+        if (has_lp[li]) {
+            double* dst = (own == net->A2 && own) ? net->A2 : net->jx[li];
+            HIP_TRY(net, launch_add_lp(dst, own, dlp[li], net->rec_cnt + (size_t)li * B, t.B, t.cap, s));
+            jump_x[li] = dst;
+        } else {
+            jump_x[li] = own;
+        }
     }
     if (t.n_lif > 0) {
         CoreBwdArgs a{};
@@ -792,11 +856,10 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
             y.recI = net->rec_I + li * B * cap;
             y.recn = net->rec_n + li * B * cap;
             y.steptab = net->steptab + li * B * (size_t)t.T * SNN_STEP_ROW;
-            y.use_a2 = (l == feed) ? 1 : 0;
+            y.A2 = jump_x[li];
         }
         a.tu = net->tu_lif;
         a.td = net->td_lif;
-        a.A2 = net->A2;
         a.st = net->st;
         a.part_off = net->bpart_off;
         TIMED(net, K_BCORE,
@@ -836,13 +899,14 @@ extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
     }
     for (int g = 0; g < net->grad_ngroups; ++g) ga.grp[g] = net->grad_grp[g];
     ga.part = net->gpart;
+    net->ran[K_GRAD] = 1;
     if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GRAD], s));
     HIP_TRY(net, launch_gradients(ga, net->grad_J, net->grad_KL, net->grad_threads, net->lds_grad, s));
     if (ga.SB > 1) HIP_TRY(net, launch_grad_reduce(ga, t.P, s));
     if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GRAD + 1], s));
     int rc = read_status(net);
     if (rc) return rc;
-    rc = collect_times(net, K_RADJ, K_N, t.n_lif > 0);
+    rc = collect_times(net, K_RADJ, K_N);
     if (rc) return rc;
     net->stats.degenerate_jumps = (int64_t)net->st_host->degenerate;
     return SNN_OK;

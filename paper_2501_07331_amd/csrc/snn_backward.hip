@@ -188,7 +188,7 @@ struct BwdCore {
         if (mine) {
             const size_t r = (size_t)b * a.cap + (ri + r0 + mine - 1);
             I = y.recI[r];
-            A2 = a.A2[r];
+            A2 = y.A2 ? y.A2[r] : 0.0;
         }
     }
 
@@ -362,7 +362,7 @@ struct BwdCore {
             for (int l = 0; l < NL; ++l) {
                 if (!A.mine[l]) continue;
                 const double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
-                jump(a, part_l, A.mine[l] - 1, A.I[l], a.ly[l].use_a2 ? A.A2[l] : 0.0, L.lv[l], L.deg);
+                jump(a, part_l, A.mine[l] - 1, A.I[l], A.A2[l], L.lv[l], L.deg);
             }
         }
         // ---- further rounds when a step has more than KP spikes
@@ -394,7 +394,7 @@ struct BwdCore {
             for (int l = 0; l < NL; ++l) {
                 if (!mine[l]) continue;
                 const double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
-                jump(a, part_l, mine[l] - 1, I[l], a.ly[l].use_a2 ? A2[l] : 0.0, L.lv[l], L.deg);
+                jump(a, part_l, mine[l] - 1, I[l], A2[l], L.lv[l], L.deg);
             }
         }
     }
@@ -672,6 +672,19 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
     }
 }
 
+// Extra jump numerator of every record of a LIF layer: dst = base + dlp
+// (either may be absent), for the stored records of each sample.
+__global__ void add_lp_kernel(double* dst, const double* base, const float* dlp, const int* cnt,
+                              int B, int cap) {
+    const int b = blockIdx.y;
+    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= B || r >= min(cnt[b], cap)) return;
+    const size_t k = (size_t)b * cap + r;
+    double v = base ? base[k] : 0.0;
+    if (dlp) v += (double)dlp[k];
+    dst[k] = v;
+}
+
 // Sample-block partial sums, added in block order.
 __global__ void grad_reduce_kernel(GradArgs a, int P) {
     const long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -761,6 +774,14 @@ hipError_t launch_gradients(const GradArgs& a, int J, int KL, int threads, size_
     SNN_GRAD(1, 8)
 #undef SNN_GRAD
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_add_lp(double* dst, const double* base, const float* dlp, const int* cnt, int B,
+                         int cap, hipStream_t s) {
+    if (B <= 0 || cap <= 0) return hipSuccess;
+    hipLaunchKernelGGL(add_lp_kernel, dim3(grid_for(cap, 256), B), dim3(256), 0, s, dst, base, dlp,
+                       cnt, B, cap);
+    return hipGetLastError();
 }
 
 hipError_t launch_grad_reduce(const GradArgs& a, int P, hipStream_t s) {

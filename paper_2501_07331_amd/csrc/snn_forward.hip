@@ -353,6 +353,70 @@ __global__ void loss_kernel(const float* z, const int* labels, int B, int C, int
     if (threadIdx.x == 0) loss_out[B] = (float)(part[0] / (double)B);
 }
 
+// Time-invariant MSE on first output spike times (SNN_LOSS_DMSE), one
+// workgroup per sample: the first record of each output neuron (records are
+// sorted by step, so the smallest index; an LDS atomic min is order-free),
+// z = first step x dt in ms (T dt if none), then in fp64 and in neuron order
+// L_b = 1/2 sum_{i != c} e_i^2, e_i = z_i - z_c - delta, and the jump terms
+// dL/dt of the batch mean, e_i / B at the first spike of i != c and
+// -sum_i e_i / B at that of c, written per record (0 elsewhere).
+__global__ void __launch_bounds__(256) dmse_loss_kernel(const int* rec_cnt, const int* rec_s,
+                                                        const int* rec_n, int cap, const int* labels,
+                                                        int B, int C, int T, float dt, float delta,
+                                                        float* z, float* loss_out, double* xlp,
+                                                        const DevStatus* st) {
+    __shared__ int first[1024];
+    if (st->bad_input) return;
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const int cnt = min(rec_cnt[b], cap);
+    const size_t base = (size_t)b * cap;
+    for (int k = tid; k < C; k += blockDim.x) first[k] = cap;
+    __syncthreads();
+    for (int r = tid; r < cnt; r += blockDim.x) {
+        atomicMin(&first[rec_n[base + r]], r);
+        xlp[base + r] = 0.0;
+    }
+    __syncthreads();
+    for (int k = tid; k < C; k += blockDim.x) {
+        const int n0 = (first[k] < cap) ? rec_s[base + first[k]] : T;
+        z[(size_t)b * C + k] = (float)((double)n0 * (double)dt);
+    }
+    __syncthreads();
+    if (tid != 0) return;
+    const int c = labels[b];
+    const float* zb = z + (size_t)b * C;
+    double L = 0.0, sc = 0.0;
+    for (int k = 0; k < C; ++k) {
+        if (k == c) continue;
+        const double e = (double)zb[k] - (double)zb[c] - (double)delta;
+        L += 0.5 * e * e;
+        sc += e;
+        if (first[k] < cap) xlp[base + first[k]] = e / (double)B;
+    }
+    if (first[c] < cap) xlp[base + first[c]] = -sc / (double)B;
+    loss_out[b] = (float)L;
+}
+
+// The batch mean of the per-sample losses, summed in sample order in fp64
+// from the fp64 values the per-sample kernel rounded to fp32 (one thread).
+__global__ void dmse_mean_kernel(const float* z, const int* labels, int B, int C, float delta,
+                                 float* loss_out, const DevStatus* st) {
+    if (st->bad_input || threadIdx.x != 0) return;
+    double tot = 0.0;
+    for (int b = 0; b < B; ++b) {
+        const int c = labels[b];
+        const float* zb = z + (size_t)b * C;
+        double L = 0.0;
+        for (int k = 0; k < C; ++k) {
+            if (k == c) continue;
+            const double e = (double)zb[k] - (double)zb[c] - (double)delta;
+            L += 0.5 * e * e;
+        }
+        tot += L;
+    }
+    loss_out[B] = (float)(tot / (double)B);
+}
+
 __global__ void copy_state_kernel(const float* src, int stride, int off, int n, int B, float* dst) {
     const long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (g >= (long long)B * n) return;
@@ -417,6 +481,18 @@ hipError_t launch_loss(const float* z, const int* labels, int B, int C, int loss
                        float tau_m, float* loss_out, float* src, const DevStatus* st, hipStream_t s) {
     hipLaunchKernelGGL(loss_kernel, dim3(1), dim3(256), 0, s, z, labels, B, C, loss, rscale, tau_m,
                        loss_out, src, st);
+    return hipGetLastError();
+}
+
+hipError_t launch_dmse_loss(const int* rec_cnt, const int* rec_s, const int* rec_n, int cap,
+                            const int* labels, int B, int C, int T, float dt, float delta, float* z,
+                            float* loss_out, double* xlp, const DevStatus* st, hipStream_t s) {
+    if (C > 1024 || cap < 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(dmse_loss_kernel, dim3(B), dim3(256), 0, s, rec_cnt, rec_s, rec_n, cap, labels,
+                       B, C, T, dt, delta, z, loss_out, xlp, st);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(dmse_mean_kernel, dim3(1), dim3(64), 0, s, z, labels, B, C, delta, loss_out, st);
     return hipGetLastError();
 }
 

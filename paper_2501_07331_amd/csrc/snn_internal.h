@@ -29,7 +29,8 @@ struct DevStatus {
 struct Topo {
     int L, P, B, T, S, cap, loss, n_in;
     int n_lif, lif_total, maxn;        // LIF layers, LIF neurons, widest non-input layer
-    int out_l;                         // the LI readout layer (L - 1)
+    int out_l;                         // the output layer (L - 1): LI readout, or LIF (spike-time loss)
+    int out_lif;                       // 1: the output layer is LIF (SNN_LOSS_DMSE)
     int out_p;                         // the projection into the readout layer
     float alpha, beta, gamma, cc, theta, rscale, tau_s, dt;
     int n[SNN_MAX_LAYERS];
@@ -157,7 +158,8 @@ struct BwdLayer {
     const float* recI;                 // [B][cap] I- of the records
     const int* recn;                   // [B][cap] neuron of the records
     const int* steptab;                // [B][T][SNN_STEP_ROW] per-step spike table
-    int use_a2;                        // 1: the layer feeds the readout (jump sums get A2)
+    const double* A2;                  // [B][cap] extra jump numerator per record (the readout
+                                       // part of the jump sums, spike-time loss terms), or NULL
 };
 
 struct CoreBwdArgs {
@@ -166,7 +168,6 @@ struct CoreBwdArgs {
     BwdLayer ly[SNN_MAX_LIF];
     float* tu;                         // [B][T][lif_total] lambda_I
     float* td;                         // [B][T][lif_total] lambda_I - lambda_V
-    const double* A2;                  // [B][cap] readout part of the jump sums (feeding layer)
     DevStatus* st;
     int part_off;                      // LDS byte offset of the partial jump sums
 };
@@ -258,6 +259,11 @@ hipError_t launch_group(const GroupArgs& a, int B, hipStream_t s);
 hipError_t launch_gradients(const GradArgs& a, int J, int KL, int threads, size_t lds, hipStream_t s);
 hipError_t launch_grad_reduce(const GradArgs& a, int P, hipStream_t s);
 hipError_t launch_optimizer(const OptArgs& a, hipStream_t s);
+hipError_t launch_dmse_loss(const int* rec_cnt, const int* rec_s, const int* rec_n, int cap,
+                            const int* labels, int B, int C, int T, float dt, float delta, float* z,
+                            float* loss_out, double* xlp, const DevStatus* st, hipStream_t s);
+hipError_t launch_add_lp(double* dst, const double* base, const float* dlp, const int* cnt, int B,
+                         int cap, hipStream_t s);
 hipError_t set_forward_lds_limits(size_t bytes, int* bad);
 hipError_t set_core_lds_limits(size_t bytes, int* bad);
 bool launch_forward_core_256(const CoreFwdArgs& a, int n_lif, int np, bool rl, int threads,

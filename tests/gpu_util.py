@@ -21,15 +21,23 @@ def oracle_net(wl: Workload, max_delay=None):
                             c.readout_scale)
 
 
-def run_oracle(wl: Workload, cap=None, modes=("f64", "f32"), max_delay=None):
+def run_oracle(wl: Workload, cap=None, modes=("f64", "f32"), max_delay=None, dlp=None):
+    """dlp: extra per-record dl_p/dt_k [n_lif][B][cap] (fp64) or None."""
     cap = default_cap(wl) if cap is None else cap
     net = oracle_net(wl, max_delay)
     f = oracle.forward(net, wl.in_off, wl.in_step, wl.in_neuron, wl.W, wl.D, cap=cap)
-    lo, g = oracle.loss(f.z, wl.labels)
+    if wl.cfg.loss == oracle.LOSS_DMSE:
+        lo, dl = oracle.loss_dmse(f.z, wl.labels, wl.cfg.dmse_delta)
+        g = np.zeros_like(f.z)
+        x = oracle.first_spike_dlp(net, f, dl)
+        x = x if dlp is None else x + dlp
+    else:
+        lo, g = oracle.loss(f.z, wl.labels)
+        x = dlp
     out = {"fwd": f, "loss": lo, "g": g}
     for m in modes:
         dW, dD, deg = oracle.backward(net, wl.in_off, wl.in_step, wl.in_neuron, wl.W, wl.D, f, g,
-                                      mode=m)
+                                      mode=m, dlp=x)
         out[m] = (dW, dD, deg)
     return out
 
@@ -40,7 +48,7 @@ def make_gpu_net(wl: Workload, cap=None, flags=0, max_delay=None):
     cap = default_cap(wl) if cap is None else cap
     return snn.Network(c.layers, c.tau_m, c.tau_s, c.theta, c.dt,
                        c.max_delay if max_delay is None else max_delay, wl.B, wl.T, c.loss,
-                       c.readout_scale, cap, flags)
+                       c.readout_scale, cap, flags, dmse_delta=c.dmse_delta)
 
 
 def to_device(wl: Workload):
@@ -55,8 +63,10 @@ def to_device(wl: Workload):
     }
 
 
-def run_gpu(wl: Workload, net=None, cap=None, flags=0, backward=True, max_delay=None, dev_in=None):
-    """Forward (+ backward) through the library; returns numpy results."""
+def run_gpu(wl: Workload, net=None, cap=None, flags=0, backward=True, max_delay=None, dev_in=None,
+            dlp=None):
+    """Forward (+ backward) through the library; returns numpy results.
+    dlp: per LIF layer None or an fp32 [B][cap] array of dl_p/dt_k."""
     import torch
     import paper_2501_07331_amd as snn
     net = make_gpu_net(wl, cap, flags, max_delay) if net is None else net
@@ -94,7 +104,12 @@ def run_gpu(wl: Workload, net=None, cap=None, flags=0, backward=True, max_delay=
     if backward and out["rc"] == 0:
         dW = [torch.full_like(w, np.nan) for w in d["W"]]
         dD = [torch.full_like(w, np.nan) for w in d["W"]]
-        net.backward(dW, dD)
+        if dlp is None:
+            net.backward(dW, dD)
+        else:
+            net.backward(dW, dD, [None if x is None else
+                                  torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(dev)
+                                  for x in dlp])
         torch.cuda.synchronize()
         out["dW"] = [x.cpu().numpy() for x in dW]
         out["dD"] = [x.cpu().numpy() for x in dD]

@@ -5,11 +5,13 @@ labels with the shapes and statistics of the paper's benchmark tasks.  It holds
 none of the method's arithmetic (no neuron dynamics, no loss, no gradients) and
 imports neither the HIP library nor the oracle.
 """
-from .configs import CONFIGS, INPUT, LIF, LI, LOSS_CE_SUM, LOSS_CE_MAX, projections, Config
+from .configs import (CONFIGS, INPUT, LIF, LI, LOSS_CE_SUM, LOSS_CE_MAX, LOSS_DMSE, projections,
+                      Config)
 from .generators import (Workload, make_workload, make_variant, input_spikes,
                          weights_and_delays, labels)
 
 __all__ = [
-    "CONFIGS", "INPUT", "LIF", "LI", "LOSS_CE_SUM", "LOSS_CE_MAX", "projections", "Config",
+    "CONFIGS", "INPUT", "LIF", "LI", "LOSS_CE_SUM", "LOSS_CE_MAX", "LOSS_DMSE", "projections",
+    "Config",
     "Workload", "make_workload", "make_variant", "input_spikes", "weights_and_delays", "labels",
 ]

@@ -27,7 +27,7 @@ from dataclasses import dataclass, field
 from typing import Dict, List, Tuple
 
 INPUT, LIF, LI = 0, 1, 2
-LOSS_CE_SUM, LOSS_CE_MAX = 0, 1
+LOSS_CE_SUM, LOSS_CE_MAX, LOSS_DMSE = 0, 1, 2
 
 
 @dataclass(frozen=True)
@@ -48,6 +48,7 @@ class Config:
     target_rate: float = 0.0                       # spikes / hidden neuron / sample for mu calibration
     w_init: Tuple[Tuple[float, float], ...] = ()   # (mean, std) per projection; std 0 -> 1/sqrt(fan_in)
     calibrate: Tuple[int, ...] = ()                # projections whose mean is calibrated
+    dmse_delta: float = 0.0                        # Delta_t (ms) of the spike-time loss
 
     @property
     def max_delay(self) -> int:

@@ -141,10 +141,13 @@ def make_workload(cid: int, B: Optional[int] = None, T: Optional[int] = None,
 
 def make_variant(cid: int, B: Optional[int] = None, T: Optional[int] = None,
                  dt: Optional[float] = None, delay_range: Optional[Sequence[int]] = None,
-                 name: Optional[str] = None) -> Workload:
-    """Config `cid` with another grid (dt, T) or other delay ranges (in steps),
-    drawn from the same seeds and weight means; the input generator keeps its
-    rates and times in ms, so a finer dt resolves the same spike trains."""
+                 name: Optional[str] = None, layers=None, loss: Optional[int] = None,
+                 dmse_delta: Optional[float] = None) -> Workload:
+    """Config `cid` with another grid (dt, T), other delay ranges (in steps),
+    or another output layer and loss (same layer sizes: a LIF output layer
+    with the spike-time loss), drawn from the same seeds and weight means;
+    the input generator keeps its rates and times in ms, so a finer dt
+    resolves the same spike trains."""
     import dataclasses
     base = CONFIGS[cid]
     kw = {}
@@ -156,6 +159,14 @@ def make_variant(cid: int, B: Optional[int] = None, T: Optional[int] = None,
         if len(delay_range) != len(base.delay_range):
             raise ValueError("one delay range per projection")
         kw["delay_range"] = tuple(int(x) for x in delay_range)
+    if layers is not None:
+        if [l[0] for l in layers] != [l[0] for l in base.layers]:
+            raise ValueError("a variant keeps the layer sizes")
+        kw["layers"] = tuple(tuple(int(x) for x in l) for l in layers)
+    if loss is not None:
+        kw["loss"] = int(loss)
+    if dmse_delta is not None:
+        kw["dmse_delta"] = float(dmse_delta)
     cfg = dataclasses.replace(base, name=name or base.name, **kw)
     B = cfg.B if B is None else B
     off, st, ne = input_spikes(cfg, B, T=cfg.T)
