@@ -624,9 +624,15 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
             __syncthreads();
 #pragma unroll
             for (int k = 0; k < KL; ++k) {
-                if (dsc[k] < 0) continue;
-                const int pi = (dsc[k] >> 20) & 1, sl = (dsc[k] >> 21) & 0xFF;
-                const float2* stk = st + ((dsc[k] >> 16) & 0xF) * T;
+                // the descriptor is made opaque here, so that what derives
+                // from it is recomputed per sample instead of being hoisted
+                // out of the sample loop (KL sets of it do not fit in
+                // registers beside the sums: the spills cost HBM writes)
+                int dk = dsc[k];
+                asm volatile("" : "+v"(dk));
+                if (dk < 0) continue;
+                const int pi = (dk >> 20) & 1, sl = (dk >> 21) & 0xFF;
+                const float2* stk = st + ((dk >> 16) & 0xF) * T;
                 const int* gs = pi ? gs1 : gs0;
                 const int off = pi ? c0 - s1 : -s0;                 // LDS index = x + off
                 float pu = 0.0f, pd = 0.0f;
