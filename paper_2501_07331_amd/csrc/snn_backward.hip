@@ -159,10 +159,12 @@ struct BwdCore {
                                                      uint2 (&ws)[NPA][KP], int& mine, float& I,
                                                      double& A2) {
         const BwdLayer& y = a.ly[l];
+        // (the ids stay in vector registers: held in scalar ones, the 16 ids
+        // and their row offsets overflow the scalar register file)
         int idc[KP];
 #pragma unroll
         for (int q = 0; q < KP; ++q)
-            idc[q] = (q < cnt) ? min(max(__builtin_amdgcn_readfirstlane(ids[q]), 0), y.n - 1) : 0;
+            idc[q] = (q < cnt) ? min(max(ids[q], 0), y.n - 1) : 0;
         mine = 0;
 #pragma unroll
         for (int q0 = 0; q0 < KP; q0 += 4) {
@@ -177,7 +179,7 @@ struct BwdCore {
                 const int col8 = min(tid, nq - 1) * 8;
 #pragma unroll
                 for (int q = q0; q < q0 + 4; ++q) {
-                    const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, col8, idc[q] * nq * 8, 0);
+                    const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, col8 + idc[q] * nq * 8, 0, 0);
                     ws[pp][q] = make_uint2((unsigned)v[0], (unsigned)v[1]);
                 }
             }
