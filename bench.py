@@ -128,6 +128,9 @@ def sweep(args):
     if args.sweep == "losses":
         losses_bench(args)
         return
+    if args.sweep == "configs":
+        configs_bench(args)
+        return
     if args.sweep == "delay":
         pts = [int(x) for x in args.points.split(",")] if args.points else [0, 25, 50, 100, 150, 200, 255]
         cases = [dict(delay_range=(m, min(m, 50), m)) for m in pts]
@@ -209,6 +212,53 @@ def _time_steps(net, fwd_args, dW, dD, steps, warmup, dlp=None):
     return (time.perf_counter() - t0) / steps, {k: round(float(np.mean(v)), 4) for k, v in kt.items()}
 
 
+def configs_bench(args):
+    """Each of the five configurations at its stated batch and grid: step
+    time, events per second and the step's algorithmic bytes against the HBM
+    peak (the same per-unit figures as the main line)."""
+    import torch
+    import paper_2501_07331_amd as snn
+    from workloads import CONFIGS, make_workload
+    dev = torch.device("cuda")
+    pts = [int(x) for x in args.points.split(",")] if args.points else sorted(CONFIGS)
+    for cid in pts:
+        wl = make_workload(cid)
+        c = wl.cfg
+        lif = [l[0] for l in c.layers if l[1] == snn.SNN_LIF]
+        cap = 64 * max(lif)
+        stream = torch.cuda.Stream()
+        with torch.cuda.stream(stream):
+            t = lambda a, dt_: torch.from_numpy(np.ascontiguousarray(a)).to(dev, dt_)
+            off, st, ne = t(wl.in_off, torch.int32), t(wl.in_step, torch.int32), t(wl.in_neuron, torch.int32)
+            W = [t(w, torch.float32) for w in wl.W]
+            D = [t(d, torch.float32) for d in wl.D]
+            labels = t(wl.labels, torch.int32)
+            recs = [(torch.zeros(wl.B, dtype=torch.int32, device=dev),
+                     torch.zeros(wl.B, cap, dtype=torch.int32, device=dev),
+                     torch.zeros(wl.B, cap, dtype=torch.int32, device=dev)) for _ in lif]
+            loss = torch.zeros(wl.B + 1, device=dev)
+            dW = [torch.zeros_like(w) for w in W]
+            dD = [torch.zeros_like(w) for w in W]
+            net = snn.Network(c.layers, c.tau_m, c.tau_s, c.theta, c.dt, c.max_delay, wl.B, wl.T,
+                              c.loss, c.readout_scale, cap, flags=snn.SNN_FLAG_TIMING, stream=stream)
+            el, kt = _time_steps(net, (off, st, ne, W, D, labels, recs, loss), dW, dD, args.steps,
+                                 args.warmup)
+            s = net.stats()
+            spikes = [int(r[0].sum().item()) for r in recs]
+            net.close()
+        # units of work: events per projection from the measured spike counts
+        E = s["events"]
+        NS = wl.B * wl.T * sum(l[0] for l in c.layers[1:])
+        byt = 34 * E + 16 * NS + 16 * sum(spikes) + 8 * s["input_spikes"]
+        print(json.dumps({"sweep": "configs", "config": cid, "workload": c.name, "B": wl.B, "T": wl.T,
+                          "ms_per_step": round(1e3 * el, 4), "events": E, "events_per_s": E / el,
+                          "step_alg_bytes": byt, "step_hbm_frac": round(byt / el / 1e9 / HBM_PEAK_GBS, 4),
+                          "lif_spikes_per_neuron": [round(x / wl.B / n, 2) for x, n in zip(spikes, lif)],
+                          "kernel_ms": kt}), flush=True)
+        del net, W, D, dW, dD, recs
+        torch.cuda.empty_cache()
+
+
 def losses_bench(args):
     """Steps with spike-time loss terms: the time-invariant MSE on the first
     spikes of a LIF output layer (the latency-coded 4-200-3 network, B = 256,
@@ -265,10 +315,11 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (the reference "
                          "kernel the HBM byte counters are scaled by) and exit")
-    ap.add_argument("--sweep", choices=("delay", "dt", "losses"), default=None,
+    ap.add_argument("--sweep", choices=("delay", "dt", "losses", "configs"), default=None,
                     help="instead of the single line: time the 700-256rec-20 step over a range "
-                         "of maximum delays (dt 1 ms) or of time steps (the same 1 s trials), or "
-                         "the steps with spike-time loss terms; one JSON line per point")
+                         "of maximum delays (dt 1 ms) or of time steps (the same 1 s trials), "
+                         "the steps with spike-time loss terms, or every configuration at its "
+                         "stated size; one JSON line per point")
     ap.add_argument("--points", type=str, default=None,
                     help="comma-separated sweep points (max delays in steps, or dt in ms)")
     args = ap.parse_args()
