@@ -341,12 +341,23 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     // gradients: one group per post layer (its projections in projection
     // order), J posts per workgroup, samples split into SB blocks so that the
     // grid has about 512 workgroups; workgroups in units of 4 J-blocks.  LDS:
-    // the J trajectories of a sample [J][T] float2 (J = 8, 4 or 1: the
-    // largest within 64 KiB), then room for the sample's spike steps (16-bit)
-    // up to 96 KiB in all, when that leaves any
+    // the J trajectories of a sample [J][T] float2 (J = 8 within 64 KiB, then
+    // room for the sample's spike steps (16-bit) up to 96 KiB in all; for
+    // longer trials J = 4, 2 or 1, the largest within 128 KiB, and the rest
+    // of the LDS for the spike steps, when that leaves any)
+    size_t grad_total = 96 * 1024;
     {
         const size_t tj = (size_t)t.T * 2 * sizeof(float);
-        net->grad_J = (8 * tj <= 64 * 1024) ? 8 : (4 * tj <= 64 * 1024) ? 4 : 1;
+        auto pick = [&](size_t cap) {
+            for (int j : {8, 4, 2})
+                if (j * tj <= cap) return j;
+            return 1;
+        };
+        net->grad_J = pick(64 * 1024);
+        if (net->grad_J < 8) {
+            net->grad_J = pick(128 * 1024);
+            grad_total = kLds;
+        }
         const int J = net->grad_J;
         int ng = 0, jblocks = 0, maxpre = 64;
         for (int q = 1; q < n_layers; ++q) {
@@ -386,7 +397,7 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         net->grad_KL = (pairs <= 4 * 1024) ? 4 : 8;
         net->grad_threads = std::min(1024, ((pairs + net->grad_KL - 1) / net->grad_KL + 63) / 64 * 64);
         const size_t traj = (size_t)J * t.T * 2 * sizeof(float);
-        const size_t room = (traj < 96 * 1024) ? 96 * 1024 - traj : 0;
+        const size_t room = (traj < grad_total) ? grad_total - traj : 0;
         net->grad_spcap = (int)(room / sizeof(unsigned short)) & ~7;
         net->lds_grad = traj + (size_t)net->grad_spcap * sizeof(unsigned short);
     }

@@ -778,6 +778,8 @@ hipError_t launch_gradients(const GradArgs& a, int J, int KL, int threads, size_
     SNN_GRAD(8, 8)
     SNN_GRAD(4, 4)
     SNN_GRAD(4, 8)
+    SNN_GRAD(2, 4)
+    SNN_GRAD(2, 8)
     SNN_GRAD(1, 4)
     SNN_GRAD(1, 8)
 #undef SNN_GRAD
@@ -808,7 +810,8 @@ hipError_t set_backward_lds_limits(size_t bytes, int* bad) {
     const void* fns[] = {(const void*)readout_adjoint_kernel, CORE_FNS(256), CORE_FNS(1024),
                          (const void*)group_kernel, (const void*)gradients_kernel<8, 4>,
                          (const void*)gradients_kernel<8, 8>, (const void*)gradients_kernel<4, 4>,
-                         (const void*)gradients_kernel<4, 8>, (const void*)gradients_kernel<1, 4>,
+                         (const void*)gradients_kernel<4, 8>, (const void*)gradients_kernel<2, 4>,
+                         (const void*)gradients_kernel<2, 8>, (const void*)gradients_kernel<1, 4>,
                          (const void*)gradients_kernel<1, 8>};
     for (int i = 0; i < (int)(sizeof(fns) / sizeof(fns[0])); ++i) {
         const hipError_t e =
