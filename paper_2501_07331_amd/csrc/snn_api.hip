@@ -31,7 +31,7 @@ struct snn_net {
     int bpart_off;              // backward-core LDS plan
     int bring_mode[SNN_MAX_LAYERS];   // adjoint ring of a LIF layer: -2 none, -1 HBM, >= 0 LDS
     int radj_threads, radj_tab;
-    int grad_J, grad_KL, grad_threads, grad_SB, grad_bs, grad_nblk, grad_ngroups, grad_spcap;
+    int grad_J, grad_TW, grad_KL, grad_threads, grad_SB, grad_bs, grad_nblk, grad_ngroups, grad_spcap;
     GradGroup grad_grp[SNN_MAX_LAYERS];
     hipStream_t stream;
     hipStream_t aux;                   // second stream: spike grouping beside the backward sweep
@@ -343,8 +343,8 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     // grid has about 512 workgroups; workgroups in units of 4 J-blocks.  LDS:
     // the J trajectories of a sample [J][T] float2 (J = 8 within 64 KiB, then
     // room for the sample's spike steps (16-bit) up to 96 KiB in all; for
-    // longer trials J = 4, 2 or 1, the largest within 128 KiB, and the rest
-    // of the LDS for the spike steps, when that leaves any)
+    // longer trials J = 4 within 128 KiB and the rest of the LDS for the spike
+    // steps; longer still, J = 8 and windows of 1024 steps)
     size_t grad_total = 96 * 1024;
     {
         const size_t tj = (size_t)t.T * 2 * sizeof(float);
@@ -354,9 +354,15 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
             return 1;
         };
         net->grad_J = pick(64 * 1024);
+        net->grad_TW = t.T;
         if (net->grad_J < 8) {
             net->grad_J = pick(128 * 1024);
             grad_total = kLds;
+            if (net->grad_J < 4) {
+                net->grad_J = 8;
+                net->grad_TW = 1024;
+                grad_total = 96 * 1024;
+            }
         }
         const int J = net->grad_J;
         int ng = 0, jblocks = 0, maxpre = 64;
@@ -396,7 +402,7 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         const int pairs = J * maxpre;
         net->grad_KL = (pairs <= 4 * 1024) ? 4 : 8;
         net->grad_threads = std::min(1024, ((pairs + net->grad_KL - 1) / net->grad_KL + 63) / 64 * 64);
-        const size_t traj = (size_t)J * t.T * 2 * sizeof(float);
+        const size_t traj = (size_t)J * net->grad_TW * 2 * sizeof(float);
         const size_t room = (traj < grad_total) ? grad_total - traj : 0;
         net->grad_spcap = (int)(room / sizeof(unsigned short)) & ~7;
         net->lds_grad = traj + (size_t)net->grad_spcap * sizeof(unsigned short);
@@ -880,6 +886,7 @@ extern "C" int snn_backward_lp(snn_net* net, const float* const* dlp, float* con
     GradArgs ga{};
     ga.B = t.B;
     ga.T = t.T;
+    ga.TW = net->grad_TW;
     ga.SB = net->grad_SB;
     ga.spcap = net->grad_spcap;
     ga.bs = net->grad_bs;

@@ -519,7 +519,7 @@ __global__ void __launch_bounds__(1024) group_kernel(GroupArgs a) {
 // Workgroups come in units of four J-post blocks that share lines of the
 // [B][T][N] trajectories; a unit's four blocks have indices 8 apart, so with
 // round-robin dispatch over the 8 XCDs they run on one XCD and share its L2.
-template <int J, int KL>
+template <int J, int KL, bool WIN>
 __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
     const int tid = threadIdx.x, nt = blockDim.x;
     int g = 0;
@@ -533,8 +533,9 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
     if (jb >= G.jb) return;
     const int nq = G.nq, j0 = jb * J, nj = min(J, nq - j0);
     const int T = a.T;
-    float2* st = reinterpret_cast<float2*>(smem);              // [J][T]
-    unsigned short* sp = reinterpret_cast<unsigned short*>(smem + (size_t)J * T * sizeof(float2));
+    const int TW = WIN ? a.TW : a.T;                            // steps per trajectory window
+    float2* st = reinterpret_cast<float2*>(smem);              // [J][TW]
+    unsigned short* sp = reinterpret_cast<unsigned short*>(smem + (size_t)J * TW * sizeof(float2));
     const float* tu = G.out ? a.tu_out : a.tu_lif;
     const float* td = G.out ? a.td_out : a.td_lif;
     const int LN = G.out ? a.C : a.lif_total;
@@ -603,64 +604,79 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
                         if (x0 + u * nt < c0 + c1) sp[x0 + u * nt] = (unsigned short)v[u];
                 }
             }
-            // the J post trajectories of the sample
+            // the J post trajectories of the sample, in windows of TW steps
+            // (one window unless the trial is long); a synapse's spikes are
+            // taken in step order, window by window, from a cursor
             const size_t base = (size_t)b * T * LN + G.off + j0;
-            for (int e0 = tid; e0 < T * J; e0 += U * nt) {
-                float2 x[U];
+            for (int w0 = 0; w0 < T; w0 += TW) {
+                const int W = min(TW, T - w0), wend = w0 + W;
+                if (w0 > 0) __syncthreads();                        // the last window's reads are done
+                for (int e0 = tid; e0 < W * J; e0 += U * nt) {
+                    float2 x[U];
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const int e = min(e0 + u * nt, T * J - 1);
-                    const int m = e / J, q = e % J;
-                    const int qc = min(q, nj - 1);
-                    x[u] = make_float2(tu[base + (size_t)m * LN + qc], td[base + (size_t)m * LN + qc]);
-                }
-#pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const int e = e0 + u * nt;
-                    if (e < T * J) {
-                        const int m = e / J, q = e % J;
-                        st[q * T + m] = (q < nj) ? x[u] : make_float2(0.0f, 0.0f);
+                    for (int u = 0; u < U; ++u) {
+                        const int e = min(e0 + u * nt, W * J - 1);
+                        const int m = w0 + e / J, q = e % J;
+                        const int qc = min(q, nj - 1);
+                        x[u] = make_float2(tu[base + (size_t)m * LN + qc], td[base + (size_t)m * LN + qc]);
                     }
-                }
-            }
-            __syncthreads();
 #pragma unroll
-            for (int k = 0; k < KL; ++k) {
-                // the descriptor is made opaque here, so that what derives
-                // from it is recomputed per sample instead of being hoisted
-                // out of the sample loop (KL sets of it do not fit in
-                // registers beside the sums: the spills cost HBM writes)
-                int dk = dsc[k];
-                asm volatile("" : "+v"(dk));
-                if (dk < 0) continue;
-                const int pi = (dk >> 20) & 1, sl = (dk >> 21) & 0xFF;
-                const float2* stk = st + ((dk >> 16) & 0xF) * T;
-                const int* gs = pi ? gs1 : gs0;
-                const int off = pi ? c0 - s1 : -s0;                 // LDS index = x + off
-                float pu = 0.0f, pd = 0.0f;
-                // four spikes at a time: their reads issued together, their
-                // terms added in spike order
-                for (int x = lo[k]; x < hi[k]; x += 4) {
-                    int m[4];
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        const int xc = min(x + u, hi[k] - 1);
-                        const int t = in_lds ? (int)sp[xc + off] : gs[xc];
-                        m[u] = (x + u < hi[k]) ? t + sl : T;             // T: no arrival
-                    }
-                    float2 ud[4];
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) ud[u] = stk[(m[u] <= T - 1) ? m[u] : 0];
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        if (m[u] <= T - 1) {
-                            pu = __fadd_rn(pu, ud[u].x);
-                            pd = __fadd_rn(pd, __fmul_rn(w[k], ud[u].y));
+                    for (int u = 0; u < U; ++u) {
+                        const int e = e0 + u * nt;
+                        if (e < W * J) {
+                            const int mw = e / J, q = e % J;
+                            st[q * TW + mw] = (q < nj) ? x[u] : make_float2(0.0f, 0.0f);
                         }
                     }
                 }
-                su[k] += (double)pu;
-                sd[k] += (double)pd;
+                __syncthreads();
+#pragma unroll
+                for (int k = 0; k < KL; ++k) {
+                    // the descriptor is made opaque here, so that what derives
+                    // from it is recomputed per sample instead of being hoisted
+                    // out of the sample loop (KL sets of it do not fit in
+                    // registers beside the sums: the spills cost HBM writes)
+                    int dk = dsc[k];
+                    asm volatile("" : "+v"(dk));
+                    if (dk < 0) continue;
+                    const int pi = (dk >> 20) & 1, sl = (dk >> 21) & 0xFF;
+                    const float2* stk = st + ((dk >> 16) & 0xF) * TW - w0;   // index: arrival step
+                    const int* gs = pi ? gs1 : gs0;
+                    const int off = pi ? c0 - s1 : -s0;             // LDS index = x + off
+                    float pu = 0.0f, pd = 0.0f;
+                    // four spikes at a time: their reads issued together, their
+                    // terms added in spike order; the arrivals ascend, so the
+                    // window's spikes are a prefix from the cursor
+                    int x = lo[k];
+                    for (; x < hi[k]; x += 4) {
+                        int m[4];
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) {
+                            const int xc = min(x + u, hi[k] - 1);
+                            const int t = in_lds ? (int)sp[xc + off] : gs[xc];
+                            m[u] = (x + u < hi[k]) ? t + sl : T;     // T: no arrival
+                        }
+                        float2 ud[4];
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) ud[u] = stk[(m[u] < wend) ? m[u] : w0];
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) {
+                            if (m[u] < wend) {
+                                pu = __fadd_rn(pu, ud[u].x);
+                                pd = __fadd_rn(pd, __fmul_rn(w[k], ud[u].y));
+                            }
+                        }
+                        if constexpr (WIN) {
+                            if (m[3] >= wend) {
+                                x += (m[0] < wend) + (m[1] < wend) + (m[2] < wend);
+                                break;
+                            }
+                        }
+                    }
+                    if constexpr (WIN) lo[k] = min(x, hi[k]);
+                    su[k] += (double)pu;
+                    sd[k] += (double)pd;
+                }
             }
         }
 #pragma unroll
@@ -769,19 +785,22 @@ hipError_t launch_group(const GroupArgs& a, int B, hipStream_t s) {
 }
 
 hipError_t launch_gradients(const GradArgs& a, int J, int KL, int threads, size_t lds, hipStream_t s) {
-#define SNN_GRAD(JJ, KK)                                                                         \
-    if (J == JJ && KL == KK) {                                                                   \
-        hipLaunchKernelGGL((gradients_kernel<JJ, KK>), dim3(a.nblk), dim3(threads), lds, s, a); \
-        return hipGetLastError();                                                                \
+    const bool win = a.TW < a.T;
+#define SNN_GRAD(JJ, KK, WW)                                                                         \
+    if (J == JJ && KL == KK && win == WW) {                                                          \
+        hipLaunchKernelGGL((gradients_kernel<JJ, KK, WW>), dim3(a.nblk), dim3(threads), lds, s, a); \
+        return hipGetLastError();                                                                    \
     }
-    SNN_GRAD(8, 4)
-    SNN_GRAD(8, 8)
-    SNN_GRAD(4, 4)
-    SNN_GRAD(4, 8)
-    SNN_GRAD(2, 4)
-    SNN_GRAD(2, 8)
-    SNN_GRAD(1, 4)
-    SNN_GRAD(1, 8)
+    SNN_GRAD(8, 4, false)
+    SNN_GRAD(8, 8, false)
+    SNN_GRAD(4, 4, false)
+    SNN_GRAD(4, 8, false)
+    SNN_GRAD(2, 4, false)
+    SNN_GRAD(2, 8, false)
+    SNN_GRAD(1, 4, false)
+    SNN_GRAD(1, 8, false)
+    SNN_GRAD(8, 4, true)
+    SNN_GRAD(8, 8, true)
 #undef SNN_GRAD
     return hipErrorInvalidValue;
 }
@@ -808,11 +827,12 @@ hipError_t launch_grad_reduce(const GradArgs& a, int P, hipStream_t s) {
 
 hipError_t set_backward_lds_limits(size_t bytes, int* bad) {
     const void* fns[] = {(const void*)readout_adjoint_kernel, CORE_FNS(256), CORE_FNS(1024),
-                         (const void*)group_kernel, (const void*)gradients_kernel<8, 4>,
-                         (const void*)gradients_kernel<8, 8>, (const void*)gradients_kernel<4, 4>,
-                         (const void*)gradients_kernel<4, 8>, (const void*)gradients_kernel<2, 4>,
-                         (const void*)gradients_kernel<2, 8>, (const void*)gradients_kernel<1, 4>,
-                         (const void*)gradients_kernel<1, 8>};
+                         (const void*)group_kernel, (const void*)gradients_kernel<8, 4, false>,
+                         (const void*)gradients_kernel<8, 8, false>, (const void*)gradients_kernel<4, 4, false>,
+                         (const void*)gradients_kernel<4, 8, false>, (const void*)gradients_kernel<2, 4, false>,
+                         (const void*)gradients_kernel<2, 8, false>, (const void*)gradients_kernel<1, 4, false>,
+                         (const void*)gradients_kernel<1, 8, false>, (const void*)gradients_kernel<8, 4, true>,
+                         (const void*)gradients_kernel<8, 8, true>};
     for (int i = 0; i < (int)(sizeof(fns) / sizeof(fns[0])); ++i) {
         const hipError_t e =
             hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);

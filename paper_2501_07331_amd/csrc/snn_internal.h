@@ -202,6 +202,7 @@ struct GradGroup {
 
 struct GradArgs {
     int B, T, SB, bs, lif_total, C, ngroups, nblk;
+    int TW;                            // trajectory window: steps staged in LDS at a time
     int spcap;                         // LDS capacity for a sample's spike steps (16-bit), 0: none
     float tau_s, dt;
     long long nparams;
