@@ -37,6 +37,10 @@ struct FwdCore {
     static constexpr int NWM = MAXT / 64;
     static constexpr int KP = (NL == 1) ? 8 : 4;     // spikes per step with prefetched weights
     static constexpr int KS = 4;                      // spikes per column_add_all of the deferred scatter
+    // spikes per chunk of the immediate scatter: with rings in device memory
+    // every chunk costs serialized round trips (weights, cells, stores), so
+    // the chunks are larger there
+    static constexpr int KI = RL ? KB : 16;
     static constexpr int NPA = NP > 0 ? NP : 1;
     // the deferred scatter's register lists fit without spills for one LIF
     // layer, or two with one LIF-post projection each, at 256 threads (and it
@@ -130,15 +134,15 @@ struct FwdCore {
                                         const unsigned long long* row, int from, int total,
                                         int smin) {
         const FwdLayer& y = a.ly[l];
-        for (int q0 = from; q0 < total; q0 += KB) {
-            int ids[KB];
-            word_ids<NWM, KB>(m, row, a.NW, q0, ids);
+        for (int q0 = from; q0 < total; q0 += KI) {
+            int ids[KI];
+            word_ids<NWM, KI>(m, row, a.NW, q0, ids);
 #pragma unroll
             for (int pp = 0; pp < NP; ++pp) {
                 if (pp >= y.npost) continue;
-                uint2 w[KB];
-                load_ws<KB>(a, l, pp, tid, ids, w);
-                scatter<KB, KB>(a, b, l, pp, tid, e, total - q0, smin, w);
+                uint2 w[KI];
+                load_ws<KI>(a, l, pp, tid, ids, w);
+                scatter<KI, KI>(a, b, l, pp, tid, e, total - q0, smin, w);
             }
         }
     }
