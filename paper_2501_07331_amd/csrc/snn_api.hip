@@ -27,7 +27,7 @@ struct snn_net {
     int core_threads;           // LIF-core workgroup size
     int read_threads;           // readout workgroup size
     size_t lds_core_f, lds_core_b, lds_scan, lds_read, lds_grad, lds_radj;
-    int mask_off, zw_off, scan_tb, table_lds;
+    int mask_off, scan_tb, table_lds;
     int bpart_off;              // backward-core LDS plan
     int bring_mode[SNN_MAX_LAYERS];   // adjoint ring of a LIF layer: -2 none, -1 HBM, >= 0 LDS
     int radj_threads, radj_tab;
@@ -264,23 +264,6 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         }
         net->mask_off = (int)align16(used);
         net->lds_core_f = net->mask_off + masks;
-        // zero-delay weights [NL][NP][SNN_ZMAX][threads] for the deferred
-        // scatter (rings in LDS only)
-        int np = 0;
-        for (int l = 1; l < n_layers; ++l) {
-            if (t.kind[l] != SNN_LIF) continue;
-            int k = 0;
-            for (int p = 0; p < t.P; ++p)
-                if (t.pre[p] == l && t.kind[t.post[p]] == SNN_LIF) ++k;
-            np = std::max(np, k);
-        }
-        const size_t zw = (size_t)std::max(t.n_lif, 1) * std::max(np, 1) * SNN_ZMAX *
-                          net->core_threads * sizeof(float);
-        net->zw_off = -1;
-        if (rings_lds && np > 0 && net->lds_core_f + zw <= kLds) {
-            net->zw_off = (int)net->lds_core_f;
-            net->lds_core_f += zw;
-        }
     }
     // backward core: partial jump sums [2][NL][KP][4 NW] and the adjoint
     // rings of the LIF layers read by LIF-pre projections (all in LDS, or all
@@ -643,7 +626,6 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
         a.If = net->If;
         a.st = net->st;
         a.mask_off = net->mask_off;
-        a.zw_off = net->zw_off;
         TIMED(net, K_CORE, launch_forward_core(a, t.n_lif, net->core_threads, net->lds_core_f, s));
     }
     if (t.out_lif) {

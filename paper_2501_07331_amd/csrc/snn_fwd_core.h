@@ -10,18 +10,12 @@
 // by projection in projection order).  A ring cell sums its weights in emission
 // order (step, then presynaptic neuron).
 //
-// Deferred scatter (rings in LDS, few zero-delay synapses): the weights and
-// slots of step n's spikes are loaded during step n and scattered at step
-// n + 1, so their load latency is hidden behind a whole step.  Arrivals with
-// delay 0 cannot wait: every lane keeps, for each LIF-post projection, the
-// presynaptic neurons with slot 0 into its post neuron (a bitmask in
-// registers; their weights in LDS, in ascending presynaptic order) and adds
-// those of step n's spikes to the arrival at step n, after the ring cell
-// (which by then holds every earlier step's weights): the same fp32 sequence
-// as adding in emission order.  With rings in HBM, more than two (layer,
-// LIF-post projection) pairs, 1024 threads, no LDS left for the weights, or
-// a post neuron with more than SNN_ZMAX zero-delay synapses, the scatter is
-// immediate.
+// The scatter of a step's spikes is immediate: in chunks, their weight rows
+// are loaded and added to the ring cells of their arrivals (delay 0
+// included) before the step's arrivals are read.  (A variant that loaded
+// the weights a step ahead and scattered them one step later, adding
+// zero-delay synapses from per-lane lists, was slower on gfx950 and is
+// gone.)
 #pragma once
 
 #include <type_traits>
@@ -30,36 +24,22 @@
 
 namespace {
 
-constexpr int kZMax = SNN_ZMAX;   // zero-delay synapses per lane and projection
-
 template <int MAXT, int NL, int NP, bool RL>
 struct FwdCore {
     static constexpr int NWM = MAXT / 64;
-    static constexpr int KP = (NL == 1) ? 8 : 4;     // spikes per step with prefetched weights
-    static constexpr int KS = 4;                      // spikes per column_add_all of the deferred scatter
     // spikes per chunk of the immediate scatter: with rings in device memory
     // every chunk costs serialized round trips (weights, cells, stores), so
     // the chunks are larger there
     static constexpr int KI = RL ? KB : 16;
-    static constexpr int NPA = NP > 0 ? NP : 1;
-    // the deferred scatter's register lists fit without spills for one LIF
-    // layer, or two with one LIF-post projection each, at 256 threads (and it
-    // needs a ring to defer into)
-    static constexpr bool kDeferable = RL && MAXT <= 256 && NP >= 1 && NL * NP <= 2;
 
-    // Loads in flight for the next step: weights and slots of this step's
-    // first KP spikes (this lane's post, every LIF-post projection) and the
-    // next input arrival.
+    // Load in flight for the next step: its input arrival.
     struct Pre {
-        uint2 ws[NL][NPA][KP];
-        int cnt[NL];
         float ain;
     };
 
     struct Lane {
         float V[NL], I[NL];
         int cnt[NL];                          // records so far (exact; may pass the capacity)
-        unsigned long long zb[NL][NPA][NWM];  // presynaptic neurons with slot 0 into this lane's post
     };
 
     template <typename Ptr>
@@ -147,7 +127,6 @@ struct FwdCore {
         }
     }
 
-    template <bool DEFER>
     static __device__ __forceinline__ void step(const CoreFwdArgs& a, int b, int tid, int n,
                                                 const Pre& P, Pre& N, Lane& L) {
         const int lane = tid & 63, wave = tid >> 6;
@@ -172,10 +151,9 @@ struct FwdCore {
         }
         __syncthreads();
 
-        // ---- counts, this lane's rank among the step's spikes (ascending
-        // neuron order) and the step's first KP spikes
+        // ---- counts and this lane's rank among the step's spikes
+        // (ascending neuron order)
         unsigned long long mw[NL][NWM];
-        int ids[NL][KP];
         int tot[NL], rank[NL], cnt0[NL];
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
@@ -193,47 +171,15 @@ struct FwdCore {
             cnt0[l] = L.cnt[l];
             L.cnt[l] += total;
             tot[l] = total;
-            word_ids<NWM, KP>(mw[l], masks + (size_t)(par * NL + l) * NW, NW, 0, ids[l]);
         }
 
-        // loads issued a step ago (P) have landed; waiting here, not at the
-        // step start, lets the dynamics, the barrier and the ids above cover
-        // their latency (no stores of this step are in flight yet)
+        // the input arrival loaded a step ago (P) has landed
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
 
-        if constexpr (DEFER) {
-            // ---- step n - 1's spikes into the rings (delays >= 1), weights loaded then
-            if (n >= 1) {
+        // ---- this step's spikes into the rings (all delays)
 #pragma unroll
-                for (int l = 0; l < NL; ++l) {
-#pragma unroll
-                    for (int pp = 0; pp < NP; ++pp) {
-                        if (pp < a.ly[l].npost)
-                            scatter<KP, KS>(a, b, l, pp, tid, n - 1, P.cnt[l], 1, P.ws[l][pp]);
-                    }
-                    if (P.cnt[l] > KP) {
-                        const unsigned long long* prow = masks + (size_t)(((n - 1) % 3) * NL + l) * NW;
-                        unsigned long long mp[NWM];
-                        row_words<NWM>(prow, NW, mp);
-                        scatter_rest(a, b, l, tid, n - 1, mp, prow, KP, P.cnt[l], 1);
-                    }
-                }
-            }
-            // ---- loads for the next step: weights of this step's spikes
-#pragma unroll
-            for (int l = 0; l < NL; ++l) {
-#pragma unroll
-                for (int pp = 0; pp < NPA; ++pp) {
-                    if (pp < NP) load_ws<KP>(a, l, pp, tid, ids[l], N.ws[l][pp]);
-                }
-                N.cnt[l] = tot[l];
-            }
-        } else {
-            // ---- this step's spikes into the rings (all delays), loaded now
-#pragma unroll
-            for (int l = 0; l < NL; ++l)
-                scatter_rest(a, b, l, tid, n, mw[l], masks + (size_t)(par * NL + l) * NW, 0, tot[l], 0);
-        }
+        for (int l = 0; l < NL; ++l)
+            scatter_rest(a, b, l, tid, n, mw[l], masks + (size_t)(par * NL + l) * NW, 0, tot[l], 0);
         N.ain = a.A_in[((size_t)b * T + min(n + 1, T - 1)) * a.n1 + min(tid, a.n1 - 1)];
 
         // ---- spike records (I- of this step), step table, overflow
@@ -265,7 +211,6 @@ struct FwdCore {
 
         // ---- arrivals at step n: per projection into the layer, in projection order
         const int n_mod = n % S;
-        const int lanes = NW * 64;
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
             const FwdLayer& y = a.ly[l];
@@ -282,54 +227,21 @@ struct FwdCore {
                     RingPtr c = ring_col<RingPtr>(a, b, sl, pp, tid) + n_mod * y.n;
                     add = *c;
                     *c = 0.0f;
-                    if constexpr (DEFER) {
-                        // delay-0 arrivals of this step's spikes, ascending presynaptic index
-#pragma unroll
-                        for (int ll = 0; ll < NL; ++ll) {
-                            if (ll != sl) continue;
-#pragma unroll
-                            for (int pq = 0; pq < NPA; ++pq) {
-                                if (pq != pp) continue;
-                                // weights of this lane's zero-delay synapses, ascending
-                                const lds_f32* zw = (const lds_f32*)(reinterpret_cast<float*>(smem + a.zw_off)) +
-                                                    (size_t)(ll * NPA + pq) * kZMax * lanes + tid;
-                                int kbase = 0;
-#pragma unroll
-                                for (int w = 0; w < NWM; ++w) {
-                                    const unsigned long long z = L.zb[ll][pq][w];
-                                    unsigned long long h = mw[ll][w] & z;
-                                    while (h) {
-                                        const int bit = __builtin_ctzll(h);
-                                        const int k = kbase + __popcll(z & ((1ull << bit) - 1ull));
-                                        add = __fadd_rn(add, zw[k * lanes]);
-                                        h &= h - 1;
-                                    }
-                                    kbase += __popcll(z);
-                                }
-                            }
-                        }
-                    }
                 }
                 L.I[l] = __fadd_rn(L.I[l], add);
             }
         }
     }
 
-    template <bool DEFER>
     static __device__ __forceinline__ void run_steps(const CoreFwdArgs& a, int b, int tid, Lane& L) {
         Pre A, B;
-#pragma unroll
-        for (int l = 0; l < NL; ++l) A.cnt[l] = 0;
         A.ain = a.A_in[(size_t)b * a.T * a.n1 + min(tid, a.n1 - 1)];
         int n = 0;
         for (; n + 1 < a.T; n += 2) {
-            step<DEFER>(a, b, tid, n, A, B, L);
-            step<DEFER>(a, b, tid, n + 1, B, A, L);
+            step(a, b, tid, n, A, B, L);
+            step(a, b, tid, n + 1, B, A, L);
         }
-        if (n < a.T) step<DEFER>(a, b, tid, n, A, B, L);
-        if constexpr (DEFER) {
-            // the spikes of the last step arrive after T: nothing to scatter
-        }
+        if (n < a.T) step(a, b, tid, n, A, B, L);
     }
 
     static __device__ __forceinline__ void run(const CoreFwdArgs& a) {
@@ -354,69 +266,8 @@ struct FwdCore {
             L.I[l] = 0.0f;
             L.cnt[l] = 0;
         }
-        bool defer = kDeferable && a.zw_off >= 0;
-        if constexpr (kDeferable) {
-            // ---- delay-0 synapses into this lane's post, per LIF-post
-            // projection: bitmask in registers, weights in LDS ascending
-            const int lanes = a.NW * 64;
-            bool over = false;
-#pragma unroll
-            for (int l = 0; l < NL; ++l) {
-#pragma unroll
-                for (int pp = 0; pp < NPA; ++pp) {
-#pragma unroll
-                    for (int w = 0; w < NWM; ++w) L.zb[l][pp][w] = 0ull;
-                    if (!defer) continue;
-                    lds_f32* zw = (lds_f32*)(reinterpret_cast<float*>(smem + a.zw_off)) +
-                                  (size_t)(l * NPA + pp) * kZMax * lanes + tid;
-                    const FwdLayer& y = a.ly[l];
-                    if (pp >= NP || pp >= y.npost) continue;
-                    const int nq = y.nq[pp];
-                    const bool live = tid < nq;
-                    const __amdgpu_buffer_rsrc_t rs = ws_rsrc(a, l, pp);
-                    const int col8 = min(tid, nq - 1) * 8;
-                    int cnt = 0;
-                    for (int i0 = 0; i0 < y.n; i0 += 8) {
-                        uint2 e8[8];
-#pragma unroll
-                        for (int k = 0; k < 8; ++k) {
-                            const auto v = __builtin_amdgcn_raw_buffer_load_b64(
-                                rs, col8, min(i0 + k, y.n - 1) * nq * 8, 0);
-                            e8[k] = make_uint2((unsigned)v[0], (unsigned)v[1]);
-                        }
-#pragma unroll
-                        for (int k = 0; k < 8; ++k) {
-                            const int i = i0 + k;
-                            if (!live || i >= y.n || e8[k].y != 0u) continue;
-#pragma unroll
-                            for (int w = 0; w < NWM; ++w)
-                                if (w == (i >> 6)) L.zb[l][pp][w] |= 1ull << (i & 63);
-                            if (cnt < kZMax) zw[cnt * lanes] = __uint_as_float(e8[k].x);
-                            ++cnt;
-                        }
-                    }
-                    over = over || cnt > kZMax;
-                }
-            }
-            // block-wide OR of `over` through mask row 2, which step 2 writes
-            // first (after the barriers of steps 0 and 1)
-            unsigned long long* vote =
-                reinterpret_cast<unsigned long long*>(smem + a.mask_off) + (size_t)2 * NL * a.NW;
-            const unsigned long long m = __ballot(over);
-            if ((tid & 63) == 0) vote[tid >> 6] = m;
-            __syncthreads();
-            bool any = false;
-            for (int w = 0; w < a.NW; ++w) any = any || vote[w] != 0ull;
-            defer = defer && !any;
-        } else {
-            __syncthreads();
-        }
-        if constexpr (kDeferable) {
-            if (defer) run_steps<true>(a, b, tid, L);
-            else run_steps<false>(a, b, tid, L);
-        } else {
-            run_steps<false>(a, b, tid, L);
-        }
+        __syncthreads();
+        run_steps(a, b, tid, L);
 
         // ---- final state and record counts
 #pragma unroll

@@ -69,7 +69,6 @@ constexpr int bwd_prefetch(int n_lif) { return n_lif == 1 ? 16 : 4; }
 
 // zero-delay synapses per post neuron and LIF-post projection that the
 // deferred forward scatter handles from LDS
-#define SNN_ZMAX 16
 
 struct FwdLayer {
     int n;
@@ -104,7 +103,6 @@ struct CoreFwdArgs {
     float* If;
     DevStatus* st;
     int mask_off;                      // byte offset of the ballot masks [3][NL][NW] in LDS
-    int zw_off;                        // byte offset of the zero-delay weights [NL][NP][SNN_ZMAX][64 NW]
                                        // in LDS, -1: none (no deferred scatter)
 };
 
