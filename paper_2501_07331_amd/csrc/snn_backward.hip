@@ -238,10 +238,11 @@ struct BwdCore {
                 int row = n_mod + sq;
                 row = (row >= a.S) ? row - a.S : row;
                 ok[k][pp] = pp < y.npost && q < cnt && tid < nq && n + sq <= a.T - 1;
+                // (in LDS the row is always in the ring and the column is
+                // clamped into it, so the read needs no mask; its value does)
                 if (RL)
-                    d[k][pp] = ((lds_f32*)(lds + y.qring_lds[pp]))[(ok[k][pp] ? row : 0) * nq +
-                                                                  (ok[k][pp] ? tid : 0)];
-                else
+                    d[k][pp] = ((lds_f32*)(lds + y.qring_lds[pp]))[row * nq + min(tid, nq - 1)];
+                else   // (masked reads share one line of device memory)
                     d[k][pp] = ((global_f32*)(y.qring[pp] +
                                               ((size_t)b * a.S + (ok[k][pp] ? row : 0)) * nq))[ok[k][pp] ? tid : 0];
             }
@@ -640,7 +641,7 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
                     asm volatile("" : "+v"(dk));
                     if (dk < 0) continue;
                     const int pi = (dk >> 20) & 1, sl = (dk >> 21) & 0xFF;
-                    const float2* stk = st + ((dk >> 16) & 0xF) * TW - w0;   // index: arrival step
+                    const float2* stk = st + ((dk >> 16) & 0xF) * TW;        // index: arrival - w0
                     const int* gs = pi ? gs1 : gs0;
                     const int off = pi ? c0 - s1 : -s0;             // LDS index = x + off
                     float pu = 0.0f, pd = 0.0f;
@@ -658,7 +659,7 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
                         }
                         float2 ud[4];
 #pragma unroll
-                        for (int u = 0; u < 4; ++u) ud[u] = stk[(m[u] < wend) ? m[u] : w0];
+                        for (int u = 0; u < 4; ++u) ud[u] = stk[(m[u] < wend) ? m[u] - w0 : 0];
 #pragma unroll
                         for (int u = 0; u < 4; ++u) {
                             if (m[u] < wend) {
