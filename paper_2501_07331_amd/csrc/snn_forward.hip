@@ -176,8 +176,11 @@ __global__ void __launch_bounds__(64) input_scan_kernel(InScanArgs a) {
                     const int s = (int)w[q].y;
                     int r = fr + (st[q] - f) + s;
                     r = (r >= R) ? r - R : r;
-                    row[q] = (q < nv && st[q] + s < T) ? r : R;
-                    wv[q] = __uint_as_float(w[q].x);
+                    // an event past the end or arriving at or after T adds
+                    // -0 (x + -0 = x exactly, signed zeros included) to its
+                    // row, which lies in the lane's own ring window
+                    row[q] = r;
+                    wv[q] = (q < nv && st[q] + s < T) ? __uint_as_float(w[q].x) : -0.0f;
                 }
                 column_add_all(ring, 64, row, wv);
             } else {
