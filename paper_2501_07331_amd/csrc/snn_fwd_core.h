@@ -99,9 +99,17 @@ struct FwdCore {
                 const int s = (int)w[q].y;
                 int r = e_mod + s;
                 r = (r >= S) ? r - S : r;
-                const bool ok = live && q < cnt && s >= smin && e + s <= a.T - 1;
-                row[k] = ok ? r : S;                  // row S: dummy
-                wv[k] = __uint_as_float(w[q].x);
+                const bool ok = q < cnt && s >= smin && e + s <= a.T - 1;
+                if constexpr (RL) {
+                    // a masked spike adds -0 (x + -0 = x exactly) to its own
+                    // row, which no pending step shares; lanes past the
+                    // layer, whose column is another lane's, use row S (dummy)
+                    row[k] = live ? r : S;
+                    wv[k] = ok ? __uint_as_float(w[q].x) : -0.0f;
+                } else {
+                    row[k] = (live && ok) ? r : S;    // row S: dummy
+                    wv[k] = __uint_as_float(w[q].x);
+                }
             }
             column_add_all(col, nq, row, wv);
         }
