@@ -27,10 +27,10 @@ namespace {
 template <int MAXT, int NL, int NP, bool RL>
 struct FwdCore {
     static constexpr int NWM = MAXT / 64;
-    // spikes per chunk of the immediate scatter: with rings in device memory
-    // every chunk costs serialized round trips (weights, cells, stores), so
-    // the chunks are larger there
-    static constexpr int KI = RL ? KB : 16;
+    // spikes per chunk of the scatter: with rings in device memory every
+    // chunk costs serialized round trips (weights, cells, stores), so wide
+    // layers, which carry tens of spikes per step, take larger chunks there
+    static constexpr int KI = (RL || MAXT <= 256) ? KB : 16;
 
     // Load in flight for the next step: its input arrival.
     struct Pre {
