@@ -66,13 +66,23 @@ __global__ void __launch_bounds__(1024) readout_adjoint_kernel(ReadoutBwdArgs a)
         const int i = a.rec_n[base + r], n = a.rec_s[base + r];
         const uint2* wsr = a.ws + (size_t)i * C;
         double acc = 0.0;
-        for (int k = 0; k < C; ++k) {
-            const uint2 e = wsr[k];
-            const int m = n + (int)e.y;
-            if (m <= T - 1) {
-                const float d = a.tab_lds ? (float)tab[m * C + k] : tdb[(size_t)m * C + k];
-                acc -= (double)__fmul_rn(__uint_as_float(e.x), d);
+        // four outputs at a time: their loads issued together, their terms
+        // added in output order
+        for (int k0 = 0; k0 < C; k0 += 4) {
+            uint2 e[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) e[u] = wsr[min(k0 + u, C - 1)];
+            float d[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int k = min(k0 + u, C - 1);
+                const int m = min(n + (int)e[u].y, T - 1);
+                d[u] = a.tab_lds ? (float)tab[m * C + k] : tdb[(size_t)m * C + k];
             }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (k0 + u < C && n + (int)e[u].y <= T - 1)
+                    acc -= (double)__fmul_rn(__uint_as_float(e[u].x), d[u]);
         }
         a.A2[base + r] = acc;
     }
