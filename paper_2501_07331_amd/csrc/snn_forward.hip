@@ -247,6 +247,57 @@ __global__ void __launch_bounds__(64) input_scan_kernel(InScanArgs a) {
 
 // ------------------------------------------------------------------ readout
 
+struct LiState {
+    float V, I, acc, best;
+    int nst;
+};
+
+// One LI step: V- = alpha V + gamma I, I- = beta I, the loss statistic of V-
+// (running sum, or first maximum and its step), then the arrivals x of the
+// step added to I.
+template <bool SUM>
+__device__ __forceinline__ void li_step(const Topo& t, int n, float x, LiState& q) {
+    const float gi = __fmul_rn(t.gamma, q.I);
+    const float Vm = __fmaf_rn(t.alpha, q.V, gi);
+    q.I = __fmul_rn(t.beta, q.I);
+    q.V = Vm;
+    if (SUM) {
+        q.acc = __fadd_rn(q.acc, Vm);
+    } else if (n == 0 || Vm > q.best) {
+        q.best = Vm;
+        q.nst = n;
+    }
+    q.I = __fadd_rn(q.I, x);
+}
+
+// The LI layer over T steps of one lane's arrival column (step n at
+// col[n * C]).  The arrivals are read in blocks of U steps, the next block's
+// reads issued before the current block is run (two register blocks taking
+// turns, so no copy waits for a read in flight); reads past the end take row
+// T - 1 and are not used.
+template <bool SUM, typename Ptr>
+__device__ __forceinline__ void li_run(Ptr col, int C, int T, const Topo& t, LiState& q) {
+    constexpr int U = 16;
+    float xa[U], xb[U];
+    auto load = [&](int n0, float (&x)[U]) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) x[u] = col[(size_t)min(n0 + u, T - 1) * C];
+    };
+    auto run = [&](int n0, const float (&x)[U]) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (n0 + u < T) li_step<SUM>(t, n0 + u, x[u], q);
+    };
+    load(0, xa);
+    for (int n0 = 0; n0 < T; n0 += 2 * U) {
+        load(n0 + U, xb);
+        run(n0, xa);
+        if (n0 + U >= T) break;
+        load(n0 + 2 * U, xa);
+        run(n0 + U, xb);
+    }
+}
+
 // One workgroup per sample.  Waves come in groups of OB = ceil(C / 64), lane
 // k of a group owning output neuron k; group g builds rows [g W, (g + 1) W)
 // of the arrival table [T + 1][C] (row T: dummy), scattering the records
@@ -294,22 +345,17 @@ __global__ void __launch_bounds__(1024) readout_forward_kernel(ReadoutArgs a) {
     if (grp != 0) return;
     if (k >= C) return;
     const global_f32* ain = (const global_f32*)(a.A_in + (size_t)b * T * C) + k;
-    float V = 0.0f, I = 0.0f, acc = 0.0f, best = 0.0f;
-    int nst = 0;
-    for (int n = 0; n < T; ++n) {
-        const float gi = __fmul_rn(t.gamma, I);
-        const float Vm = __fmaf_rn(t.alpha, V, gi);
-        I = __fmul_rn(t.beta, I);
-        V = Vm;
-        if (t.loss == SNN_LOSS_CE_SUM) {
-            acc = __fadd_rn(acc, Vm);
-        } else if (n == 0 || Vm > best) {
-            best = Vm;
-            nst = n;
-        }
-        const float add = (pa == 0) ? ain[(size_t)n * C] : (in_lds ? lcol[n * C] : gcol[n * C]);
-        I = __fadd_rn(I, add);
+    LiState q{};
+    const bool sum = t.loss == SNN_LOSS_CE_SUM;
+    if (pa == 0) {
+        if (sum) li_run<true>(ain, C, T, t, q); else li_run<false>(ain, C, T, t, q);
+    } else if (in_lds) {
+        if (sum) li_run<true>(lcol, C, T, t, q); else li_run<false>(lcol, C, T, t, q);
+    } else {
+        if (sum) li_run<true>(gcol, C, T, t, q); else li_run<false>(gcol, C, T, t, q);
     }
+    const float V = q.V, I = q.I, acc = q.acc, best = q.best;
+    const int nst = q.nst;
     a.z[(size_t)b * C + k] = (t.loss == SNN_LOSS_CE_SUM) ? __fmul_rn(t.rscale, acc) : best;
     a.nstar[(size_t)b * C + k] = (t.loss == SNN_LOSS_CE_SUM) ? -1 : nst;
     int nstate = 0;
