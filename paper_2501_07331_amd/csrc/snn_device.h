@@ -82,8 +82,13 @@ __device__ __forceinline__ bool bits_chunk(BitIter& it, int (&ids)[N]) {
 template <int NWM>
 __device__ __forceinline__ void row_words(const unsigned long long* row, int NW,
                                           unsigned long long (&m)[NWM]) {
+    // every read stays in the row (no branch around it); words past NW are
+    // zeroed after the read
 #pragma unroll
-    for (int w = 0; w < NWM; ++w) m[w] = (w < NW) ? row[w] : 0ull;
+    for (int w = 0; w < NWM; ++w) {
+        const unsigned long long v = row[min(w, NW - 1)];
+        m[w] = (w < NW) ? v : 0ull;
+    }
 #pragma unroll
     for (int w = 0; w < NWM; ++w) m[w] = uniform64(m[w]);
 }
