@@ -1,6 +1,8 @@
 // Device helpers shared by the kernels of libsnn (gfx950, wave64).
 #pragma once
 
+#include <type_traits>
+
 #include "snn_internal.h"
 
 extern __shared__ __align__(16) unsigned char smem[];
@@ -178,6 +180,43 @@ __device__ __forceinline__ void column_add_all(Ptr col, int stride, const int (&
     for (int k = 0; k < K; ++k) col[row[k] * stride] = v[k];
 }
 
+// The same sums for a column in LDS, in rounds of P entries: a round reads
+// its P cells, merges equal rows among them in registers, adds and writes
+// back, and the next round's reads are issued after those writes (the LDS
+// accesses of a lane complete in order), so they see them.  Fewer merge
+// instructions (P (P - 1) / 2 pairs per round instead of K (K - 1) / 2) for
+// more LDS round trips; P = 2 is the fastest split for chunks of 8 on gfx950.
+template <int P, int K>
+__device__ __forceinline__ void column_add_rounds(lds_f32* col, int stride, const int (&row)[K],
+                                                  const float (&w)[K]) {
+    static_assert(K % P == 0, "rounds must cover the chunk");
+#pragma unroll
+    for (int h = 0; h < K / P; ++h) {
+        float v[P];
+#pragma unroll
+        for (int k = 0; k < P; ++k) v[k] = col[row[h * P + k] * stride];
+#pragma unroll
+        for (int k = 0; k < P; ++k) {
+            float base = v[k];
+#pragma unroll
+            for (int j = 0; j < k; ++j) base = (row[h * P + j] == row[h * P + k]) ? v[j] : base;
+            v[k] = __fadd_rn(base, w[h * P + k]);
+        }
+#pragma unroll
+        for (int k = 0; k < P; ++k) col[row[h * P + k] * stride] = v[k];
+    }
+}
+
+// Chunk sums into a column: in LDS in rounds of two entries, in device
+// memory all at once (every round there would be a memory round trip).
+template <typename Ptr, int K>
+__device__ __forceinline__ void column_add(Ptr col, int stride, const int (&row)[K], const float (&w)[K]) {
+    if constexpr (std::is_same<Ptr, lds_f32*>::value)
+        column_add_rounds<2>(col, stride, row, w);
+    else
+        column_add_all(col, stride, row, w);
+}
+
 // Delayed scatter of a sorted event list into a table, one column per lane:
 // for every event e in [e_lo, e_hi) in order (presynaptic neuron ids[e] at
 // step steps[e]), the lane adds w(ids[e], col) to the cell of arrival step
@@ -192,9 +231,9 @@ __device__ __forceinline__ void column_add_all(Ptr col, int stride, const int (&
 // of chunks (one event per lane) are in flight.  One wait at each chunk
 // start covers the loads issued a chunk earlier, and the weight registers
 // alternate between the two chunks of a pair, so no register copy waits for
-// a load in flight.  A lane adds a chunk to its own column with one
-// read-modify-write per cell, equal rows merged in registers in event order
-// (fp32 LDS atomics would keep the order too, but are far slower).
+// a load in flight.  A lane adds a chunk to its own column in event order
+// (column_add: in LDS in rounds of two events; fp32 LDS atomics would keep
+// the order too, but are far slower).
 template <typename Ptr>
 __device__ __forceinline__ void scatter_events(const int* ids, const int* steps, int e_lo, int e_hi,
                                                const uint2* ws, int ws_bytes, int npost, int col,
@@ -230,7 +269,7 @@ __device__ __forceinline__ void scatter_events(const int* ids, const int* steps,
             row[q] = (q < nv && (unsigned)d < span) ? d : dummy;
             wv[q] = __uint_as_float(w[q].x);
         }
-        column_add_all(tab, ld, row, wv);
+        column_add(tab, ld, row, wv);
     };
     int idA, stA, idB, stB;
     uint2 w0[KB], w1[KB];

@@ -182,7 +182,7 @@ __global__ void __launch_bounds__(64) input_scan_kernel(InScanArgs a) {
                     row[q] = r;
                     wv[q] = (q < nv && st[q] + s < T) ? __uint_as_float(w[q].x) : -0.0f;
                 }
-                column_add_all(ring, 64, row, wv);
+                column_add(ring, 64, row, wv);
             } else {
                 // rare: events one by one, reloaded
                 const int n = min(nv, KB);

@@ -111,7 +111,7 @@ struct FwdCore {
                     wv[k] = __uint_as_float(w[q].x);
                 }
             }
-            column_add_all(col, nq, row, wv);
+            column_add(col, nq, row, wv);
         }
     }
 
