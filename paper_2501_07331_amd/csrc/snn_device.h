@@ -246,16 +246,17 @@ __device__ __forceinline__ void scatter_events(const int* ids, const int* steps,
     const int col8 = min(max(col, 0), npost - 1) * 8;
     const int row8 = npost * 8;
     const unsigned span = (unsigned)(live ? m_end - m0 : 0);   // dead lanes: all to the dummy
-    auto load_pair = [&](int e0, int& id, int& st) {  // lane q < 2 KB: event e0 + q
+    // lane q < 2 KB: event e0 + q, the byte offset of its weight row and its step
+    auto load_pair = [&](int e0, int& id, int& st) {
         const int e = min(e0 + (lane & (2 * KB - 1)), e_hi - 1);
-        id = ids[e];
+        id = ids[e] * row8;
         st = steps[e];
     };
-    auto load_ws = [&](int id_v, int qoff, uint2 (&w)[KB]) {
+    auto load_ws = [&](int off_v, int qoff, uint2 (&w)[KB]) {
 #pragma unroll
         for (int q = 0; q < KB; ++q) {
-            const int id = __builtin_amdgcn_readlane(id_v, qoff + q);
-            const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, col8, id * row8, 0);
+            const int off = __builtin_amdgcn_readlane(off_v, qoff + q);
+            const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, col8, off, 0);
             w[q] = make_uint2((unsigned)v[0], (unsigned)v[1]);
         }
     };

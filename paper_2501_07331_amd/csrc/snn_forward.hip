@@ -134,17 +134,18 @@ __global__ void __launch_bounds__(64) input_scan_kernel(InScanArgs a) {
         const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
             (void*)a.ws0, (short)0, a.n_in * n1 * 8, 0x00020000);
         const int col8 = jc * 8, row8 = n1 * 8;
-        // events e0 + q for lanes q < 2 KB (clamped to the last event)
-        auto load_pair = [&](int e0, int& idv, int& stv) {
+        // events e0 + q for lanes q < 2 KB (clamped to the last event): the
+        // byte offset of the event's weight row, and its step
+        auto load_pair = [&](int e0, int& rowv, int& stv) {
             const int e = min(e0 + (lane & (2 * KB - 1)), E1 - 1);
-            idv = a.in_neuron[e];
+            rowv = a.in_neuron[e] * row8;
             stv = a.in_step[e];
         };
-        auto load_ws = [&](int idv, int u8, uint2 (&w)[KB]) {
+        auto load_ws = [&](int rowv, int u8, uint2 (&w)[KB]) {
 #pragma unroll
             for (int q = 0; q < KB; ++q) {
-                const int id = __builtin_amdgcn_readlane(idv, u8 + q);
-                const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, col8, id * row8, 0);
+                const int off = __builtin_amdgcn_readlane(rowv, u8 + q);
+                const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, col8, off, 0);
                 w[q] = make_uint2((unsigned)v[0], (unsigned)v[1]);
             }
         };
@@ -165,9 +166,7 @@ __global__ void __launch_bounds__(64) input_scan_kernel(InScanArgs a) {
             int st[KB];
 #pragma unroll
             for (int q = 0; q < KB; ++q) st[q] = __builtin_amdgcn_readlane(stv, u8 + q);
-            int last = st[0];
-#pragma unroll
-            for (int q = 1; q < KB; ++q) last = (q < nv) ? st[q] : last;
+            const int last = __builtin_amdgcn_readlane(stv, u8 + min(nv, KB) - 1);   // last valid step
             if (last - f < TB) {
                 int row[KB];
                 float wv[KB];
@@ -201,44 +200,44 @@ __global__ void __launch_bounds__(64) input_scan_kernel(InScanArgs a) {
         // vmcnt(8): all but the newest eight operations (chunk c + 1's weight
         // loads) have landed
         constexpr int kWaitVm8 = 0x0F70 | 8;
-        int idX, stX, idY, stY, idZ, stZ;
+        int rowX, stX, rowY, stY, rowZ, stZ;
         uint2 w0[KB], w1[KB], w2[KB];
-        load_pair(E0, idX, stX);
-        load_pair(E0 + 2 * KB, idY, stY);
+        load_pair(E0, rowX, stX);
+        load_pair(E0 + 2 * KB, rowY, stY);
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
-        load_ws(idX, 0, w0);
-        load_ws(idX, KB, w1);
+        load_ws(rowX, 0, w0);
+        load_ws(rowX, KB, w1);
         // per chunk: wait, write out, next pair's ids, weights of chunk c + 2,
         // add chunk c; pairs X, Y, Z hold events e0 .., e0 + 16 .., e0 + 32 ..
         for (int e0 = E0; e0 < E1; e0 += 6 * KB) {
             __builtin_amdgcn_s_waitcnt(kWaitVm8);
             flush_before(e0, stX, 0);
-            load_pair(e0 + 4 * KB, idZ, stZ);
-            load_ws(idY, 0, w2);
+            load_pair(e0 + 4 * KB, rowZ, stZ);
+            load_ws(rowY, 0, w2);
             add_chunk(e0, stX, 0, w0);
             __builtin_amdgcn_s_waitcnt(kWaitVm8);
             flush_before(e0 + KB, stX, KB);
-            load_ws(idY, KB, w0);
+            load_ws(rowY, KB, w0);
             add_chunk(e0 + KB, stX, KB, w1);
             if (e0 + 2 * KB >= E1) break;
             __builtin_amdgcn_s_waitcnt(kWaitVm8);
             flush_before(e0 + 2 * KB, stY, 0);
-            load_pair(e0 + 6 * KB, idX, stX);
-            load_ws(idZ, 0, w1);
+            load_pair(e0 + 6 * KB, rowX, stX);
+            load_ws(rowZ, 0, w1);
             add_chunk(e0 + 2 * KB, stY, 0, w2);
             __builtin_amdgcn_s_waitcnt(kWaitVm8);
             flush_before(e0 + 3 * KB, stY, KB);
-            load_ws(idZ, KB, w2);
+            load_ws(rowZ, KB, w2);
             add_chunk(e0 + 3 * KB, stY, KB, w0);
             if (e0 + 4 * KB >= E1) break;
             __builtin_amdgcn_s_waitcnt(kWaitVm8);
             flush_before(e0 + 4 * KB, stZ, 0);
-            load_pair(e0 + 8 * KB, idY, stY);
-            load_ws(idX, 0, w0);
+            load_pair(e0 + 8 * KB, rowY, stY);
+            load_ws(rowX, 0, w0);
             add_chunk(e0 + 4 * KB, stZ, 0, w1);
             __builtin_amdgcn_s_waitcnt(kWaitVm8);
             flush_before(e0 + 5 * KB, stZ, KB);
-            load_ws(idX, KB, w1);
+            load_ws(rowX, KB, w1);
             add_chunk(e0 + 5 * KB, stZ, KB, w2);
         }
     }
