@@ -173,13 +173,16 @@ __global__ void __launch_bounds__(64) input_scan_kernel(InScanArgs a) {
 #pragma unroll
                 for (int q = 0; q < KB; ++q) {
                     const int s = (int)w[q].y;
-                    int r = fr + (st[q] - f) + s;
-                    r = (r >= R) ? r - R : r;
+                    // uniform parts: the ring row of arrival step st[q], and
+                    // the slots that arrive before T (none past the end)
+                    const int r0 = fr + (st[q] - f);
+                    const int lim = (q < nv) ? T - st[q] : 0;
+                    const unsigned r = (unsigned)(r0 + s);
                     // an event past the end or arriving at or after T adds
                     // -0 (x + -0 = x exactly, signed zeros included) to its
                     // row, which lies in the lane's own ring window
-                    row[q] = r;
-                    wv[q] = (q < nv && st[q] + s < T) ? __uint_as_float(w[q].x) : -0.0f;
+                    row[q] = (int)min(r, r - (unsigned)R);     // r mod R (r < 2 R)
+                    wv[q] = (s < lim) ? __uint_as_float(w[q].x) : -0.0f;
                 }
                 column_add(ring, 64, row, wv);
             } else {
