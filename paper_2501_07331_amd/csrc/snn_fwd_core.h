@@ -78,16 +78,22 @@ struct FwdCore {
     }
 
     // Adds the weights of spikes 0 .. N) (valid below cnt) emitted at step e to
-    // the ring cells of their arrivals, slots >= smin, arrivals before T, in
-    // chunks of C.
+    // the ring cells of their arrivals, arrivals before T, in chunks of C.
     template <int N, int C>
     static __device__ __forceinline__ void scatter(const CoreFwdArgs& a, int b, int l, int pp, int tid,
-                                                   int e, int cnt, int smin, const uint2 (&w)[N]) {
+                                                   int e, int cnt, const uint2 (&w)[N]) {
         const FwdLayer& y = a.ly[l];
         const int nq = y.nq[pp], S = a.S;
         const bool live = pp < y.npost && tid < nq;
         const int e_mod = e % S;
         RingPtr col = ring_col<RingPtr>(a, b, l, pp, min(tid, nq - 1));
+        int stride = nq;
+        if constexpr (RL) {
+            // lanes past the layer, whose column is another lane's, add
+            // every spike to row S (dummy) of it: stride 0 from that cell
+            col = live ? col : col + S * nq;
+            stride = live ? nq : 0;
+        }
 #pragma unroll
         for (int q0 = 0; q0 < N; q0 += C) {
             if (cnt <= q0) continue;
@@ -97,21 +103,23 @@ struct FwdCore {
             for (int k = 0; k < C; ++k) {
                 const int q = q0 + k;
                 const int s = (int)w[q].y;
-                int r = e_mod + s;
-                r = (r >= S) ? r - S : r;
-                const bool ok = q < cnt && s >= smin && e + s <= a.T - 1;
                 if constexpr (RL) {
+                    // slots below lim arrive before T (none past the count);
                     // a masked spike adds -0 (x + -0 = x exactly) to its own
-                    // row, which no pending step shares; lanes past the
-                    // layer, whose column is another lane's, use row S (dummy)
-                    row[k] = live ? r : S;
-                    wv[k] = ok ? __uint_as_float(w[q].x) : -0.0f;
+                    // row, which no pending step shares
+                    const int lim = (q < cnt) ? a.T - e : 0;
+                    const unsigned r = (unsigned)(e_mod + s);
+                    row[k] = (int)min(r, r - (unsigned)S);     // (e + s) mod S, as e_mod + s < 2 S
+                    wv[k] = (s < lim) ? __uint_as_float(w[q].x) : -0.0f;
                 } else {
+                    int r = e_mod + s;
+                    r = (r >= S) ? r - S : r;
+                    const bool ok = q < cnt && e + s <= a.T - 1;
                     row[k] = (live && ok) ? r : S;    // row S: dummy
                     wv[k] = __uint_as_float(w[q].x);
                 }
             }
-            column_add(col, nq, row, wv);
+            column_add(col, stride, row, wv);
         }
     }
 
@@ -119,8 +127,7 @@ struct FwdCore {
     // in chunks of KB with their weights loaded now.
     static __device__ __forceinline__ void scatter_rest(const CoreFwdArgs& a, int b, int l, int tid, int e,
                                         const unsigned long long (&m)[NWM],
-                                        const unsigned long long* row, int from, int total,
-                                        int smin) {
+                                        const unsigned long long* row, int from, int total) {
         const FwdLayer& y = a.ly[l];
         for (int q0 = from; q0 < total; q0 += KI) {
             int ids[KI];
@@ -130,7 +137,7 @@ struct FwdCore {
                 if (pp >= y.npost) continue;
                 uint2 w[KI];
                 load_ws<KI>(a, l, pp, tid, ids, w);
-                scatter<KI, KI>(a, b, l, pp, tid, e, total - q0, smin, w);
+                scatter<KI, KI>(a, b, l, pp, tid, e, total - q0, w);
             }
         }
     }
@@ -187,7 +194,7 @@ struct FwdCore {
         // ---- this step's spikes into the rings (all delays)
 #pragma unroll
         for (int l = 0; l < NL; ++l)
-            scatter_rest(a, b, l, tid, n, mw[l], masks + (size_t)(par * NL + l) * NW, 0, tot[l], 0);
+            scatter_rest(a, b, l, tid, n, mw[l], masks + (size_t)(par * NL + l) * NW, 0, tot[l]);
         N.ain = a.A_in[((size_t)b * T + min(n + 1, T - 1)) * a.n1 + min(tid, a.n1 - 1)];
 
         // ---- spike records (I- of this step), step table, overflow
