@@ -232,7 +232,7 @@ struct BwdCore {
         // column 0), issued together; the empty asm takes them as operands so
         // that the compiler keeps them unconditional (it would otherwise move
         // each read behind its own mask branch and wait for it there) and one
-        // wait covers all of them; a masked term is then 0 x 0
+        // wait covers all of them; a masked term is then +0
         float d[4][NPA];
         bool ok[4][NPA];
 #pragma unroll
@@ -245,9 +245,13 @@ struct BwdCore {
                 if (pp >= NP) continue;
                 const int nq = y.nq[pp];
                 const int sq = (int)ws[pp][q].y;
-                int row = n_mod + sq;
-                row = (row >= a.S) ? row - a.S : row;
-                ok[k][pp] = pp < y.npost && q < cnt && tid < nq && n + sq <= a.T - 1;
+                // uniform: slots below lim arrive by T - 1 (none past the
+                // count or the projections); the row by an unsigned min, as
+                // n_mod + sq < 2 S
+                const int lim = (pp < y.npost && q < cnt) ? a.T - n : 0;
+                const unsigned ru = (unsigned)(n_mod + sq);
+                const int row = (int)min(ru, ru - (unsigned)a.S);
+                ok[k][pp] = sq < lim && tid < nq;
                 // (in LDS the row is always in the ring and the column is
                 // clamped into it, so the read needs no mask; its value does)
                 if (RL)
@@ -270,9 +274,9 @@ struct BwdCore {
             v[k] = 0.0;
 #pragma unroll
             for (int pp = 0; pp < NP; ++pp) {
-                const float wm = ok[k][pp] ? __uint_as_float(ws[pp][q].x) : 0.0f;
-                const float dm = ok[k][pp] ? d[k][pp] : 0.0f;
-                v[k] -= (double)__fmul_rn(wm, dm);
+                // a masked term is +0 (v - 0 = v exactly)
+                const float t = __fmul_rn(__uint_as_float(ws[pp][q].x), d[k][pp]);
+                v[k] -= (double)(ok[k][pp] ? t : 0.0f);
             }
         }
         const double x = row_sum4(v, lane);
