@@ -170,11 +170,13 @@ struct BwdCore {
                                                      double& A2) {
         const BwdLayer& y = a.ly[l];
         // (the ids stay in vector registers: held in scalar ones, the 16 ids
-        // and their row offsets overflow the scalar register file)
+        // and their row offsets overflow the scalar register file).  Entries
+        // past the count are not ids (stale table entries): their loads are
+        // bounds-checked buffer loads (an offset outside the matrix reads 0)
+        // and their values are masked, so the ids are used unclamped.
         int idc[KP];
 #pragma unroll
-        for (int q = 0; q < KP; ++q)
-            idc[q] = (q < cnt) ? min(max(ids[q], 0), y.n - 1) : 0;
+        for (int q = 0; q < KP; ++q) idc[q] = ids[q];
         mine = 0;
 #pragma unroll
         for (int q0 = 0; q0 < KP; q0 += 4) {
@@ -189,7 +191,9 @@ struct BwdCore {
                 const int col8 = min(tid, nq - 1) * 8;
 #pragma unroll
                 for (int q = q0; q < q0 + 4; ++q) {
-                    const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, col8 + idc[q] * nq * 8, 0, 0);
+                    // (unsigned: a stale entry's offset wraps instead of overflowing)
+                    const unsigned off = (unsigned)col8 + (unsigned)idc[q] * (unsigned)(nq * 8);
+                    const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, (int)off, 0, 0);
                     ws[pp][q] = make_uint2((unsigned)v[0], (unsigned)v[1]);
                 }
             }
