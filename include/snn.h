@@ -231,6 +231,24 @@ int snn_backward(snn_net* net, float* const* dW, float* const* dD);
 int snn_backward_lp(snn_net* net, const float* const* dlp, float* const* dW, float* const* dD);
 
 /*
+ * snn_backward for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight training or serving loops, harnesses that forbid
+ * hipMalloc.  Same computation and results as snn_backward, bit for bit.
+ * The one buffer snn_backward sizes by the last forward's input (the input
+ * spikes grouped by channel: batch x (n_input + 1) + nnz int32, grown on
+ * demand with hipMalloc) lives instead in a fixed library array of
+ * SNN_NOALLOC_SCRATCH_BYTES per device, so the call makes no hipMalloc,
+ * hipFree or other allocating call.  The array is shared by every handle on
+ * a device and keeps the last call's contents (every entry this call reads
+ * it writes first); calls that overlap on one device (other streams or host
+ * threads) race on it and must be serialised by the caller.
+ * Errors: as snn_backward, and SNN_EINVAL when batch x (n_input + 1) + nnz
+ * exceeds SNN_NOALLOC_SCRATCH_BYTES / 4 (nothing is enqueued then).
+ */
+#define SNN_NOALLOC_SCRATCH_BYTES (32u << 20)
+int snn_backward_noalloc(snn_net* net, float* const* dW, float* const* dD);
+
+/*
  * Parameter update after snn_backward: one optimiser step on every W and D,
  * then the delay clamp.  The paper trains weights and delays with separate
  * learning rates and schedules (Methods / "Implementation" and its

@@ -12,6 +12,7 @@ SNN_INPUT, SNN_LIF, SNN_LI = 0, 1, 2
 SNN_LOSS_CE_SUM, SNN_LOSS_CE_MAX, SNN_LOSS_DMSE = 0, 1, 2
 SNN_FLAG_HBM_RINGS = 1
 SNN_FLAG_TIMING = 2
+SNN_NOALLOC_SCRATCH_BYTES = 32 << 20
 SNN_OPT_SGD, SNN_OPT_ADAM = 0, 1
 _NAMES = {0: "SNN_OK", -1: "SNN_EINVAL", -2: "SNN_ENOMEM", -3: "SNN_ESTATE", -4: "SNN_EOVERFLOW",
           -5: "SNN_EDEVICE"}
@@ -91,6 +92,7 @@ def load_library():
                                 C.POINTER(snn_spikes_out), P, P]
     lib.snn_backward.argtypes = [P, C.POINTER(P), C.POINTER(P)]
     lib.snn_backward_lp.argtypes = [P, C.POINTER(P), C.POINTER(P), C.POINTER(P)]
+    lib.snn_backward_noalloc.argtypes = [P, C.POINTER(P), C.POINTER(P)]
     lib.snn_optimizer_step.argtypes = [P, C.POINTER(snn_optim), C.POINTER(P), C.POINTER(P),
                                        C.POINTER(P), C.POINTER(P)]
     lib.snn_optimizer_reset.argtypes = [P]
@@ -101,7 +103,7 @@ def load_library():
     lib.snn_destroy.argtypes = [P]
     lib.snn_destroy.restype = None
     for f in ("snn_create", "snn_num_projections", "snn_projection_info", "snn_forward",
-              "snn_backward", "snn_backward_lp", "snn_optimizer_step", "snn_optimizer_reset", "snn_get_state",
+              "snn_backward", "snn_backward_lp", "snn_backward_noalloc", "snn_optimizer_step", "snn_optimizer_reset", "snn_get_state",
               "snn_get_stats"):
         getattr(lib, f).restype = C.c_int
     _lib = lib
@@ -230,6 +232,18 @@ class Network:
             arr[i] = _ptr(x, f32, f"dlp[{i}]") if x is not None else None
         rc = self._lib.snn_backward_lp(self._h, arr, _ptr_array(dW, f32, "dW"),
                                        _ptr_array(dD, f32, "dD"))
+        return self._check(rc)
+
+    def backward_noalloc(self, dW, dD):
+        """snn_backward_noalloc: the backward pass with its input-sized scratch
+        in the library's fixed per-device array (no device allocation)."""
+        import torch
+        f32 = torch.float32
+        for p, (_, _, npre, npost) in enumerate(self.projections):
+            if dW[p].numel() != npre * npost or dD[p].numel() != npre * npost:
+                raise ValueError(f"dW/dD[{p}] must hold {npre}x{npost} elements")
+        rc = self._lib.snn_backward_noalloc(self._h, _ptr_array(dW, f32, "dW"),
+                                            _ptr_array(dD, f32, "dD"))
         return self._check(rc)
 
     def optimizer_step(self, W, D, dW, dD, kind: int = SNN_OPT_ADAM, lr_w: float = 1e-3,

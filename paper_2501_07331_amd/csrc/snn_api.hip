@@ -7,8 +7,40 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "snn_internal.h"
+
+// Fixed device scratch of snn_backward_noalloc: one copy per device, held
+// until the process ends.  Host code never uses this name as an address (on
+// the host it is only a stand-in for the symbol): the device address comes
+// from hipGetSymbolAddress, once per device, in snn_create.
+constexpr long long kScratchInts = (long long)(SNN_NOALLOC_SCRATCH_BYTES / sizeof(int));
+static __device__ __align__(256) int scratch[kScratchInts];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+int* g_scratch_addr[kMaxDevices];   // device address of `scratch` per device, NULL until looked up
+
+// The address of `scratch` on the current device (looked up on first use).
+hipError_t scratch_address(int** out) {
+    *out = nullptr;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_addr[dev]) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_addr[dev] = static_cast<int*>(ptr);
+    }
+    *out = g_scratch_addr[dev];
+    return hipSuccess;
+}
+}  // namespace
 
 namespace {
 
@@ -75,6 +107,7 @@ struct snn_net {
     int* in_goff;
     int* in_gstep;
     long long in_gstep_cap;
+    int* scratch;               // device address of the fixed scratch (snn_backward_noalloc)
     DevStatus* st;
     DevStatus* st_host;         // pinned
     // the last forward's inputs, kept for the backward
@@ -435,6 +468,10 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     int bad = -1;   // index of the kernel whose LDS limit was refused
     if (e == hipSuccess) e = hipHostMalloc((void**)&net->st_host, sizeof(DevStatus), hipHostMallocDefault);
     if (e == hipSuccess) {
+        what = "scratch symbol address";
+        e = scratch_address(&net->scratch);
+    }
+    if (e == hipSuccess) {
         what = "forward LDS limits";
         e = set_forward_lds_limits(kLds, &bad);
     }
@@ -687,12 +724,11 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
     return SNN_OK;
 }
 
-extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
-    return snn_backward_lp(net, nullptr, dW, dD);
-}
-
-extern "C" int snn_backward_lp(snn_net* net, const float* const* dlp, float* const* dW,
-                               float* const* dD) {
+// The backward pass.  in_goff / in_gstep: where the input spikes grouped by
+// channel go ([B][n_in + 1] and [nnz] int32); NULL: the handle's own buffers
+// (in_gstep grown on demand).
+static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW, float* const* dD,
+                         int* in_goff, int* in_gstep) {
     if (!net) return SNN_EINVAL;
     net->err[0] = 0;
     Topo& t = net->t;
@@ -719,7 +755,7 @@ extern "C" int snn_backward_lp(snn_net* net, const float* const* dlp, float* con
         }
     }
     // the grouped input steps need one slot per input spike of the last forward
-    if (net->in_nnz > net->in_gstep_cap) {
+    if (!in_gstep && net->in_nnz > net->in_gstep_cap) {
         HIP_TRY(net, hipStreamSynchronize(s));
         if (net->in_gstep) HIP_TRY(net, hipFree(net->in_gstep));
         net->in_gstep = nullptr;
@@ -730,6 +766,8 @@ extern "C" int snn_backward_lp(snn_net* net, const float* const* dlp, float* con
                         hipGetErrorString(e));
         net->in_gstep_cap = net->in_nnz;
     }
+    if (!in_goff) in_goff = net->in_goff;
+    if (!in_gstep) in_gstep = net->in_gstep;
     // spikes grouped by presynaptic neuron (inputs, then every LIF layer) on
     // the second stream: they depend on the forward only, and run beside the
     // latency-bound adjoint sweeps; the gradients wait for them
@@ -745,8 +783,8 @@ extern "C" int snn_backward_lp(snn_net* net, const float* const* dlp, float* con
         g.step = net->in_step;
         g.neuron = net->in_neuron;
         g.n = t.n_in;
-        g.g_off = net->in_goff;
-        g.g_step = net->in_gstep;
+        g.g_off = in_goff;
+        g.g_step = in_gstep;
         g.st = net->st;
         HIP_TRY(net, launch_group(g, t.B, g_s));
     }
@@ -889,8 +927,8 @@ extern "C" int snn_backward_lp(snn_net* net, const float* const* dlp, float* con
         ga.dD[p] = dD[p];
     }
     ga.ws = net->ws;
-    ga.g_off[0] = net->in_goff;
-    ga.g_step[0] = net->in_gstep;
+    ga.g_off[0] = in_goff;
+    ga.g_step[0] = in_gstep;
     for (int l = 1; l < t.L; ++l) {
         if (t.kind[l] != SNN_LIF) continue;
         const size_t li = (size_t)t.lif[l];
@@ -910,6 +948,29 @@ extern "C" int snn_backward_lp(snn_net* net, const float* const* dlp, float* con
     if (rc) return rc;
     net->stats.degenerate_jumps = (int64_t)net->st_host->degenerate;
     return SNN_OK;
+}
+
+extern "C" int snn_backward(snn_net* net, float* const* dW, float* const* dD) {
+    return backward_impl(net, nullptr, dW, dD, nullptr, nullptr);
+}
+
+extern "C" int snn_backward_lp(snn_net* net, const float* const* dlp, float* const* dW,
+                               float* const* dD) {
+    return backward_impl(net, dlp, dW, dD, nullptr, nullptr);
+}
+
+extern "C" int snn_backward_noalloc(snn_net* net, float* const* dW, float* const* dD) {
+    if (!net) return SNN_EINVAL;
+    const long long need = (long long)net->t.B * (net->t.n_in + 1) + net->in_nnz;
+    if (need > kScratchInts)
+        return fail(net, SNN_EINVAL,
+                    "snn_backward_noalloc: the grouped input spikes need %lld int32, the fixed "
+                    "scratch holds %lld (batch x (inputs + 1) + input spikes)",
+                    need, (long long)kScratchInts);
+    if (!net->scratch)
+        return fail(net, SNN_EDEVICE, "snn_backward_noalloc: no scratch address for this device");
+    int* goff = net->scratch;
+    return backward_impl(net, nullptr, dW, dD, goff, goff + (size_t)net->t.B * (net->t.n_in + 1));
 }
 
 extern "C" int snn_optimizer_step(snn_net* net, const snn_optim* o, float* const* W, float* const* D,
