@@ -28,15 +28,17 @@
  * gamma = tau_s/(tau_s - tau_m) (beta - alpha) (constants computed in fp64 on
  * the host, rounded to fp32); threshold V- >= theta, reset, record (n, i, I-);
  * emit every presynaptic spike into its projection's delay ring (one per
- * sample and projection) at slot (n + d) mod S, S = max_delay + 1, dropping
- * arrivals at or after T; then I = I- + ring_p[n mod S] for the projections p
- * into the layer, in projection order.  Delays are integer multiples of dt:
- * the slot is rint(D) (round half to even) clamped to [0, max_delay],
- * NaN -> 0.  All forward arithmetic is IEEE fp32 with no contraction; a ring
- * cell sums its weights in (emission step, presynaptic index) order, so spike
- * records are bit-reproducible.  The backward pass keeps adjoints in fp32 and
- * sums each synapse's gradient terms over one sample in fp32, in spike order,
- * and over the samples in fp64, in sample order: dW and dD are deterministic.
+ * sample and projection) at slot (n + d) mod S_p, S_p = the projection's
+ * largest delay + 1, dropping arrivals at or after T; then I = I- +
+ * ring_p[n mod S_p] for the projections p into the layer, in projection
+ * order.  Delays are integer multiples of dt: the slot is rint(D) (round half
+ * to even) clamped to [0, the projection's largest delay], NaN -> 0.  All
+ * forward arithmetic is IEEE fp32 with no contraction; a ring cell sums its
+ * weights in (emission step, presynaptic index) order, so spike records are
+ * bit-reproducible.  The backward pass is fp64 throughout (adjoints, their
+ * trajectories, jump sums, gradient sums), on the fp32 forward, and sums in
+ * a fixed order: dW and dD are deterministic and within rounding of the fp64
+ * evaluation of the same expressions.
  *
  * Projections.  Fixed order: for l = 1 .. L-1, the feed-forward projection
  * (l-1 -> l), then the recurrent one (l -> l) if layer l is recurrent.  Weight
@@ -78,7 +80,9 @@ enum { SNN_LOSS_CE_SUM = 0, SNN_LOSS_CE_MAX = 1, SNN_LOSS_DMSE = 2 };   /* losse
 
 #define SNN_MAX_LAYERS 6
 #define SNN_MAX_NEURONS 1024   /* per non-input layer */
+#define SNN_MAX_INPUT 16384    /* input neurons */
 #define SNN_MAX_DELAY 255
+#define SNN_MAX_T 65536        /* steps per sample (spike steps are staged as 16-bit values) */
 
 typedef struct snn_net snn_net;
 
@@ -105,6 +109,11 @@ typedef struct {
  *                   output neuron (a neuron that never fires carries none)
  * readout_scale:    s above (sum readout only)
  * record_capacity:  spike records kept per sample and LIF layer
+ * proj_max_delay:   host array of one largest delay (in steps) per projection,
+ *                   each in [0, max_delay], or NULL (max_delay for every
+ *                   projection): projection p's delays are clamped to it and
+ *                   its delay ring (and the adjoint ring of its post layer)
+ *                   holds that many steps + 1; read during snn_create only
  * flags:            bitwise OR of
  *                   SNN_FLAG_HBM_RINGS: keep every delay and adjoint ring in
  *                   device memory even where it would fit in LDS (same
@@ -124,6 +133,7 @@ typedef struct {
     int32_t flags;
     void* hip_stream;
     float dmse_delta;
+    const int32_t* proj_max_delay;
 } snn_opts;
 
 /* Input spikes, CSR over samples (dev): offsets [batch+1] with offsets[0] = 0
@@ -167,10 +177,11 @@ typedef struct {
  * 1 .. L-2 SNN_LIF, last layer SNN_LI, or a non-recurrent SNN_LIF with
  * SNN_LOSS_DMSE, 2 <= L <= SNN_MAX_LAYERS, at most SNN_MAX_LAYERS - 2 LIF
  * layers, non-input layers of 1 .. SNN_MAX_NEURONS neurons, only LIF layers
- * recurrent),
+ * recurrent, at most SNN_MAX_INPUT input neurons),
  * computes the fp32 constants on the host in fp64, and allocates the device
  * scratch for opts->batch samples.  dt > 0, tau_m != tau_s, both > 0,
- * 0 <= max_delay <= SNN_MAX_DELAY.  No device compute.  *out receives the
+ * 0 <= max_delay <= SNN_MAX_DELAY, 1 <= opts->T <= SNN_MAX_T,
+ * opts->batch x (opts->T + 1) <= 2^31.  No device compute.  *out receives the
  * handle (NULL on error); errors: SNN_EINVAL, SNN_ENOMEM, SNN_EDEVICE.
  */
 int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m, float tau_s, float theta,
@@ -208,8 +219,9 @@ int snn_forward(snn_net* net, const snn_spikes_in* in, const float* const* W, co
  *   dW, dD:   host arrays of P device pointers, [n_pre][n_post] fp32; dD is
  *             dL per step of delay.  Gradients are summed over the batch of
  *             the mean loss (so they are batch means).
- * Adjoint state is fp32; gradient sums and the jump's postsynaptic sum are
- * accumulated in fp64.  Errors: SNN_ESTATE (no successful forward),
+ * Adjoint state, trajectories, the jump's postsynaptic sum and the gradient
+ * sums are fp64; dW and dD are rounded to fp32 once, at the end.
+ * Errors: SNN_ESTATE (no successful forward),
  * SNN_EOVERFLOW (the forward overflowed its records), SNN_EINVAL, SNN_EDEVICE.
  */
 int snn_backward(snn_net* net, float* const* dW, float* const* dD);
@@ -295,6 +307,14 @@ int snn_optimizer_reset(snn_net* net);
 /* Copy the final V and I of non-input layer `layer` after the last forward
  * into (dev) [batch][n_layer] buffers. */
 int snn_get_state(const snn_net* net, int32_t layer, float* V, float* I);
+
+/* Copy I- (the synaptic current just before the threshold test, Table 1
+ * forward dynamics) of every stored spike record of LIF layer `layer` after
+ * the last forward into (dev) [batch][record_capacity] fp32, in the order of
+ * that layer's records; entries past a sample's stored count are
+ * unspecified.  These are the denominators' currents of the backward jumps.
+ * Errors: SNN_EINVAL (not a LIF layer, NULL I), SNN_ESTATE (no forward). */
+int snn_get_record_currents(const snn_net* net, int32_t layer, float* I);
 
 /* Statistics of the last forward / backward. */
 int snn_get_stats(const snn_net* net, snn_stats* out);

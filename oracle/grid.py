@@ -27,13 +27,13 @@ def _load():
                           C.POINTER(C.c_long))
         lib.oracle_constants.argtypes = [C.c_float, C.c_float, C.c_float, fp]
         lib.oracle_forward.argtypes = (
-            [C.c_int, ip, ip, ip, C.c_float, C.c_float, C.c_float, C.c_float, C.c_int,
+            [C.c_int, ip, ip, ip, C.c_float, C.c_float, C.c_float, C.c_float, C.c_int, ip,
              C.c_int, C.c_int, C.c_int, C.c_float, ip, ip, ip, fp, fp, C.c_int,
              ip, ip, ip, fp, fp, ip, fp, fp, fp, lp])
         lib.oracle_loss.argtypes = [C.c_int, C.c_int, fp, ip, fp, fp]
         lib.oracle_loss_dmse.argtypes = [C.c_int, C.c_int, fp, ip, C.c_float, fp, dp]
         lib.oracle_backward.argtypes = (
-            [C.c_int, ip, ip, ip, C.c_float, C.c_float, C.c_float, C.c_float, C.c_int,
+            [C.c_int, ip, ip, ip, C.c_float, C.c_float, C.c_float, C.c_float, C.c_int, ip,
              C.c_int, C.c_int, C.c_int, C.c_float, ip, ip, ip, fp, fp, C.c_int,
              ip, ip, ip, fp, fp, ip, dp, C.c_int, dp, dp, lp])
         for f in (lib.oracle_constants, lib.oracle_forward, lib.oracle_loss, lib.oracle_loss_dmse,
@@ -78,6 +78,7 @@ class OracleNet:
     T: int
     loss: int
     readout_scale: float
+    proj_max_delay: Optional[Sequence[int]] = None   # largest delay per projection (None: max_delay)
 
     @property
     def L(self):
@@ -88,6 +89,9 @@ class OracleNet:
         k = _i32([l[1] for l in self.layers])
         r = _i32([l[2] for l in self.layers])
         return n, k, r
+
+    def pmax(self):
+        return None if self.proj_max_delay is None else _i32(self.proj_max_delay)
 
     @property
     def n_lif(self):
@@ -148,8 +152,9 @@ def forward(net: OracleNet, in_off, in_step, in_neuron, W: Sequence[np.ndarray],
     Vt = np.zeros((B, net.T, net.n_state), np.float32) if trace else None
     stats = np.zeros(4, np.int64)
     Wf, Df = _flat(W), _flat(D)
+    pm = net.pmax()
     rc = lib.oracle_forward(net.L, _p(n, C.c_int), _p(k, C.c_int), _p(r, C.c_int),
-                            net.tau_m, net.tau_s, net.theta, net.dt, net.max_delay,
+                            net.tau_m, net.tau_s, net.theta, net.dt, net.max_delay, _p(pm, C.c_int),
                             B, net.T, net.loss, net.readout_scale,
                             _p(in_off, C.c_int), _p(in_step, C.c_int), _p(in_neuron, C.c_int),
                             _p(Wf, C.c_float), _p(Df, C.c_float), cap,
@@ -229,8 +234,9 @@ def backward(net: OracleNet, in_off, in_step, in_neuron, W: Sequence[np.ndarray]
     if dlp is not None:
         dlp = np.ascontiguousarray(dlp, dtype=np.float64)
         assert dlp.shape == (max(net.n_lif, 1), B, fwd.cap)
+    pm = net.pmax()
     rc = lib.oracle_backward(net.L, _p(n, C.c_int), _p(k, C.c_int), _p(r, C.c_int),
-                             net.tau_m, net.tau_s, net.theta, net.dt, net.max_delay,
+                             net.tau_m, net.tau_s, net.theta, net.dt, net.max_delay, _p(pm, C.c_int),
                              B, net.T, net.loss, net.readout_scale,
                              _p(in_off, C.c_int), _p(in_step, C.c_int), _p(in_neuron, C.c_int),
                              _p(Wf, C.c_float), _p(Df, C.c_float), fwd.cap,

@@ -9,7 +9,8 @@
  * What it computes (per sample; samples are independent):
  *
  *   Forward, n = 0 .. T-1, state V = I = 0 at t = 0, one delay ring
- *   R_p[S][N_post] = 0 per projection p, S = max_delay + 1:
+ *   R_p[S][N_post] = 0 per projection p, S = max_delay + 1 (at least the
+ *   projection's largest delay + 1; the ring depth does not change results):
  *     1. every non-input neuron: V- = fma(alpha, V, gamma*I), I- = beta*I
  *        (n = 0: V- = I- = 0).  alpha = e^{-dt/tau_m}, beta = e^{-dt/tau_s},
  *        gamma = tau_s/(tau_s - tau_m) (beta - alpha): the exact solution of
@@ -53,14 +54,17 @@
  *   delay gradients of Table 1 / the Methods, with the post adjoints taken at
  *   the delayed arrival time.
  *
- * mode 0 runs the backward in fp64 with fp64 constants (the definition).
- * mode 1 rounds every backward operation to fp32 exactly as the HIP kernels
- * do, the kernel-precision model: fp32 state and products, each sample's
- * SU/SD terms summed in fp32 in spike order, the per-sample sums then added
- * over the batch in fp64 in sample order, and the jump's postsynaptic sum A
- * in fp64.
+ * mode 0 runs the backward in fp64 with fp64 constants: the definition the
+ * parity tests judge against.
+ * mode 1 rounds every backward operation to fp32, in the order written above
+ * (the batch sums SU, SD and the jump's postsynaptic sum A included): how far
+ * an fp32 evaluation of the same expressions lands from the fp64 one, a noise
+ * floor reported beside the parity results.
  * The forward is fp32 with no contraction in both modes: spike decisions are
- * taken in the kernel's precision.
+ * taken in fp32, the precision of the forward pass.
+ *
+ * Delays: slot = rint(D) (half to even) clamped to [0, pmax[p]] per
+ * projection p (pmax NULL: max_delay for every projection), NaN -> 0.
  */
 #include <math.h>
 #include <stdint.h>
@@ -142,6 +146,21 @@ static int delay_slot(float d, int max_delay, long* clamped) {
     return (int)r;
 }
 
+/* Slots of every synapse, projection by projection (pmax: largest delay per
+ * projection, or NULL for max_delay everywhere); returns OR_EINVAL if a
+ * pmax entry lies outside [0, max_delay]. */
+static int fill_slots(const topo_t* t, const float* D, int max_delay, const int* pmax,
+                      unsigned char* slot, long* clamped) {
+    for (int p = 0; p < t->P; ++p) {
+        const int dm = pmax ? pmax[p] : max_delay;
+        if (dm < 0 || dm > max_delay) return OR_EINVAL;
+        const long n_p = (long)t->n[t->pre[p]] * t->n[t->post[p]];
+        for (long k = 0; k < n_p; ++k)
+            slot[t->w_off[p] + k] = (unsigned char)delay_slot(D[t->w_off[p] + k], dm, clamped);
+    }
+    return OR_OK;
+}
+
 int oracle_constants(float tau_m, float tau_s, float dt, float* out4) {
     if (!(dt > 0.0f) || !(tau_m > 0.0f) || !(tau_s > 0.0f) || tau_m == tau_s) return OR_EINVAL;
     double a = exp(-(double)dt / (double)tau_m);
@@ -181,7 +200,7 @@ static int check_inputs(const topo_t* t, int B, int T, const int* in_off, const 
  * produced more than cap spikes in some layer; counts are still exact.
  */
 int oracle_forward(int L, const int* n, const int* kind, const int* rec,
-                   float tau_m, float tau_s, float theta, float dt, int max_delay,
+                   float tau_m, float tau_s, float theta, float dt, int max_delay, const int* pmax,
                    int B, int T, int loss, float readout_scale,
                    const int* in_off, const int* in_step, const int* in_neuron,
                    const float* W, const float* D, int cap,
@@ -224,7 +243,10 @@ int oracle_forward(int L, const int* n, const int* kind, const int* rec,
         free(slot); free(V); free(I); free(ring); free(spk); free(acc); free(best); free(first);
         return OR_ENOMEM;
     }
-    for (long k = 0; k < t.n_params; ++k) slot[k] = (unsigned char)delay_slot(D[k], max_delay, &clamped);
+    if (fill_slots(&t, D, max_delay, pmax, slot, &clamped)) {
+        free(slot); free(V); free(I); free(ring); free(spk); free(acc); free(best); free(first);
+        return OR_EINVAL;
+    }
 
     int overflow = 0;
     for (int b = 0; b < B; ++b) {
@@ -400,7 +422,7 @@ static inline double rnd(int f32, double x) { return f32 ? (double)(float)x : x;
  * stats[0] = degenerate crossings (I- <= theta) whose jump was skipped.
  */
 int oracle_backward(int L, const int* n, const int* kind, const int* rec,
-                    float tau_m, float tau_s, float theta, float dt, int max_delay,
+                    float tau_m, float tau_s, float theta, float dt, int max_delay, const int* pmax,
                     int B, int T, int loss, float readout_scale,
                     const int* in_off, const int* in_step, const int* in_neuron,
                     const float* W, const float* D, int cap,
@@ -444,19 +466,14 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
     double* H = (double*)malloc(sizeof(double) * 2 * (size_t)T * t.n_state);
     double* A = (double*)malloc(sizeof(double) * t.n_state);
     double* src = (double*)malloc(sizeof(double) * C);
-    /* per-sample partial sums (fp32 model) */
-    double* PU = (double*)calloc((size_t)t.n_params, sizeof(double));
-    double* PD = (double*)calloc((size_t)t.n_params, sizeof(double));
-    if (!slot || !SU || !SD || !lv || !lI || !H || !A || !src || !PU || !PD) {
+    if (!slot || !SU || !SD || !lv || !lI || !H || !A || !src) {
         free(slot); free(SU); free(SD); free(lv); free(lI); free(H); free(A); free(src);
-        free(PU); free(PD);
         return OR_ENOMEM;
     }
-    (void)max_delay;
-    for (long k = 0; k < t.n_params; ++k) slot[k] = (unsigned char)delay_slot(D[k], max_delay, &clamped);
-    /* f64: terms go straight into the batch sums; f32: into per-sample fp32 sums */
-    double* TU = f32 ? PU : SU;
-    double* TD = f32 ? PD : SD;
+    if (fill_slots(&t, D, max_delay, pmax, slot, &clamped)) {
+        free(slot); free(SU); free(SD); free(lv); free(lI); free(H); free(A); free(src);
+        return OR_EINVAL;
+    }
 
     int rec_hi[OR_MAXL];
     for (int b = 0; b < B; ++b) {
@@ -515,9 +532,9 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
                         if (m > T - 1) continue;
                         const double* hv = H + 2 * ((size_t)m * t.n_state + t.st_off[q] + j);
                         const double d = rnd(f32, hv[1] - hv[0]);
-                        Ai -= rnd(f32, (double)W[row + j] * d);
+                        Ai = rnd(f32, Ai - rnd(f32, (double)W[row + j] * d));
                     }
-                    A[t.st_off[a] + i] += Ai;
+                    A[t.st_off[a] + i] = rnd(f32, A[t.st_off[a] + i] + Ai);
                 }
             }
             for (int l = 1; l < L; ++l) {
@@ -527,8 +544,8 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
                     const int s = t.st_off[l] + rec_neuron[base + k];
                     const double den = rnd(f32, (double)rec_I[base + k] - (double)theta);
                     if (den > 0.0) {
-                        double num = (double)theta * lv[s] + A[s];
-                        if (rec_dlp) num += rec_dlp[base + k];
+                        double num = rnd(f32, rnd(f32, (double)theta * lv[s]) + A[s]);
+                        if (rec_dlp) num = rnd(f32, num + rec_dlp[base + k]);
                         lv[s] = rnd(f32, lv[s] + rnd(f32, num / den));
                     } else {
                         ++degenerate;
@@ -554,17 +571,9 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
                     const double v = hv[0], u = hv[1];
                     const double d = rnd(f32, u - v);
                     const double wd = rnd(f32, (double)W[row + j] * d);
-                    TU[row + j] = rnd(f32, TU[row + j] + u);
-                    TD[row + j] = rnd(f32, TD[row + j] + wd);
+                    SU[row + j] = rnd(f32, SU[row + j] + u);
+                    SD[row + j] = rnd(f32, SD[row + j] + wd);
                 }
-            }
-        }
-        if (f32) {
-            for (long k = 0; k < t.n_params; ++k) {
-                SU[k] += PU[k];
-                SD[k] += PD[k];
-                PU[k] = 0.0;
-                PD[k] = 0.0;
             }
         }
     }
@@ -574,6 +583,5 @@ int oracle_backward(int L, const int* n, const int* kind, const int* rec,
     }
     if (stats) stats[0] = degenerate;
     free(slot); free(SU); free(SD); free(lv); free(lI); free(H); free(A); free(src);
-    free(PU); free(PD);
     return OR_OK;
 }

@@ -35,7 +35,8 @@ class snn_layer(C.Structure):
 class snn_opts(C.Structure):
     _fields_ = [("batch", C.c_int32), ("T", C.c_int32), ("loss", C.c_int32),
                 ("readout_scale", C.c_float), ("record_capacity", C.c_int32),
-                ("flags", C.c_int32), ("hip_stream", C.c_void_p), ("dmse_delta", C.c_float)]
+                ("flags", C.c_int32), ("hip_stream", C.c_void_p), ("dmse_delta", C.c_float),
+                ("proj_max_delay", C.c_void_p)]
 
 
 class snn_spikes_in(C.Structure):
@@ -97,6 +98,7 @@ def load_library():
                                        C.POINTER(P), C.POINTER(P)]
     lib.snn_optimizer_reset.argtypes = [P]
     lib.snn_get_state.argtypes = [P, C.c_int32, P, P]
+    lib.snn_get_record_currents.argtypes = [P, C.c_int32, P]
     lib.snn_get_stats.argtypes = [P, C.POINTER(snn_stats)]
     lib.snn_last_error.argtypes = [P]
     lib.snn_last_error.restype = C.c_char_p
@@ -104,7 +106,7 @@ def load_library():
     lib.snn_destroy.restype = None
     for f in ("snn_create", "snn_num_projections", "snn_projection_info", "snn_forward",
               "snn_backward", "snn_backward_lp", "snn_backward_noalloc", "snn_optimizer_step", "snn_optimizer_reset", "snn_get_state",
-              "snn_get_stats"):
+              "snn_get_record_currents", "snn_get_stats"):
         getattr(lib, f).restype = C.c_int
     _lib = lib
     return lib
@@ -137,7 +139,7 @@ class Network:
     def __init__(self, layers: Sequence[Tuple[int, int, int]], tau_m: float, tau_s: float,
                  theta: float, dt: float, max_delay: int, batch: int, T: int, loss: int,
                  readout_scale: float, record_capacity: int, flags: int = 0, stream=None,
-                 dmse_delta: float = 0.0):
+                 dmse_delta: float = 0.0, proj_max_delay: Optional[Sequence[int]] = None):
         import torch
         self._lib = load_library()
         self.layers = [tuple(int(x) for x in l) for l in layers]
@@ -148,8 +150,12 @@ class Network:
             stream = torch.cuda.current_stream()
         self.stream = stream
         arr = (snn_layer * len(layers))(*[snn_layer(*l) for l in self.layers])
+        self.proj_max_delay = None if proj_max_delay is None else [int(x) for x in proj_max_delay]
+        pmd = (C.c_int32 * len(self.proj_max_delay))(*self.proj_max_delay) \
+            if self.proj_max_delay is not None else None
         opts = snn_opts(self.batch, self.T, int(loss), float(readout_scale), self.record_capacity,
-                        int(flags), C.c_void_p(stream.cuda_stream), float(dmse_delta))
+                        int(flags), C.c_void_p(stream.cuda_stream), float(dmse_delta),
+                        C.cast(pmd, C.c_void_p) if pmd is not None else None)
         h = C.c_void_p()
         rc = self._lib.snn_create(arr, len(layers), tau_m, tau_s, theta, dt, int(max_delay),
                                   C.byref(opts), C.byref(h))
@@ -281,6 +287,14 @@ class Network:
         import torch
         rc = self._lib.snn_get_state(self._h, int(layer), _ptr(V, torch.float32, "V"),
                                      _ptr(I, torch.float32, "I"))
+        return self._check(rc)
+
+    def record_currents(self, layer: int, I):
+        """I- of every stored record of LIF layer `layer`: fp32 [B][cap] device tensor."""
+        import torch
+        if I.numel() != self.batch * self.record_capacity:
+            raise ValueError("I must hold B x record_capacity elements")
+        rc = self._lib.snn_get_record_currents(self._h, int(layer), _ptr(I, torch.float32, "I"))
         return self._check(rc)
 
     def stats(self) -> dict:

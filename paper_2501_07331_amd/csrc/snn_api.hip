@@ -54,6 +54,7 @@ size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
 struct snn_net {
     Topo t;
     float tau_m, tau_s, theta, dt;
+    double alpha64, beta64, cc64;   // backward propagators, fp64
     float dmse_delta;
     int max_delay;
     int core_threads;           // LIF-core workgroup size
@@ -62,6 +63,7 @@ struct snn_net {
     int mask_off, scan_tb, table_lds;
     int bpart_off;              // backward-core LDS plan
     int bring_mode[SNN_MAX_LAYERS];   // adjoint ring of a LIF layer: -2 none, -1 HBM, >= 0 LDS
+                                      // byte offset
     int radj_threads, radj_tab;
     int grad_J, grad_TW, grad_KL, grad_threads, grad_SB, grad_bs, grad_nblk, grad_ngroups, grad_spcap;
     GradGroup grad_grp[SNN_MAX_LAYERS];
@@ -79,7 +81,7 @@ struct snn_net {
     int* in_idx;
     float* A_in;
     float* fring[SNN_MAXP];
-    float* bring[SNN_MAX_LAYERS];
+    double* bring[SNN_MAX_LAYERS];
     int* rec_n;
     int* rec_s;
     float* rec_I;
@@ -89,14 +91,12 @@ struct snn_net {
     int* rec_gstep;
     float* z;
     int* nstar;
-    float* src;
+    double* src;
     float* Vf;
     float* If;
     float* table;
-    float* tu_lif;
-    float* td_lif;
-    float* tu_out;
-    float* td_out;
+    double2* tr_lif;            // adjoint trajectories (lambda_I, lambda_I - lambda_V) [B][T][N]
+    double2* tr_out;
     double* A2;
     double* gpart;
     float* mom;                 // Adam moments [4][n_params], allocated by the first Adam step
@@ -143,8 +143,8 @@ static int fail(snn_net* net, int code, const char* fmt, ...) {
 static void free_all(snn_net* n) {
     void* bufs[] = {n->slot,    n->in_idx,  n->A_in,     n->rec_n,     n->rec_s,  n->rec_I,
                     n->rec_idx, n->rec_cnt, n->rec_goff, n->rec_gstep, n->z,      n->nstar,
-                    n->src,     n->Vf,      n->If,       n->table,     n->tu_lif, n->td_lif,
-                    n->tu_out,  n->td_out,  n->A2,       n->in_goff,   n->in_gstep, n->st,
+                    n->src,     n->Vf,      n->If,       n->table,     n->tr_lif, n->tr_out,
+                    n->A2,       n->in_goff,   n->in_gstep, n->st,
                     n->gpart,   n->ws,      n->steptab, n->mom,   n->xlp_out};
     for (void* p : bufs)
         if (p) (void)hipFree(p);
@@ -203,8 +203,8 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     }
     // the kernels hold per-LIF-layer state for at most SNN_MAX_LIF layers
     if (dmse && n_layers - 1 > SNN_MAX_LIF) return SNN_EINVAL;
-    // the gradient kernel stages (lambda_I, lambda_I - lambda_V) of T steps in LDS
-    if ((size_t)opts->T * 2 * sizeof(float) > kLds) return SNN_EINVAL;
+    // spike steps are staged as 16-bit values in the gradient pass
+    if (opts->T > SNN_MAX_T) return SNN_EINVAL;
     if ((long long)opts->batch * (opts->T + 1) > (1LL << 31)) return SNN_EINVAL;
 
     snn_net* net = (snn_net*)calloc(1, sizeof(snn_net));
@@ -213,7 +213,7 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     t.L = n_layers;
     t.B = opts->batch;
     t.T = opts->T;
-    t.S = max_delay + 1;
+    t.S = max_delay + 1;     // per projection below
     t.cap = opts->record_capacity;
     t.loss = opts->loss;
     t.n_in = layers[0].n;
@@ -228,6 +228,9 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     t.beta = (float)bb;
     t.gamma = (float)((double)tau_s / ((double)tau_s - (double)tau_m) * (bb - a));
     t.cc = (float)((double)tau_m / ((double)tau_m - (double)tau_s) * (a - bb));
+    net->alpha64 = a;
+    net->beta64 = bb;
+    net->cc64 = (double)tau_m / ((double)tau_m - (double)tau_s) * (a - bb);
     net->tau_m = tau_m;
     net->tau_s = tau_s;
     net->theta = theta;
@@ -273,6 +276,22 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     net->n_params = off;
     t.out_p = t.P - 1;
     const int C = t.n[t.out_l];
+    // delay rings as deep as each projection's largest delay
+    for (int p = 0; p < t.P; ++p) {
+        const int dm = opts->proj_max_delay ? opts->proj_max_delay[p] : max_delay;
+        if (dm < 0 || dm > max_delay) {
+            snprintf(g_create_err, sizeof(g_create_err),
+                     "snn_create: proj_max_delay[%d] = %d outside [0, max_delay = %d]", p, dm, max_delay);
+            free(net);
+            return SNN_EINVAL;
+        }
+        t.dmax[p] = dm;
+        t.Sp[p] = dm + 1;
+    }
+    for (int l = 0; l < n_layers; ++l) t.Sb[l] = 0;
+    for (int p = 0; p < t.P; ++p)
+        if (t.pre[p] != 0 && t.kind[t.post[p]] == SNN_LIF)
+            t.Sb[t.post[p]] = std::max(t.Sb[t.post[p]], t.Sp[p]);
 
     // ---- LDS plans
     int maxlif = 0;
@@ -288,7 +307,7 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         for (int p = 0; p < t.P; ++p) {
             if (t.pre[p] == 0 || t.kind[t.post[p]] != SNN_LIF) continue;
             t.fring[p] = (int)(used / sizeof(float));
-            used += (size_t)(t.S + 1) * t.n[t.post[p]] * sizeof(float);
+            used += (size_t)(t.Sp[p] + 1) * t.n[t.post[p]] * sizeof(float);
         }
         const bool rings_lds = !(hbm || used + masks > kLds);
         if (!rings_lds) {
@@ -298,9 +317,9 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         net->mask_off = (int)align16(used);
         net->lds_core_f = net->mask_off + masks;
     }
-    // backward core: partial jump sums [2][NL][KP][4 NW] and the adjoint
-    // rings of the LIF layers read by LIF-pre projections (all in LDS, or all
-    // in HBM)
+    // backward core: partial jump sums [2][NL][KP][4 NW] and the fp64 adjoint
+    // rings [Sb][n] of the LIF layers read by LIF-pre projections (all in
+    // LDS, or all in HBM)
     bool read_by_lif[SNN_MAX_LAYERS] = {false};
     for (int p = 0; p < t.P; ++p)
         if (t.pre[p] != 0 && t.kind[t.post[p]] == SNN_LIF) read_by_lif[t.post[p]] = true;
@@ -314,8 +333,8 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         for (int l = 0; l < n_layers; ++l) {
             net->bring_mode[l] = -2;
             if (!read_by_lif[l]) continue;
-            const size_t bytes = (size_t)t.S * t.n[l] * sizeof(float);
-            net->bring_mode[l] = (int)(used / sizeof(float));
+            const size_t bytes = align16((size_t)t.Sb[l] * t.n[l] * sizeof(double));
+            net->bring_mode[l] = (int)used;
             used += bytes;
         }
         if (used > kLds) all_lds = false;
@@ -331,8 +350,8 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     // input scan ring: S + TB - 1 arrival steps and a dummy row per 64-post
     // wave; TB as large as keeps four rings in one CU's LDS (40 KiB each),
     // at least 8
-    net->scan_tb = std::max(8, std::min(64, 160 - t.S));
-    net->lds_scan = (size_t)(t.S + net->scan_tb) * 64 * sizeof(float);
+    net->scan_tb = std::max(8, std::min(64, 160 - t.Sp[0]));
+    net->lds_scan = (size_t)(t.Sp[0] + net->scan_tb) * 64 * sizeof(float);
     // readout forward: arrival table [T + 1][C] (row T: dummy) in LDS when it fits
     // readout: groups of ceil(C / 64) waves, each building a window of the
     // arrival table; up to 1024 threads
@@ -350,35 +369,26 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
             net->lds_read = 0;
         }
     }
-    // readout adjoint: the [T][C] table of lambda_I - lambda_V in LDS when it fits
+    // readout adjoint: the [T][C] table of lambda_I - lambda_V (fp64) in LDS when it fits
     net->radj_threads = std::min(1024, std::max(256, ((C + 63) / 64) * 64));
-    net->radj_tab = (!hbm && (size_t)t.T * C * sizeof(float) <= kLds) ? 1 : 0;
-    net->lds_radj = net->radj_tab ? (size_t)t.T * C * sizeof(float) : 0;
+    net->radj_tab = (!hbm && (size_t)t.T * C * sizeof(double) <= kLds) ? 1 : 0;
+    net->lds_radj = net->radj_tab ? (size_t)t.T * C * sizeof(double) : 0;
     // gradients: one group per post layer (its projections in projection
     // order), J posts per workgroup, samples split into SB blocks so that the
     // grid has about 512 workgroups; workgroups in units of 4 J-blocks.  LDS:
-    // the J trajectories of a sample [J][T] float2 (J = 8 within 64 KiB, then
-    // room for the sample's spike steps (16-bit) up to 96 KiB in all; for
-    // longer trials J = 4 within 128 KiB and the rest of the LDS for the spike
-    // steps; longer still, J = 8 and windows of 1024 steps)
-    size_t grad_total = 96 * 1024;
+    // the J trajectories of a sample [J][T] double2, J = 8, 4 or 2 within
+    // 128 KiB (longer trials: J = 8 in windows of 1024 steps), and the rest of
+    // the LDS for the sample's spike steps (16-bit)
+    const size_t grad_total = kLds;
     {
-        const size_t tj = (size_t)t.T * 2 * sizeof(float);
-        auto pick = [&](size_t cap) {
-            for (int j : {8, 4, 2})
-                if (j * tj <= cap) return j;
-            return 1;
-        };
-        net->grad_J = pick(64 * 1024);
+        const size_t tj = (size_t)t.T * sizeof(double2);
+        net->grad_J = 0;
         net->grad_TW = t.T;
-        if (net->grad_J < 8) {
-            net->grad_J = pick(128 * 1024);
-            grad_total = kLds;
-            if (net->grad_J < 4) {
-                net->grad_J = 8;
-                net->grad_TW = 1024;
-                grad_total = 96 * 1024;
-            }
+        for (int j : {8, 4, 2})
+            if (!net->grad_J && j * tj <= 128 * 1024) net->grad_J = j;
+        if (!net->grad_J) {
+            net->grad_J = 8;
+            net->grad_TW = 1024;
         }
         const int J = net->grad_J;
         int ng = 0, jblocks = 0, maxpre = 64;
@@ -418,7 +428,7 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         const int pairs = J * maxpre;
         net->grad_KL = (pairs <= 4 * 1024) ? 4 : 8;
         net->grad_threads = std::min(1024, ((pairs + net->grad_KL - 1) / net->grad_KL + 63) / 64 * 64);
-        const size_t traj = (size_t)J * net->grad_TW * 2 * sizeof(float);
+        const size_t traj = (size_t)J * net->grad_TW * sizeof(double2);
         const size_t room = (traj < grad_total) ? grad_total - traj : 0;
         net->grad_spcap = (int)(room / sizeof(unsigned short)) & ~7;
         net->lds_grad = traj + (size_t)net->grad_spcap * sizeof(unsigned short);
@@ -438,9 +448,9 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     ALLOC(net->A_in, B * T * t.n[1]);
     for (int p = 0; p < t.P; ++p)
         if (t.pre[p] != 0 && t.kind[t.post[p]] == SNN_LIF && t.fring[p] < 0)
-            ALLOC(net->fring[p], B * (t.S + 1) * t.n[t.post[p]]);
+            ALLOC(net->fring[p], B * (t.Sp[p] + 1) * t.n[t.post[p]]);
     for (int l = 1; l < n_layers; ++l)
-        if (net->bring_mode[l] == -1) ALLOC(net->bring[l], B * t.S * t.n[l]);
+        if (net->bring_mode[l] == -1) ALLOC(net->bring[l], B * t.Sb[l] * t.n[l]);
     ALLOC(net->rec_n, nl * B * cap);
     ALLOC(net->rec_s, nl * B * cap);
     ALLOC(net->rec_I, nl * B * cap);
@@ -454,10 +464,8 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     ALLOC(net->Vf, B * so);
     ALLOC(net->If, B * so);
     if (net->table_lds < 0) ALLOC(net->table, B * (T + 1) * C);
-    ALLOC(net->tu_lif, B * T * t.lif_total);
-    ALLOC(net->td_lif, B * T * t.lif_total);
-    ALLOC(net->tu_out, B * T * C);
-    ALLOC(net->td_out, B * T * C);
+    ALLOC(net->tr_lif, B * T * t.lif_total);
+    ALLOC(net->tr_out, B * T * C);
     if (net->grad_SB > 1) ALLOC(net->gpart, (size_t)net->grad_SB * 2 * (size_t)net->n_params);
     if (feed != 0 && !t.out_lif) ALLOC(net->A2, B * cap);
     if (t.out_lif) ALLOC(net->xlp_out, B * cap);
@@ -572,13 +580,13 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
     HIP_TRY(net, launch_validate(in->offsets, in->step, in->neuron, in->nnz, t.B, t.T, t.n_in, labels,
                                  C, net->st, s));
     HIP_TRY(net, launch_step_index(in->offsets, in->step, t.B, t.T, net->in_idx, net->st, s));
-    HIP_TRY(net, launch_round_delays(D, W, t.woff, net->cnt, t.P, net->max_delay, net->slot, net->ws,
+    HIP_TRY(net, launch_round_delays(D, W, t.woff, net->cnt, t.P, t.dmax, net->slot, net->ws,
                                      net->st, s));
 
     InScanArgs sa{};
     sa.B = t.B;
     sa.T = t.T;
-    sa.S = t.S;
+    sa.S = t.Sp[0];
     sa.n_in = t.n_in;
     sa.n1 = t.n[1];
     sa.TB = net->scan_tb;
@@ -594,7 +602,6 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
         CoreFwdArgs a{};
         a.B = t.B;
         a.T = t.T;
-        a.S = t.S;
         a.cap = t.cap;
         a.NW = net->core_threads / 64;
         a.n1 = t.n[1];
@@ -631,6 +638,7 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
                 if (t.pre[p] != l || t.kind[q] != SNN_LIF) continue;
                 y.nq[y.npost] = t.n[q];
                 y.npre[y.npost] = t.n[l];
+                y.S[y.npost] = t.Sp[p];
                 y.ring_lds[y.npost] = t.fring[p];
                 y.ring[y.npost] = net->fring[p];
                 y.ws[y.npost] = net->ws + t.woff[p];
@@ -643,6 +651,7 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
                     if (t.pre[p] == 0 || t.kind[q] != SNN_LIF) continue;
                     y.nq[k] = t.n[q];
                     y.npre[k] = t.n[t.pre[p]];
+                    y.S[k] = t.Sp[p];
                     y.ring_lds[k] = t.fring[p];
                     y.ring[k] = net->fring[p];
                     y.ws[k] = net->ws + t.woff[p];
@@ -814,9 +823,9 @@ static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW
         r.C = C;
         r.cap = t.cap;
         r.loss = t.loss;
-        r.alpha = t.alpha;
-        r.beta = t.beta;
-        r.cc = t.cc;
+        r.alpha = net->alpha64;
+        r.beta = net->beta64;
+        r.cc = net->cc64;
         r.ws = net->ws + t.woff[t.out_p];
         if (feed != 0) {
             const size_t li = (size_t)t.lif[feed];
@@ -826,8 +835,7 @@ static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW
         }
         r.nstar = net->nstar;
         r.src = net->src;
-        r.tu = net->tu_out;
-        r.td = net->td_out;
+        r.traj = net->tr_out;
         r.A2 = net->A2;
         r.tab_lds = net->radj_tab;
         TIMED(net, K_RADJ, launch_readout_adjoint(r, net->radj_threads, net->lds_radj, s));
@@ -852,20 +860,20 @@ static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW
         CoreBwdArgs a{};
         a.B = t.B;
         a.T = t.T;
-        a.S = t.S;
         a.cap = t.cap;
         a.NW = net->core_threads / 64;
         a.lif_total = t.lif_total;
-        a.alpha = t.alpha;
-        a.beta = t.beta;
-        a.cc = t.cc;
-        a.theta = t.theta;
+        a.alpha = net->alpha64;
+        a.beta = net->beta64;
+        a.cc = net->cc64;
+        a.theta = (double)t.theta;
         for (int l = 1; l < t.L; ++l) {
             if (t.kind[l] != SNN_LIF) continue;
             const size_t li = (size_t)t.lif[l];
             BwdLayer& y = a.ly[li];
             y.n = t.n[l];
             y.lif_off = t.lif_off[l];
+            y.S = std::max(t.Sb[l], 1);
             y.ring_lds = net->bring_mode[l];
             y.ring = net->bring[l];
             for (int p = 0; p < t.P; ++p) {
@@ -874,6 +882,7 @@ static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW
                 y.ws[y.npost] = net->ws + t.woff[p];
                 y.nq[y.npost] = t.n[q];
                 y.npre[y.npost] = t.n[l];
+                y.qS[y.npost] = t.Sb[q];
                 y.qring_lds[y.npost] = net->bring_mode[q] >= 0 ? net->bring_mode[q] : -1;
                 y.qring[y.npost] = net->bring[q];
                 ++y.npost;
@@ -886,6 +895,7 @@ static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW
                     y.ws[k] = net->ws + t.woff[p];
                     y.nq[k] = t.n[q];
                     y.npre[k] = t.n[t.pre[p]];
+                    y.qS[k] = t.Sb[q];
                     y.qring_lds[k] = net->bring_mode[q] >= 0 ? net->bring_mode[q] : -1;
                     y.qring[k] = net->bring[q];
                 }
@@ -895,8 +905,7 @@ static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW
             y.steptab = net->steptab + li * B * (size_t)t.T * SNN_STEP_ROW;
             y.A2 = jump_x[li];
         }
-        a.tu = net->tu_lif;
-        a.td = net->td_lif;
+        a.traj = net->tr_lif;
         a.st = net->st;
         a.part_off = net->bpart_off;
         TIMED(net, K_BCORE,
@@ -917,10 +926,8 @@ static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW
     ga.tau_s = t.tau_s;
     ga.dt = t.dt;
     ga.nparams = net->n_params;
-    ga.tu_lif = net->tu_lif;
-    ga.td_lif = net->td_lif;
-    ga.tu_out = net->tu_out;
-    ga.td_out = net->td_out;
+    ga.tr_lif = net->tr_lif;
+    ga.tr_out = net->tr_out;
     for (int p = 0; p < t.P; ++p) {
         ga.woff[p] = t.woff[p];
         ga.dW[p] = dW[p];
@@ -1055,6 +1062,20 @@ extern "C" int snn_get_state(const snn_net* net, int32_t layer, float* V, float*
                                  net->stream));
     HIP_TRY(m, launch_copy_state(net->If, net->n_state, net->st_off[layer], t.n[layer], t.B, I,
                                  net->stream));
+    HIP_TRY(m, hipStreamSynchronize(net->stream));
+    return SNN_OK;
+}
+
+extern "C" int snn_get_record_currents(const snn_net* net, int32_t layer, float* I) {
+    if (!net || layer < 1 || layer >= net->t.L || net->t.kind[layer] != SNN_LIF || !I)
+        return SNN_EINVAL;
+    if (!net->fwd_ok) return SNN_ESTATE;
+    snn_net* m = const_cast<snn_net*>(net);
+    const Topo& t = net->t;
+    const size_t n = (size_t)t.B * t.cap;
+    if (n == 0) return SNN_OK;
+    HIP_TRY(m, hipMemcpyAsync(I, net->rec_I + (size_t)t.lif[layer] * n, n * sizeof(float),
+                              hipMemcpyDeviceToDevice, net->stream));
     HIP_TRY(m, hipStreamSynchronize(net->stream));
     return SNN_OK;
 }

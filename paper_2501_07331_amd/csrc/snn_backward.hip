@@ -12,17 +12,21 @@
 //                   forward's per-step masks, so the weights and slots of a
 //                   step's spikes, their I- and readout jump parts are
 //                   loaded one step ahead; the per-step chain is then LDS and
-//                   ALU work only: free dynamics, trajectory tile, adjoint
+//                   ALU work only: free dynamics, trajectory row, adjoint
 //                   ring, delayed postsynaptic sums, one barrier, jumps.
 //  group            spikes of every sample grouped by presynaptic neuron.
 //  gradients        workgroup = (post layer, block of J posts, block of
 //                   samples): lanes over the presynaptic neurons of every
 //                   projection into the layer; per sample the J post
 //                   trajectories are staged in LDS and each lane sums, over
-//                   its spikes in step order, lambda_I and w (lambda_I -
-//                   lambda_V) at the delayed arrivals in fp32, then adds the
-//                   sample's sums in fp64.  Sample blocks are reduced in a
-//                   fixed order: no atomics, deterministic.
+//                   its spikes in step order, lambda_I and lambda_I -
+//                   lambda_V at the delayed arrivals.  Sample blocks are
+//                   reduced in a fixed order: no atomics, deterministic.
+//
+// The whole backward pass is fp64 (constants, adjoints, trajectories, rings,
+// jump sums, gradient sums): the adjoints are amplified through small jump
+// denominators I- - theta, and fp32 state there moves some gradients by
+// percents from the exact (fp64) result on the audio-sized networks.
 #include "snn_device.h"
 
 namespace {
@@ -33,35 +37,33 @@ namespace {
 // lambda_V (old lambda_V in both), then the step's loss source; the "+"
 // values before the source are the trajectory.  Then every thread takes
 // spikes (n, i) of the feeding LIF layer: A2 = sum_k w_ik (lambda_V -
-// lambda_I)_k at step n + slot_ik, fp64 over k ascending.
+// lambda_I)_k at step n + slot_ik, over k ascending.  All fp64.
 __global__ void __launch_bounds__(1024) readout_adjoint_kernel(ReadoutBwdArgs a) {
     const int b = blockIdx.x, tid = threadIdx.x;
     const int C = a.C, T = a.T;
-    lds_f32* tab = (lds_f32*)smem;                                // [T][C] lambda_I - lambda_V
+    lds_f64* tab = (lds_f64*)smem;                                // [T][C] lambda_I - lambda_V
     if (tid < C) {
-        const float srcv = a.src[(size_t)b * C + tid];
+        const double srcv = a.src[(size_t)b * C + tid];
         const int nst = a.nstar[(size_t)b * C + tid];
-        global_f32* tu = (global_f32*)(a.tu + (size_t)b * T * C + tid);
-        global_f32* td = (global_f32*)(a.td + (size_t)b * T * C + tid);
-        float lv = 0.0f, lI = 0.0f;
+        double2* tr = a.traj + (size_t)b * T * C + tid;
+        double lv = 0.0, lI = 0.0;
         for (int n = T - 1; n >= 0; --n) {
             if (n <= T - 2) {
-                const float v = lv;
-                lI = __fadd_rn(__fmul_rn(a.beta, lI), __fmul_rn(a.cc, v));
-                lv = __fmul_rn(a.alpha, v);
+                const double v = lv;
+                lI = __dadd_rn(__dmul_rn(a.beta, lI), __dmul_rn(a.cc, v));
+                lv = __dmul_rn(a.alpha, v);
             }
-            const float d = __fsub_rn(lI, lv);
-            tu[(size_t)n * C] = lI;
-            td[(size_t)n * C] = d;
+            const double d = __dsub_rn(lI, lv);
+            tr[(size_t)n * C] = make_double2(lI, d);
             if (a.tab_lds) tab[n * C + tid] = d;
-            if (a.loss == SNN_LOSS_CE_SUM || nst == n) lv = __fsub_rn(lv, srcv);
+            if (a.loss == SNN_LOSS_CE_SUM || nst == n) lv = __dsub_rn(lv, srcv);
         }
     }
     if (!a.rec_n) return;
     __syncthreads();
     const int cnt = a.rec_cnt[b];
     const size_t base = (size_t)b * a.cap;
-    const float* tdb = a.td + (size_t)b * T * C;
+    const double2* trb = a.traj + (size_t)b * T * C;
     for (int r = tid; r < cnt; r += blockDim.x) {
         const int i = a.rec_n[base + r], n = a.rec_s[base + r];
         const uint2* wsr = a.ws + (size_t)i * C;
@@ -72,17 +74,17 @@ __global__ void __launch_bounds__(1024) readout_adjoint_kernel(ReadoutBwdArgs a)
             uint2 e[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) e[u] = wsr[min(k0 + u, C - 1)];
-            float d[4];
+            double d[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int k = min(k0 + u, C - 1);
                 const int m = min(n + (int)e[u].y, T - 1);
-                d[u] = a.tab_lds ? (float)tab[m * C + k] : tdb[(size_t)m * C + k];
+                d[u] = a.tab_lds ? (double)tab[m * C + k] : trb[(size_t)m * C + k].y;
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u)
                 if (k0 + u < C && n + (int)e[u].y <= T - 1)
-                    acc -= (double)__fmul_rn(__uint_as_float(e[u].x), d[u]);
+                    acc = __dsub_rn(acc, __dmul_rn((double)__uint_as_float(e[u].x), d[u]));
         }
         a.A2[base + r] = acc;
     }
@@ -124,7 +126,7 @@ struct BwdState {
     int id3[NL][KP];
     uint2 ws[NL][NPA][KP];        //   (weight bits, slot) of the LIF-post projections, this lane's post
     int mine[NL];                 //   1 + position of this lane's neuron among id3[0 .. KP), 0: none
-    float I[NL];                  //   I- and readout jump part of this lane's spike (raw)
+    float I[NL];                  //   I- (fp32 record) and extra jump numerator of this lane's spike
     double A2[NL];
 };
 
@@ -225,44 +227,44 @@ struct BwdCore {
 
     // Delayed postsynaptic sums of spikes ids[q0 .. q0 + 4) (valid for q < cnt)
     // of layer l, reduced per 16-lane row into part_l[q][wave * 4 + row].
+    // n_mod[pp]: n modulo the adjoint-ring slots of projection pp's post layer.
     static __device__ __forceinline__ void gather4(const CoreBwdArgs& a, int b, int tid, int n,
-                                                   int n_mod, int l, int q0, int cnt,
+                                                   const int (&n_mod)[NPA], int l, int q0, int cnt,
                                                    const int (&ids)[KP], const uint2 (&ws)[NPA][KP],
                                                    double* part_l) {
         const BwdLayer& y = a.ly[l];
         const int lane = tid & 63, wave = tid >> 6;
-        float* lds = reinterpret_cast<float*>(smem);
         // the reads of the chunk, all in bounds (masked terms read row 0,
         // column 0), issued together; the empty asm takes them as operands so
         // that the compiler keeps them unconditional (it would otherwise move
         // each read behind its own mask branch and wait for it there) and one
         // wait covers all of them; a masked term is then +0
-        float d[4][NPA];
+        double d[4][NPA];
         bool ok[4][NPA];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const int q = q0 + k;
 #pragma unroll
             for (int pp = 0; pp < NPA; ++pp) {
-                d[k][pp] = 0.0f;
+                d[k][pp] = 0.0;
                 ok[k][pp] = false;
                 if (pp >= NP) continue;
-                const int nq = y.nq[pp];
+                const int nq = y.nq[pp], S = y.qS[pp];
                 const int sq = (int)ws[pp][q].y;
                 // uniform: slots below lim arrive by T - 1 (none past the
                 // count or the projections); the row by an unsigned min, as
                 // n_mod + sq < 2 S
                 const int lim = (pp < y.npost && q < cnt) ? a.T - n : 0;
-                const unsigned ru = (unsigned)(n_mod + sq);
-                const int row = (int)min(ru, ru - (unsigned)a.S);
+                const unsigned ru = (unsigned)(n_mod[pp] + sq);
+                const int row = (int)min(ru, ru - (unsigned)S);
                 ok[k][pp] = sq < lim && tid < nq;
                 // (in LDS the row is always in the ring and the column is
                 // clamped into it, so the read needs no mask; its value does)
                 if (RL)
-                    d[k][pp] = ((lds_f32*)(lds + y.qring_lds[pp]))[row * nq + min(tid, nq - 1)];
+                    d[k][pp] = ((lds_f64*)(smem + y.qring_lds[pp]))[row * nq + min(tid, nq - 1)];
                 else   // (masked reads share one line of device memory)
-                    d[k][pp] = ((global_f32*)(y.qring[pp] +
-                                              ((size_t)b * a.S + (ok[k][pp] ? row : 0)) * nq))[ok[k][pp] ? tid : 0];
+                    d[k][pp] = ((global_f64*)(y.qring[pp] +
+                                              ((size_t)b * S + (ok[k][pp] ? row : 0)) * nq))[ok[k][pp] ? tid : 0];
             }
         }
         if constexpr (NPA == 1) {
@@ -279,8 +281,8 @@ struct BwdCore {
 #pragma unroll
             for (int pp = 0; pp < NP; ++pp) {
                 // a masked term is +0 (v - 0 = v exactly)
-                const float t = __fmul_rn(__uint_as_float(ws[pp][q].x), d[k][pp]);
-                v[k] -= (double)(ok[k][pp] ? t : 0.0f);
+                const double t = __dmul_rn((double)__uint_as_float(ws[pp][q].x), d[k][pp]);
+                v[k] = __dsub_rn(v[k], ok[k][pp] ? t : 0.0);
             }
         }
         const double x = row_sum4(v, lane);
@@ -289,8 +291,9 @@ struct BwdCore {
     }
 
     static __device__ __forceinline__ void gather(const CoreBwdArgs& a, int b, int tid, int n,
-                                                  int n_mod, int l, int cnt, const int (&ids)[KP],
-                                                  const uint2 (&ws)[NPA][KP], double* part_l) {
+                                                  const int (&n_mod)[NPA], int l, int cnt,
+                                                  const int (&ids)[KP], const uint2 (&ws)[NPA][KP],
+                                                  double* part_l) {
 #pragma unroll
         for (int q0 = 0; q0 < KP; q0 += 4)
             if (cnt > q0) gather4(a, b, tid, n, n_mod, l, q0, cnt, ids, ws, part_l);
@@ -298,7 +301,7 @@ struct BwdCore {
 
     // The lambda_V jump of this lane's spike at position q of a round.
     static __device__ __forceinline__ void jump(const CoreBwdArgs& a, const double* part_l, int q,
-                                                float I, double A2, float& lv,
+                                                float I, double A2, double& lv,
                                                 unsigned long long& deg) {
         double A = A2;
         if (NP > 0) {
@@ -318,17 +321,17 @@ struct BwdCore {
             }
             A += Ap;
         }
-        const float den = __fsub_rn(I, a.theta);
-        if (den > 0.0f) {
-            const float D = (float)(((double)a.theta * (double)lv + A) / (double)den);
-            lv = __fadd_rn(lv, D);
+        // tau_m dV/dt just before the crossing is I- - theta (V- = theta)
+        const double den = __dsub_rn((double)I, a.theta);
+        if (den > 0.0) {
+            lv = __dadd_rn(lv, __dadd_rn(__dmul_rn(a.theta, lv), A) / den);
         } else {
             ++deg;
         }
     }
 
     struct Lane {
-        float lv[NL], lI[NL];
+        double lv[NL], lI[NL];
         unsigned long long deg;
         int rnd;
     };
@@ -336,10 +339,14 @@ struct BwdCore {
     // One reverse-time step n with the loads of A, issuing those of B.
     static __device__ __forceinline__ void step(const CoreBwdArgs& a, int b, int tid, int n,
                                                 const State& A, State& B, Lane& L) {
-        const int T = a.T, S = a.S, LT = a.lif_total;
-        const int n_mod = n % S;
-        float* lds = reinterpret_cast<float*>(smem);
+        const int T = a.T, LT = a.lif_total;
         double* part = reinterpret_cast<double*>(smem + a.part_off);   // [2][NL][KP][4 NW]
+        // n modulo the adjoint-ring slots of each post layer read by layer l
+        int nm[NL][NPA];
+#pragma unroll
+        for (int l = 0; l < NL; ++l)
+#pragma unroll
+            for (int pp = 0; pp < NPA; ++pp) nm[l][pp] = (NP > 0) ? n % a.ly[l].qS[pp] : 0;
 
         // the loads issued one step ago (A) have landed: wait for them once,
         // here, so that no later use waits for this step's loads
@@ -352,19 +359,18 @@ struct BwdCore {
             const BwdLayer& y = a.ly[l];
             if (tid >= y.n) continue;
             if (n <= T - 2) {
-                const float v = L.lv[l];
-                L.lI[l] = __fadd_rn(__fmul_rn(a.beta, L.lI[l]), __fmul_rn(a.cc, v));
-                L.lv[l] = __fmul_rn(a.alpha, v);
+                const double v = L.lv[l];
+                L.lI[l] = __dadd_rn(__dmul_rn(a.beta, L.lI[l]), __dmul_rn(a.cc, v));
+                L.lv[l] = __dmul_rn(a.alpha, v);
             }
-            const float d = __fsub_rn(L.lI[l], L.lv[l]);
-            const size_t o = ((size_t)b * T + n) * LT + y.lif_off + tid;
-            a.tu[o] = L.lI[l];
-            a.td[o] = d;
+            const double d = __dsub_rn(L.lI[l], L.lv[l]);
+            a.traj[((size_t)b * T + n) * LT + y.lif_off + tid] = make_double2(L.lI[l], d);
             if (y.ring_lds == -2) continue;
+            const int n_own = n % y.S;
             if (RL)
-                ((lds_f32*)(lds + y.ring_lds))[n_mod * y.n + tid] = d;
+                ((lds_f64*)(smem + y.ring_lds))[n_own * y.n + tid] = d;
             else
-                ((global_f32*)(y.ring + ((size_t)b * S + n_mod) * y.n))[tid] = d;
+                ((global_f64*)(y.ring + ((size_t)b * y.S + n_own) * y.n))[tid] = d;
         }
 
         // ---- round 0: the first KP spikes of every layer, prefetched
@@ -375,7 +381,7 @@ struct BwdCore {
 #pragma unroll
                 for (int l = 0; l < NL; ++l) {
                     double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
-                    gather(a, b, tid, n, n_mod, l, A.cnt3[l], A.id3[l], A.ws[l], part_l);
+                    gather(a, b, tid, n, nm[l], l, A.cnt3[l], A.id3[l], A.ws[l], part_l);
                 }
             }
             __syncthreads();
@@ -408,7 +414,7 @@ struct BwdCore {
                 uint2 ws[NPA][KP];
                 load_step(a, b, tid, l, A.ri3[l], cnt, ids, r * KP, ws, mine[l], I[l], A2[l]);
                 double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
-                if (NP > 0) gather(a, b, tid, n, n_mod, l, cnt, ids, ws, part_l);
+                if (NP > 0) gather(a, b, tid, n, nm[l], l, cnt, ids, ws, part_l);
             }
             __syncthreads();
 #pragma unroll
@@ -426,8 +432,8 @@ struct BwdCore {
         Lane L;
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
-            L.lv[l] = 0.0f;
-            L.lI[l] = 0.0f;
+            L.lv[l] = 0.0;
+            L.lI[l] = 0.0;
         }
         L.deg = 0;
         L.rnd = 0;
@@ -531,9 +537,10 @@ __global__ void __launch_bounds__(1024) group_kernel(GroupArgs a) {
 // apart, so every lane sums about the same number of spikes however the
 // input concentrates on some channels.  Per sample the J post trajectories
 // and the sample's grouped spike steps are staged in LDS; each lane sums, per
-// synapse and in spike order, lambda_I and w (lambda_I - lambda_V) at the
-// delayed arrivals in fp32, then adds the sample's sums in fp64.  Sample
-// blocks are reduced in a fixed order: no atomics, deterministic.
+// synapse, in sample then spike order, lambda_I and lambda_I - lambda_V at
+// the delayed arrivals in fp64; the weight multiplies the delay sum once at
+// the end.  Sample blocks are reduced in a fixed order: no atomics,
+// deterministic.
 //
 // Workgroups come in units of four J-post blocks that share lines of the
 // [B][T][N] trajectories; a unit's four blocks have indices 8 apart, so with
@@ -553,10 +560,9 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
     const int nq = G.nq, j0 = jb * J, nj = min(J, nq - j0);
     const int T = a.T;
     const int TW = WIN ? a.TW : a.T;                            // steps per trajectory window
-    float2* st = reinterpret_cast<float2*>(smem);              // [J][TW]
-    unsigned short* sp = reinterpret_cast<unsigned short*>(smem + (size_t)J * TW * sizeof(float2));
-    const float* tu = G.out ? a.tu_out : a.tu_lif;
-    const float* td = G.out ? a.td_out : a.td_lif;
+    double2* st = reinterpret_cast<double2*>(smem);            // [J][TW]
+    unsigned short* sp = reinterpret_cast<unsigned short*>(smem + (size_t)J * TW * sizeof(double2));
+    const double2* tr = G.out ? a.tr_out : a.tr_lif;
     const int LN = G.out ? a.C : a.lif_total;
     const int n0 = G.npre[0], n1 = (G.np > 1) ? G.npre[1] : 0;
     const int vtot = n0 + n1;
@@ -570,17 +576,14 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
         // post within the block (16-19), projection part (20), slot (21-28);
         // -1: none
         int dsc[KL];
-        float w[KL];
 #pragma unroll
         for (int k = 0; k < KL; ++k) {
             const int p = pbase + tid + nt * k;
             const int v = p / J, q = p % J;
             dsc[k] = -1;
-            w[k] = 0.0f;
             if (p < J * vtot && q < nj) {
                 const int pi = (v >= n0) ? 1 : 0, i = v - (pi ? n0 : 0);
                 const uint2 e = a.ws[a.woff[G.p[pi]] + (size_t)i * nq + j0 + q];
-                w[k] = __uint_as_float(e.x);
                 dsc[k] = i | (q << 16) | (pi << 20) | ((int)e.y << 21);
             }
         }
@@ -608,7 +611,7 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
             const bool in_lds = c0 + c1 <= a.spcap;
             // (loads of eight iterations issued before their stores, so that a
             // sample's staging costs a few memory round trips, not one each)
-            constexpr int U = 8;
+            constexpr int U = (KL > 4) ? 4 : 8;
             if (in_lds) {
                 for (int x0 = tid; x0 < c0 + c1; x0 += U * nt) {
                     int v[U];
@@ -631,20 +634,20 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
                 const int W = min(TW, T - w0), wend = w0 + W;
                 if (w0 > 0) __syncthreads();                        // the last window's reads are done
                 for (int e0 = tid; e0 < W * J; e0 += U * nt) {
-                    float2 x[U];
+                    double2 x[U];
 #pragma unroll
                     for (int u = 0; u < U; ++u) {
                         const int e = min(e0 + u * nt, W * J - 1);
                         const int m = w0 + e / J, q = e % J;
                         const int qc = min(q, nj - 1);
-                        x[u] = make_float2(tu[base + (size_t)m * LN + qc], td[base + (size_t)m * LN + qc]);
+                        x[u] = tr[base + (size_t)m * LN + qc];
                     }
 #pragma unroll
                     for (int u = 0; u < U; ++u) {
                         const int e = e0 + u * nt;
                         if (e < W * J) {
                             const int mw = e / J, q = e % J;
-                            st[q * TW + mw] = (q < nj) ? x[u] : make_float2(0.0f, 0.0f);
+                            st[q * TW + mw] = (q < nj) ? x[u] : make_double2(0.0, 0.0);
                         }
                     }
                 }
@@ -659,10 +662,10 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
                     asm volatile("" : "+v"(dk));
                     if (dk < 0) continue;
                     const int pi = (dk >> 20) & 1, sl = (dk >> 21) & 0xFF;
-                    const float2* stk = st + ((dk >> 16) & 0xF) * TW;        // index: arrival - w0
+                    const double2* stk = st + ((dk >> 16) & 0xF) * TW;       // index: arrival - w0
                     const int* gs = pi ? gs1 : gs0;
                     const int off = pi ? c0 - s1 : -s0;             // LDS index = x + off
-                    float pu = 0.0f, pd = 0.0f;
+                    double pu = su[k], pd = sd[k];
                     // four spikes at a time: their reads issued together, their
                     // terms added in spike order; the arrivals ascend, so the
                     // window's spikes are a prefix from the cursor
@@ -675,14 +678,14 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
                             const int t = in_lds ? (int)sp[xc + off] : gs[xc];
                             m[u] = (x + u < hi[k]) ? t + sl : T;     // T: no arrival
                         }
-                        float2 ud[4];
+                        double2 ud[4];
 #pragma unroll
                         for (int u = 0; u < 4; ++u) ud[u] = stk[(m[u] < wend) ? m[u] - w0 : 0];
 #pragma unroll
                         for (int u = 0; u < 4; ++u) {
                             if (m[u] < wend) {
-                                pu = __fadd_rn(pu, ud[u].x);
-                                pd = __fadd_rn(pd, __fmul_rn(w[k], ud[u].y));
+                                pu = __dadd_rn(pu, ud[u].x);
+                                pd = __dadd_rn(pd, ud[u].y);
                             }
                         }
                         if constexpr (WIN) {
@@ -693,8 +696,8 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
                         }
                     }
                     if constexpr (WIN) lo[k] = min(x, hi[k]);
-                    su[k] += (double)pu;
-                    sd[k] += (double)pd;
+                    su[k] = pu;
+                    sd[k] = pd;
                 }
             }
         }
@@ -704,8 +707,9 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
             const int p = G.p[(dsc[k] >> 20) & 1];
             const size_t kk = (size_t)(dsc[k] & 0xFFFF) * nq + j0 + ((dsc[k] >> 16) & 0xF);
             if (a.SB == 1) {
+                const double w = (double)__uint_as_float(a.ws[a.woff[p] + kk].x);
                 a.dW[p][kk] = (float)(-(double)a.tau_s * su[k]);
-                a.dD[p][kk] = (float)(-(double)a.dt * sd[k]);
+                a.dD[p][kk] = (float)(-(double)a.dt * (w * sd[k]));
             } else {
                 const size_t gi = (size_t)a.woff[p] + kk;
                 a.part[((size_t)sb * 2 + 0) * a.nparams + gi] = su[k];
@@ -740,8 +744,9 @@ __global__ void grad_reduce_kernel(GradArgs a, int P) {
         sd += a.part[((size_t)sb * 2 + 1) * a.nparams + g];
     }
     const long long kk = g - a.woff[p];
+    const double w = (double)__uint_as_float(a.ws[g].x);
     a.dW[p][kk] = (float)(-(double)a.tau_s * su);
-    a.dD[p][kk] = (float)(-(double)a.dt * sd);
+    a.dD[p][kk] = (float)(-(double)a.dt * (w * sd));
 }
 
 }  // namespace

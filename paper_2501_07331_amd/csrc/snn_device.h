@@ -5,11 +5,10 @@
 
 #include "snn_internal.h"
 
+// dynamic LDS of every kernel
 extern __shared__ __align__(16) unsigned char smem[];
 
 namespace {
-
-extern __shared__ __align__(16) unsigned char smem[];
 
 __device__ __forceinline__ unsigned long long uniform64(unsigned long long x) {
     const unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)x);
@@ -28,6 +27,8 @@ __device__ __forceinline__ int lanes_below(unsigned long long m) {
 // folded into one flat access, and the fp64 LDS atomic is ds_add_f64.
 typedef __attribute__((address_space(1))) float global_f32;
 typedef __attribute__((address_space(3))) float lds_f32;
+typedef __attribute__((address_space(1))) double global_f64;
+typedef __attribute__((address_space(3))) double lds_f64;
 
 // x of the lane given by the DPP control CTRL (within 16-lane rows), fp64 as
 // two 32-bit moves.
@@ -41,9 +42,8 @@ __device__ __forceinline__ double dpp_f64(double x) {
 
 inline unsigned grid_for(long long n, int block) { return (unsigned)((n + block - 1) / block); }
 
-// ------------------------------------------------------------------ batched ring updates
-
-constexpr int KB = 8;   // spikes per batch
+// spikes per chunk of the delayed scatters
+constexpr int KB = 8;
 
 // ------------------------------------------------------------------ forward core
 

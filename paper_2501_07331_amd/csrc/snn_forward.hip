@@ -60,11 +60,13 @@ struct RoundArgs {
     const float* D[SNN_MAXP];
     const float* W[SNN_MAXP];
     long long woff[SNN_MAXP + 1];
-    int P, max_delay;
+    int dmax[SNN_MAXP];
+    int P;
 };
 
-// Delays are integer multiples of the time step: rint (half to even), clamp.
-// Also writes (weight bits, slot) pairs for one-load access to both.
+// Delays are integer multiples of the time step: rint (half to even), clamp
+// to [0, the projection's largest delay].  Also writes (weight bits, slot)
+// pairs for one-load access to both.
 __global__ void round_delays_kernel(RoundArgs a, uint8_t* slot, uint2* ws, DevStatus* st) {
     const long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     bool clamped = false;
@@ -74,7 +76,7 @@ __global__ void round_delays_kernel(RoundArgs a, uint8_t* slot, uint2* ws, DevSt
         const float r = rintf(a.D[p][g - a.woff[p]]);
         int s;
         if (!(r >= 0.0f)) { s = 0; clamped = true; }            // negative or NaN
-        else if (r > (float)a.max_delay) { s = a.max_delay; clamped = true; }
+        else if (r > (float)a.dmax[p]) { s = a.dmax[p]; clamped = true; }
         else s = (int)r;
         slot[g] = (uint8_t)s;
         ws[g] = make_uint2(__float_as_uint(a.W[p][g - a.woff[p]]), (unsigned)s);
@@ -333,7 +335,7 @@ __global__ void __launch_bounds__(1024) readout_forward_kernel(ReadoutArgs a) {
             }
             const size_t base = ((size_t)t.lif[pa] * t.B + b) * t.cap;
             const int* idx = a.rec_idx + ((size_t)t.lif[pa] * t.B + b) * (T + 1);
-            const int e_lo = idx[max(0, m0 - (t.S - 1))], e_hi = idx[m1];
+            const int e_lo = idx[max(0, m0 - (t.Sp[t.out_p] - 1))], e_hi = idx[m1];
             const int wsb = t.n[pa] * C * 8;
             if (in_lds)
                 scatter_events(a.rec_n + base, a.rec_s + base, e_lo, e_hi, a.ws, wsb, C, k, k < C, m0, m1,
@@ -370,9 +372,9 @@ __global__ void __launch_bounds__(1024) readout_forward_kernel(ReadoutArgs a) {
 
 // Softmax cross-entropy on z in fp64; loss_out[b], loss_out[B] = mean; the
 // per-step loss source on the readout adjoint src = s g / tau_m (sum) or
-// g / tau_m (max), g = (softmax - onehot) / B rounded to fp32 first.
+// g / tau_m (max) in fp64, g = (softmax - onehot) / B rounded to fp32 first.
 __global__ void loss_kernel(const float* z, const int* labels, int B, int C, int loss, float rscale,
-                            float tau_m, float* loss_out, float* src, const DevStatus* st) {
+                            float tau_m, float* loss_out, double* src, const DevStatus* st) {
     __shared__ double part[256];
     if (st->bad_input) return;
     double tot = 0.0;
@@ -390,9 +392,9 @@ __global__ void loss_kernel(const float* z, const int* labels, int B, int C, int
         for (int k = 0; k < C; ++k) {
             const double p = exp((double)zb[k] - lse);
             const float g = (float)((p - (k == y ? 1.0 : 0.0)) / (double)B);
-            const double sk = (loss == SNN_LOSS_CE_SUM) ? (double)rscale * (double)g / (double)tau_m
-                                                        : (double)g / (double)tau_m;
-            src[(size_t)b * C + k] = (float)sk;
+            src[(size_t)b * C + k] = (loss == SNN_LOSS_CE_SUM)
+                                         ? (double)rscale * (double)g / (double)tau_m
+                                         : (double)g / (double)tau_m;
         }
     }
     part[threadIdx.x] = tot;
@@ -500,17 +502,17 @@ hipError_t launch_step_index(const int* off, const int* step, int B, int T, int*
 }
 
 hipError_t launch_round_delays(const float* const* D, const float* const* W, const long long* woff,
-                               const long long* cnt, int P, int max_delay, uint8_t* slot, uint2* ws,
+                               const long long* cnt, int P, const int* dmax, uint8_t* slot, uint2* ws,
                                DevStatus* st, hipStream_t s) {
     RoundArgs a{};
     for (int p = 0; p < P; ++p) {
         a.D[p] = D[p];
         a.W[p] = W[p];
         a.woff[p] = woff[p];
+        a.dmax[p] = dmax[p];
     }
     a.woff[P] = woff[P - 1] + cnt[P - 1];
     a.P = P;
-    a.max_delay = max_delay;
     hipLaunchKernelGGL(round_delays_kernel, dim3(grid_for(a.woff[P], 256)), dim3(256), 0, s, a, slot,
                        ws, st);
     return hipGetLastError();
@@ -529,7 +531,7 @@ hipError_t launch_readout_forward(const ReadoutArgs& a, int threads, size_t lds,
 }
 
 hipError_t launch_loss(const float* z, const int* labels, int B, int C, int loss, float rscale,
-                       float tau_m, float* loss_out, float* src, const DevStatus* st, hipStream_t s) {
+                       float tau_m, float* loss_out, double* src, const DevStatus* st, hipStream_t s) {
     hipLaunchKernelGGL(loss_kernel, dim3(1), dim3(256), 0, s, z, labels, B, C, loss, rscale, tau_m,
                        loss_out, src, st);
     return hipGetLastError();

@@ -48,7 +48,7 @@ struct FwdCore {
         if constexpr (RL) {
             return (lds_f32*)(reinterpret_cast<float*>(smem) + y.ring_lds[pp]) + col;
         } else {
-            return (global_f32*)(y.ring[pp] + (size_t)b * (a.S + 1) * y.nq[pp]) + col;
+            return (global_f32*)(y.ring[pp] + (size_t)b * (y.S[pp] + 1) * y.nq[pp]) + col;
         }
     }
     typedef typename std::conditional<RL, lds_f32*, global_f32*>::type RingPtr;
@@ -83,7 +83,7 @@ struct FwdCore {
     static __device__ __forceinline__ void scatter(const CoreFwdArgs& a, int b, int l, int pp, int tid,
                                                    int e, int cnt, const uint2 (&w)[N]) {
         const FwdLayer& y = a.ly[l];
-        const int nq = y.nq[pp], S = a.S;
+        const int nq = y.nq[pp], S = y.S[pp];
         const bool live = pp < y.npost && tid < nq;
         const int e_mod = e % S;
         RingPtr col = ring_col<RingPtr>(a, b, l, pp, min(tid, nq - 1));
@@ -145,7 +145,7 @@ struct FwdCore {
     static __device__ __forceinline__ void step(const CoreFwdArgs& a, int b, int tid, int n,
                                                 const Pre& P, Pre& N, Lane& L) {
         const int lane = tid & 63, wave = tid >> 6;
-        const int T = a.T, S = a.S, NW = a.NW;
+        const int T = a.T, NW = a.NW;
         unsigned long long* masks = reinterpret_cast<unsigned long long*>(smem + a.mask_off);
         const int par = n % 3;
 
@@ -225,7 +225,6 @@ struct FwdCore {
         }
 
         // ---- arrivals at step n: per projection into the layer, in projection order
-        const int n_mod = n % S;
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
             const FwdLayer& y = a.ly[l];
@@ -239,6 +238,7 @@ struct FwdCore {
                     add = P.ain;
                 } else {
                     const int pp = y.in_pp[e];
+                    const int n_mod = n % a.ly[sl].S[pp];
                     RingPtr c = ring_col<RingPtr>(a, b, sl, pp, tid) + n_mod * y.n;
                     add = *c;
                     *c = 0.0f;
@@ -262,7 +262,6 @@ struct FwdCore {
     static __device__ __forceinline__ void run(const CoreFwdArgs& a) {
         if (a.st->bad_input) return;
         const int b = blockIdx.x, tid = threadIdx.x;
-        const int S = a.S;
         // ---- zero the ring columns this lane owns (rows 0 .. S, row S: dummy)
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
@@ -271,7 +270,7 @@ struct FwdCore {
                 const FwdLayer& y = a.ly[l];
                 if (pp >= y.npost || tid >= y.nq[pp]) continue;
                 RingPtr c = ring_col<RingPtr>(a, b, l, pp, tid);
-                for (int r = 0; r <= S; ++r) c[r * y.nq[pp]] = 0.0f;
+                for (int r = 0; r <= y.S[pp]; ++r) c[r * y.nq[pp]] = 0.0f;
             }
         }
         Lane L;

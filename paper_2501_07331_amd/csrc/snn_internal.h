@@ -8,7 +8,6 @@
 
 #define SNN_MAXP (2 * SNN_MAX_LAYERS)
 #define SNN_MAX_LIF (SNN_MAX_LAYERS - 2)  // LIF layers are 1 .. L-2
-#define SNN_MAX_INPUT 16384          // input neurons (per-sample spike grouping in LDS)
 
 // Per-step spike table of a LIF layer, one row per (sample, step):
 // [spikes at the step, record index of its first spike, first SNN_STEP_IDS
@@ -27,7 +26,7 @@ struct DevStatus {
 
 // Topology, constants and the LDS plan, passed by value to every kernel.
 struct Topo {
-    int L, P, B, T, S, cap, loss, n_in;
+    int L, P, B, T, S, cap, loss, n_in;   // S: the deepest delay ring (max_delay + 1)
     int n_lif, lif_total, maxn;        // LIF layers, LIF neurons, widest non-input layer
     int out_l;                         // the output layer (L - 1): LI readout, or LIF (spike-time loss)
     int out_lif;                       // 1: the output layer is LIF (SNN_LOSS_DMSE)
@@ -39,19 +38,24 @@ struct Topo {
     int lif_off[SNN_MAX_LAYERS];       // offset of a LIF layer among all LIF neurons
     int pre[SNN_MAXP], post[SNN_MAXP];
     long long woff[SNN_MAXP];          // offset of projection p in flat parameter arrays
+    int dmax[SNN_MAXP];                // largest delay slot of projection p (its clamp)
+    int Sp[SNN_MAXP];                  // delay-ring slots of projection p: dmax + 1
+    int Sb[SNN_MAX_LAYERS];            // adjoint-ring slots of a LIF layer: the largest Sp of
+                                       // the LIF-pre projections into it (0: no such ring)
     // forward delay ring of projection p (LIF pre and LIF post): LDS float
     // offset, or -1 for the global ring [B][S][n_post]
     int fring[SNN_MAXP];
-    // backward ring of lambda_I - lambda_V of a LIF layer read by LIF-pre
-    // projections: LDS float offset, or -1 for the global ring [B][S][n]
+    // backward ring of lambda_I - lambda_V (fp64) of a LIF layer read by
+    // LIF-pre projections: LDS byte offset, or -1 for the global ring [B][Sb][n]
     int bring[SNN_MAX_LAYERS];
 };
 
 // Input projection arrivals: A_in[b][n][j] = sum, in emission order, of the
 // input-projection weights arriving at post j of layer 1 at step n.
 struct InScanArgs {
-    int B, T, S, n_in, n1, TB;         // TB: step span of an 8-event chunk on the fast path;
-                                       // the LDS ring holds S + TB - 1 arrival steps
+    int B, T, S, n_in, n1, TB;         // S: ring slots of the input projection; TB: step span
+                                       // of an 8-event chunk on the fast path; the LDS ring
+                                       // holds S + TB - 1 arrival steps
     const uint2* ws0;                  // input projection (weight bits, slot) [n_in][n1]
     const int* in_neuron;
     const int* in_step;
@@ -60,16 +64,13 @@ struct InScanArgs {
     const DevStatus* st;
 };
 
-// One LIF layer as seen by the forward core.
-// spikes per step of a LIF layer whose data the backward core prefetches a
+// Spikes per step of a LIF layer whose data the backward core prefetches a
 // step ahead (more are loaded in further rounds), by LIF layer count; 16
 // covers nearly every step of a 256-neuron layer at 14 spikes per neuron
-// while its input is active (8 left a quarter of them to an extra round)
+// while its input is active (8 left a quarter of them to an extra round).
 constexpr int bwd_prefetch(int n_lif) { return n_lif == 1 ? 16 : 4; }
 
-// zero-delay synapses per post neuron and LIF-post projection that the
-// deferred forward scatter handles from LDS
-
+// One LIF layer as seen by the forward core.
 struct FwdLayer {
     int n;
     int nin;                           // projections into the layer, in projection order:
@@ -79,6 +80,7 @@ struct FwdLayer {
                                        // feed-forward); entries past npost repeat a valid one
     int nq[2];                         //   post neurons
     int npre[2];                       //   rows of ws (the presynaptic layer's neurons)
+    int S[2];                          //   ring slots (the projection's largest delay + 1)
     int ring_lds[2];                   //   delay ring [S+1][nq] (row S: dummy): LDS float offset,
     float* ring[2];                    //   or the HBM ring [B][S+1][nq]
     const uint2* ws[2];                //   (weight bits, slot) [n][nq]
@@ -94,7 +96,7 @@ struct FwdLayer {
 };
 
 struct CoreFwdArgs {
-    int B, T, S, cap, NW, n1, nstate;
+    int B, T, cap, NW, n1, nstate;
     float alpha, beta, gamma, theta;
     FwdLayer ly[SNN_MAX_LIF];
     int soff[SNN_MAX_LIF];             // offset of each LIF layer in the [B][nstate] final state
@@ -103,7 +105,6 @@ struct CoreFwdArgs {
     float* If;
     DevStatus* st;
     int mask_off;                      // byte offset of the ballot masks [3][NL][NW] in LDS
-                                       // in LDS, -1: none (no deferred scatter)
 };
 
 struct ReadoutArgs {
@@ -124,34 +125,38 @@ struct ReadoutArgs {
 
 // Readout adjoint: lambda of the LI layer from its loss source, trajectories,
 // and the readout part of the jump sum of every spike of the feeding layer.
+// The backward pass is fp64 throughout: constants from fp64 host arithmetic,
+// adjoints, trajectories, rings, jump sums and gradient sums.
 struct ReadoutBwdArgs {
     int B, T, C, cap, loss;
-    float alpha, beta, cc;
+    double alpha, beta, cc;
     const uint2* ws;                   // [n_feed][C] (weight bits, slot)
     const int* rec_n;                  // records of the feeding LIF layer [B][cap], or NULL
     const int* rec_s;
     const int* rec_cnt;                // [B]
     const int* nstar;                  // [B][C]
-    const float* src;                  // [B][C]
-    float* tu;                         // [B][T][C] lambda_I
-    float* td;                         // [B][T][C] lambda_I - lambda_V
+    const double* src;                 // [B][C] loss source on lambda_V per step (sum) or at n*
+    double2* traj;                     // [B][T][C] (lambda_I, lambda_I - lambda_V)
     double* A2;                        // [B][cap]
-    int tab_lds;                       // 1: the [T][C] table of td lives in LDS
+    int tab_lds;                       // 1: the [T][C] table of lambda_I - lambda_V lives in LDS
 };
 
 // One LIF layer as seen by the backward core.
 struct BwdLayer {
     int n, lif_off;
-    int ring_lds;                      // LDS float offset of the adjoint ring [S][n]; -1 global; -2 none
-    float* ring;                       // global adjoint ring [B][S][n] when ring_lds == -1
+    int S;                             // adjoint-ring slots
+    int ring_lds;                      // LDS byte offset of the adjoint ring [S][n] (fp64); -1
+                                       // global; -2 none
+    double* ring;                      // global adjoint ring [B][S][n] when ring_lds == -1
     int npost;                         // LIF-post projections out of this layer: the recurrent
                                        // one, then the feed-forward one (projection order); the
                                        // entries past npost repeat a valid projection (loads stay
                                        // in bounds; their contributions are masked)
     int nq[2];                         // their post layer's neurons,
     int npre[2];                       //   rows of ws (an entry past npost may have fewer than n),
-    int qring_lds[2];                  //   adjoint ring (LDS float offset, or -1: global qring)
-    float* qring[2];
+    int qS[2];                         //   adjoint-ring slots of the post layer,
+    int qring_lds[2];                  //   its adjoint ring (LDS byte offset, or -1: global qring)
+    double* qring[2];
     const uint2* ws[2];                //   (weight bits, slot) [n][nq]
     const float* recI;                 // [B][cap] I- of the records
     const int* recn;                   // [B][cap] neuron of the records
@@ -161,11 +166,10 @@ struct BwdLayer {
 };
 
 struct CoreBwdArgs {
-    int B, T, S, cap, NW, lif_total;
-    float alpha, beta, cc, theta;
+    int B, T, cap, NW, lif_total;
+    double alpha, beta, cc, theta;
     BwdLayer ly[SNN_MAX_LIF];
-    float* tu;                         // [B][T][lif_total] lambda_I
-    float* td;                         // [B][T][lif_total] lambda_I - lambda_V
+    double2* traj;                     // [B][T][lif_total] (lambda_I, lambda_I - lambda_V)
     DevStatus* st;
     int part_off;                      // LDS byte offset of the partial jump sums
 };
@@ -204,10 +208,8 @@ struct GradArgs {
     int spcap;                         // LDS capacity for a sample's spike steps (16-bit), 0: none
     float tau_s, dt;
     long long nparams;
-    const float* tu_lif;               // [B][T][lif_total]
-    const float* td_lif;
-    const float* tu_out;               // [B][T][C]
-    const float* td_out;
+    const double2* tr_lif;             // [B][T][lif_total] (lambda_I, lambda_I - lambda_V)
+    const double2* tr_out;             // [B][T][C]
     const uint2* ws;                   // flat [params] (weight bits, slot)
     long long woff[SNN_MAXP];
     const int* g_off[SNN_MAX_LAYERS];  // per presynaptic layer: [B][n+1]
@@ -241,14 +243,14 @@ hipError_t launch_validate(const int* off, const int* step, const int* neuron, i
 hipError_t launch_step_index(const int* off, const int* step, int B, int T, int* idx,
                              const DevStatus* st, hipStream_t s);
 hipError_t launch_round_delays(const float* const* D, const float* const* W, const long long* woff,
-                               const long long* cnt, int P, int max_delay, uint8_t* slot, uint2* ws,
+                               const long long* cnt, int P, const int* dmax, uint8_t* slot, uint2* ws,
                                DevStatus* st, hipStream_t s);
 hipError_t launch_input_scan(const InScanArgs& a, size_t lds, hipStream_t s);
 hipError_t launch_forward_core(const CoreFwdArgs& a, int n_lif, int threads, size_t lds,
                                hipStream_t s);
 hipError_t launch_readout_forward(const ReadoutArgs& a, int threads, size_t lds, hipStream_t s);
 hipError_t launch_loss(const float* z, const int* labels, int B, int C, int loss, float rscale,
-                       float tau_m, float* loss_out, float* src, const DevStatus* st, hipStream_t s);
+                       float tau_m, float* loss_out, double* src, const DevStatus* st, hipStream_t s);
 hipError_t launch_copy_state(const float* src, int stride, int off, int n, int B, float* dst,
                              hipStream_t s);
 hipError_t launch_readout_adjoint(const ReadoutBwdArgs& a, int threads, size_t lds, hipStream_t s);

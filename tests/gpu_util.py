@@ -14,17 +14,26 @@ def default_cap(wl: Workload) -> int:
     return 64 * max(lif + [1])
 
 
-def oracle_net(wl: Workload, max_delay=None):
+def proj_delays(wl: Workload, max_delay=None, per_proj=True):
+    """(network-wide max delay, per-projection largest delays or None): each
+    projection's delay range of the config, capped at max_delay if given."""
     c = wl.cfg
-    return oracle.OracleNet(c.layers, c.tau_m, c.tau_s, c.theta, c.dt,
-                            c.max_delay if max_delay is None else max_delay, wl.T, c.loss,
-                            c.readout_scale)
+    md = c.max_delay if max_delay is None else max_delay
+    return md, ([min(r, md) for r in c.delay_range] if per_proj else None)
 
 
-def run_oracle(wl: Workload, cap=None, modes=("f64", "f32"), max_delay=None, dlp=None):
+def oracle_net(wl: Workload, max_delay=None, per_proj=True):
+    c = wl.cfg
+    md, pm = proj_delays(wl, max_delay, per_proj)
+    return oracle.OracleNet(c.layers, c.tau_m, c.tau_s, c.theta, c.dt, md, wl.T, c.loss,
+                            c.readout_scale, pm)
+
+
+def run_oracle(wl: Workload, cap=None, modes=("f64", "f32"), max_delay=None, dlp=None,
+               per_proj=True):
     """dlp: extra per-record dl_p/dt_k [n_lif][B][cap] (fp64) or None."""
     cap = default_cap(wl) if cap is None else cap
-    net = oracle_net(wl, max_delay)
+    net = oracle_net(wl, max_delay, per_proj)
     f = oracle.forward(net, wl.in_off, wl.in_step, wl.in_neuron, wl.W, wl.D, cap=cap)
     if wl.cfg.loss == oracle.LOSS_DMSE:
         lo, dl = oracle.loss_dmse(f.z, wl.labels, wl.cfg.dmse_delta)
@@ -42,13 +51,13 @@ def run_oracle(wl: Workload, cap=None, modes=("f64", "f32"), max_delay=None, dlp
     return out
 
 
-def make_gpu_net(wl: Workload, cap=None, flags=0, max_delay=None):
+def make_gpu_net(wl: Workload, cap=None, flags=0, max_delay=None, per_proj=True):
     import paper_2501_07331_amd as snn
     c = wl.cfg
     cap = default_cap(wl) if cap is None else cap
-    return snn.Network(c.layers, c.tau_m, c.tau_s, c.theta, c.dt,
-                       c.max_delay if max_delay is None else max_delay, wl.B, wl.T, c.loss,
-                       c.readout_scale, cap, flags, dmse_delta=c.dmse_delta)
+    md, pm = proj_delays(wl, max_delay, per_proj)
+    return snn.Network(c.layers, c.tau_m, c.tau_s, c.theta, c.dt, md, wl.B, wl.T, c.loss,
+                       c.readout_scale, cap, flags, dmse_delta=c.dmse_delta, proj_max_delay=pm)
 
 
 def to_device(wl: Workload):
@@ -64,12 +73,12 @@ def to_device(wl: Workload):
 
 
 def run_gpu(wl: Workload, net=None, cap=None, flags=0, backward=True, max_delay=None, dev_in=None,
-            dlp=None):
+            dlp=None, per_proj=True):
     """Forward (+ backward) through the library; returns numpy results.
     dlp: per LIF layer None or an fp32 [B][cap] array of dl_p/dt_k."""
     import torch
     import paper_2501_07331_amd as snn
-    net = make_gpu_net(wl, cap, flags, max_delay) if net is None else net
+    net = make_gpu_net(wl, cap, flags, max_delay, per_proj) if net is None else net
     cap = net.record_capacity
     d = to_device(wl) if dev_in is None else dev_in
     dev = torch.device("cuda")
@@ -101,6 +110,13 @@ def run_gpu(wl: Workload, net=None, cap=None, flags=0, backward=True, max_delay=
         Is.append(I.cpu().numpy())
     out["V"] = np.concatenate(Vs, axis=1)
     out["I"] = np.concatenate(Is, axis=1)
+    if out["rc"] in (0, snn.SNN_EOVERFLOW) and recs:
+        Im = []
+        for l in net.lif_layers:
+            x = torch.zeros(B, cap, dtype=torch.float32, device=dev)
+            net.record_currents(l, x)
+            Im.append(x.cpu().numpy())
+        out["I_minus"] = np.stack(Im)
     if backward and out["rc"] == 0:
         dW = [torch.full_like(w, np.nan) for w in d["W"]]
         dD = [torch.full_like(w, np.nan) for w in d["W"]]
@@ -118,9 +134,8 @@ def run_gpu(wl: Workload, net=None, cap=None, flags=0, backward=True, max_delay=
 
 
 def grad_close(gpu, ref, rtol=1e-4, atol_rel=1e-6):
-    """|gpu - ref| <= atol_rel * max|ref| + rtol * |ref| elementwise (the abs
-    tolerance is taken relative to the tensor's scale: the gradients of a
-    batch-mean loss with a time-averaged readout are far below 1)."""
+    """|gpu - ref| <= atol_rel * max|ref| + rtol * |ref| elementwise, for
+    comparisons of GPU results with each other (batch linearity)."""
     ref = np.asarray(ref, np.float64)
     gpu = np.asarray(gpu, np.float64)
     scale = np.abs(ref).max()
@@ -131,6 +146,8 @@ def grad_close(gpu, ref, rtol=1e-4, atol_rel=1e-6):
 
 
 def assert_forward_bitexact(gpu, orc, wl):
+    """Spike counts, records (step, neuron, I- at the spike), z and the final
+    V and I equal to the oracle's, bit for bit."""
     f = orc["fwd"]
     nl = gpu["count"].shape[0]
     assert np.array_equal(gpu["count"], f.count[:nl]), "spike counts differ"
@@ -139,31 +156,35 @@ def assert_forward_bitexact(gpu, orc, wl):
             c = min(int(f.count[li, b]), f.cap)
             assert np.array_equal(gpu["step"][li, b, :c], f.step[li, b, :c]), (li, b, "steps")
             assert np.array_equal(gpu["neuron"][li, b, :c], f.neuron[li, b, :c]), (li, b, "neurons")
+            if "I_minus" in gpu:
+                assert np.array_equal(gpu["I_minus"][li, b, :c].view(np.uint32),
+                                      f.I_minus[li, b, :c].view(np.uint32)), (li, b, "I- records")
     assert np.array_equal(gpu["z"].view(np.uint32), f.z.view(np.uint32)), "readout z differs"
     assert np.array_equal(gpu["V"].view(np.uint32), f.V_final.view(np.uint32)), "final V differs"
     assert np.array_equal(gpu["I"].view(np.uint32), f.I_final.view(np.uint32)), "final I differs"
 
 
-def assert_backward_close(gpu, orc, rtol=1e-4, atol_rel=1e-6, f64_bound=1e-4, model_gap=False):
-    """GPU vs the fp32 kernel-precision model at the stated tolerance, and vs
-    the fp64 definition within f64_bound of each tensor's scale.  With
-    model_gap, the fp64 bound of a tensor is at least twice the distance of
-    the oracle's own fp32 model from its fp64 definition (fp32 adjoints lose
-    accuracy over long, spike-dense trials: about 1e-3 of scale at T = 10^4)."""
-    dW32, dD32, deg32 = orc["f32"]
-    assert gpu["stats"]["degenerate_jumps"] == deg32
-    for p in range(len(dW32)):
-        for nm, g, r in (("dW", gpu["dW"][p], dW32[p]), ("dD", gpu["dD"][p], dD32[p])):
-            ok, worst, _ = grad_close(g, r, rtol, atol_rel)
-            assert ok, f"{nm}[{p}] vs fp32 model: worst error / tolerance = {worst:.3g}"
-    if "f64" in orc:
-        dW64, dD64, _ = orc["f64"]
-        for p in range(len(dW64)):
-            for nm, g, r in (("dW", gpu["dW"][p], dW64[p]), ("dD", gpu["dD"][p], dD64[p])):
-                scale = np.abs(r).max()
-                err = np.abs(g.astype(np.float64) - r).max()
-                bound = f64_bound
-                if model_gap:
-                    m32 = (dW32 if nm == "dW" else dD32)[p]
-                    bound = max(bound, 2.0 * np.abs(m32.astype(np.float64) - r).max() / scale)
-                assert err <= bound * scale + 1e-30, f"{nm}[{p}] vs fp64: {err / scale:.3g} of scale"
+RTOL, ATOL = 1e-4, 1e-6
+
+
+def assert_backward_close(gpu, orc, rtol=RTOL, atol=ATOL):
+    """Every element of every dW and dD within atol + rtol |ref| of the
+    oracle's fp64 definition (absolute atol, not scaled), and the same count
+    of skipped degenerate jumps.  The oracle's fp32 evaluation of the same
+    expressions, where computed, is printed beside it as the noise floor."""
+    dW64, dD64, deg = orc["f64"]
+    assert gpu["stats"]["degenerate_jumps"] == deg
+    for p in range(len(dW64)):
+        for nm, g, r, i in (("dW", gpu["dW"][p], dW64[p], 0), ("dD", gpu["dD"][p], dD64[p], 1)):
+            g = np.asarray(g, np.float64)
+            tol = atol + rtol * np.abs(r)
+            err = np.abs(g - r)
+            worst = float((err / tol).max()) if err.size else 0.0
+            floor = ""
+            if "f32" in orc:
+                r32 = np.asarray(orc["f32"][i][p], np.float64)
+                floor = f", fp32 evaluation {float((np.abs(r32 - r) / tol).max()):.3g}"
+            print(f"[grad] {nm}[{p}] worst |gpu - fp64| / tol = {worst:.3g}{floor}", flush=True)
+            bad = ~(err <= tol)
+            assert not bad.any(), (f"{nm}[{p}]: {int(bad.sum())} of {bad.size} elements off the "
+                                   f"fp64 definition, worst error / tolerance {worst:.3g}")

@@ -29,16 +29,30 @@ def test_every_declared_symbol_is_exported(lib):
         assert hasattr(lib, n), n
 
 
-def test_struct_layouts_match_header():
+def test_struct_layouts_match_header(tmp_path):
+    """Every field offset and struct size of the ctypes mirror equals what a C
+    compiler makes of include/snn.h."""
+    import subprocess
     from paper_2501_07331_amd import binding as b
-    # int32 x5 + int32 flags + pointer + float (+pad); int32 x3; 3 pointers + int32 (+pad)
-    assert C.sizeof(b.snn_opts) == 40
-    assert C.sizeof(b.snn_layer) == 12
-    assert C.sizeof(b.snn_spikes_in) == 32
-    assert C.sizeof(b.snn_spikes_out) == 24
-    assert C.sizeof(b.snn_stats) == 80
-    # int32 + 7 floats; 2 pointers
-    assert C.sizeof(b.snn_optim) == 48
+    structs = [b.snn_layer, b.snn_opts, b.snn_spikes_in, b.snn_spikes_out, b.snn_stats, b.snn_optim]
+    lines = ['#include <stddef.h>', '#include <stdio.h>', '#include "snn.h"', 'int main(void) {']
+    for st in structs:
+        nm = st.__name__
+        lines.append(f'  printf("{nm} %zu\\n", sizeof({nm}));')
+        for f, _ in st._fields_:
+            lines.append(f'  printf("{nm}.{f} %zu\\n", offsetof({nm}, {f}));')
+    lines += ['  return 0;', '}']
+    src = tmp_path / "probe.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "probe"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), "-o", str(exe), str(src)], check=True)
+    got = dict(l.split() for l in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                  check=True).stdout.splitlines())
+    for st in structs:
+        nm = st.__name__
+        assert int(got[nm]) == C.sizeof(st), nm
+        for f, _ in st._fields_:
+            assert int(got[f"{nm}.{f}"]) == getattr(st, f).offset, f"{nm}.{f}"
 
 
 def _create(lib, layers, tau_m=20.0, tau_s=5.0, theta=1.0, dt=1.0, max_delay=10, **opt):
