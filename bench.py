@@ -50,8 +50,9 @@ def step_bytes(u):
 
 
 def measured_traffic(kernel):
-    """HBM bytes per launch of `kernel` from the committed counter summary, or
-    None when the kernel sources changed since the counters were taken."""
+    """HBM bytes (FETCH + WRITE, calibrated) per launch of `kernel` from the
+    committed counter summary, or None when the kernel sources changed since
+    the counters were taken."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "hbm_traffic_audio-700-256rec-20.txt")
     if not os.path.exists(path):
@@ -75,9 +76,24 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def host_cpu():
+    """CPU model name and the number of CPUs of the host."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, os.cpu_count()
+
+
 def cpu_baseline(wl, n_samples):
     """The oracle as it stands (single thread, fp64 backward) on the first
-    n_samples samples of the same workload."""
+    n_samples samples of the same workload, with this process pinned to one
+    host core for the timed call (and unpinned afterwards)."""
     import oracle
     from workloads.generators import Workload
     B = min(n_samples, wl.B)
@@ -86,20 +102,28 @@ def cpu_baseline(wl, n_samples):
                    wl.labels[:B])
     c = wl.cfg
     net = oracle.OracleNet(c.layers, c.tau_m, c.tau_s, c.theta, c.dt, c.max_delay, sub.T, c.loss,
-                           c.readout_scale)
+                           c.readout_scale, list(c.delay_range))
     cap = 64 * 256
-    t0 = time.perf_counter()
-    f = oracle.forward(net, sub.in_off, sub.in_step, sub.in_neuron, sub.W, sub.D, cap=cap)
-    lo, g = oracle.loss(f.z, sub.labels)
-    oracle.backward(net, sub.in_off, sub.in_step, sub.in_neuron, sub.W, sub.D, f, g, mode="f64")
-    dt = time.perf_counter() - t0
+    allowed = sorted(os.sched_getaffinity(0))
+    core = allowed[-1]
+    os.sched_setaffinity(0, {core})
+    try:
+        t0 = time.perf_counter()
+        f = oracle.forward(net, sub.in_off, sub.in_step, sub.in_neuron, sub.W, sub.D, cap=cap)
+        lo, g = oracle.loss(f.z, sub.labels)
+        oracle.backward(net, sub.in_off, sub.in_step, sub.in_neuron, sub.W, sub.D, f, g, mode="f64")
+        dt = time.perf_counter() - t0
+    finally:
+        os.sched_setaffinity(0, set(allowed))
     E = 0
     for (a, q) in [(0, 1), (1, 1), (1, 2)]:
         spikes = int(off[-1]) if a == 0 else int(f.count[0].sum())
         E += spikes * c.layers[q][0]
+    model, ncpu = host_cpu()
     return {"value": E / dt, "unit": "events/s", "cores": 1, "kind": "oracle",
+            "cpu_model": model, "nproc": ncpu, "cpus_allowed": len(allowed), "pinned_core": core,
             "sample": f"first {B} of the {wl.B} samples, forward + loss + fp64 backward, "
-                      f"{dt:.2f} s wall on one host core, {E} events"}
+                      f"{dt:.2f} s wall pinned to host core {core}, {E} events"}
 
 
 def copy_calibration(mib):
@@ -160,7 +184,8 @@ def sweep(args):
             dW = [torch.zeros_like(w) for w in W]
             dD = [torch.zeros_like(w) for w in W]
             net = snn.Network(c.layers, c.tau_m, c.tau_s, c.theta, c.dt, c.max_delay, wl.B, wl.T,
-                              c.loss, c.readout_scale, cap, flags=snn.SNN_FLAG_TIMING, stream=stream)
+                              c.loss, c.readout_scale, cap, flags=snn.SNN_FLAG_TIMING, stream=stream,
+                              proj_max_delay=list(c.delay_range))
             for _ in range(args.warmup):
                 net.forward(off, st, ne, W, D, labels, recs, loss)
                 net.backward(dW, dD)
@@ -240,7 +265,8 @@ def configs_bench(args):
             dW = [torch.zeros_like(w) for w in W]
             dD = [torch.zeros_like(w) for w in W]
             net = snn.Network(c.layers, c.tau_m, c.tau_s, c.theta, c.dt, c.max_delay, wl.B, wl.T,
-                              c.loss, c.readout_scale, cap, flags=snn.SNN_FLAG_TIMING, stream=stream)
+                              c.loss, c.readout_scale, cap, flags=snn.SNN_FLAG_TIMING, stream=stream,
+                              proj_max_delay=list(c.delay_range))
             el, kt = _time_steps(net, (off, st, ne, W, D, labels, recs, loss), dW, dD, args.steps,
                                  args.warmup)
             s = net.stats()
@@ -252,7 +278,8 @@ def configs_bench(args):
         byt = 34 * E + 16 * NS + 16 * sum(spikes) + 8 * s["input_spikes"]
         print(json.dumps({"sweep": "configs", "config": cid, "workload": c.name, "B": wl.B, "T": wl.T,
                           "ms_per_step": round(1e3 * el, 4), "events": E, "events_per_s": E / el,
-                          "step_alg_bytes": byt, "step_hbm_frac": round(byt / el / 1e9 / HBM_PEAK_GBS, 4),
+                          "step_alg_bytes": byt,
+                          "step_alg_bytes_frac_of_hbm_peak": round(byt / el / 1e9 / HBM_PEAK_GBS, 4),
                           "lif_spikes_per_neuron": [round(x / wl.B / n, 2) for x, n in zip(spikes, lif)],
                           "kernel_ms": kt}), flush=True)
         del net, W, D, dW, dD, recs
@@ -291,7 +318,7 @@ def losses_bench(args):
             dD = [torch.zeros_like(w) for w in W]
             net = snn.Network(c.layers, c.tau_m, c.tau_s, c.theta, c.dt, c.max_delay, wl.B, wl.T,
                               c.loss, c.readout_scale, cap, flags=snn.SNN_FLAG_TIMING, stream=stream,
-                              dmse_delta=c.dmse_delta)
+                              dmse_delta=c.dmse_delta, proj_max_delay=list(c.delay_range))
             dlp = None
             if hidden_lp:
                 dlp = [torch.full((wl.B, cap), 1e-4, device=dev)]
@@ -359,7 +386,8 @@ def main():
         dW = [torch.zeros_like(w) for w in W]
         dD = [torch.zeros_like(w) for w in W]
         net = snn.Network(c.layers, c.tau_m, c.tau_s, c.theta, c.dt, c.max_delay, wl.B, wl.T, c.loss,
-                          c.readout_scale, cap, flags=snn.SNN_FLAG_TIMING, stream=stream)
+                          c.readout_scale, cap, flags=snn.SNN_FLAG_TIMING, stream=stream,
+                          proj_max_delay=list(c.delay_range))
 
         def step():
             net.forward(off, st, ne, W, D, labels, recs, loss, z)
@@ -415,7 +443,16 @@ def main():
     dom = max(avg, key=avg.get)
     kb = kernel_bytes(u)
     ach = kb[dom] / (avg[dom] * 1e-3) / 1e9
+    # algorithmic bytes / time, as a fraction of the HBM peak (LDS- and
+    # L2-served kernels can pass 1), and the counter-measured HBM rate where
+    # the committed counters match the sources
     kernel_frac = {k: round(kb[k] / (avg[k] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4) for k in avg}
+    kernel_meas = {}
+    for k in avg:
+        tr = measured_traffic(k)
+        if tr is not None and avg[k] > 0:
+            gbs = tr / (avg[k] * 1e-3) / 1e9
+            kernel_meas[k] = {"gb_s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
     log(f"kernel ms: {avg}  step ms {ms:.3f}  events {E}  lif spikes/neuron/sample "
         f"{s['lif_spikes'] / wl.B / 256:.2f}")
     out = {
@@ -436,9 +473,11 @@ def main():
                    "events_per_step": E, "input_spikes": s["input_spikes"],
                    "lif_spikes": s["lif_spikes"],
                    "kernel_ms": {k: round(v, 4) for k, v in avg.items()},
-                   "kernel_hbm_frac": kernel_frac,
+                   "kernel_alg_bytes_frac_of_hbm_peak": kernel_frac,
+                   "kernel_measured_hbm": kernel_meas,
                    "step_alg_bytes": step_bytes(u),
-                   "step_hbm_frac": round(step_bytes(u) / (elapsed / args.steps) / 1e9 / HBM_PEAK_GBS, 4),
+                   "step_alg_bytes_frac_of_hbm_peak":
+                       round(step_bytes(u) / (elapsed / args.steps) / 1e9 / HBM_PEAK_GBS, 4),
                    "train_step_ms": round(train_ms, 4),
                    "optimizer": {"kind": "adam", "params": 2 * n_params,
                                  "ms": round(float(np.mean(opt_ms)), 4),
