@@ -60,6 +60,23 @@ def test_delay_rounding_half_even_and_clamp():
     assert f.clamped == 3
 
 
+def test_per_projection_delay_clamp():
+    """A projection's own largest delay clamps its delays (and is counted),
+    below the network-wide max_delay."""
+    D = np.array([[0.5, 1.5, 2.5, -0.7, 12.6, np.nan, 4.4, 4.6]], np.float32)
+    W = np.ones((1, 8), np.float32)
+    net = net_of(((1, INPUT, 0), (8, LI, 0)), T=30, max_delay=10)
+    net.proj_max_delay = [4]
+    off, st, ne = one_sample_csr([(0, 0)])
+    f = oracle.forward(net, off, st, ne, [W], [D], trace=True)
+    first = [int(np.nonzero(f.V_trace[0, :, j])[0][0]) - 1 for j in range(8)]
+    assert first == [0, 2, 2, 0, 4, 0, 4, 4]
+    assert f.clamped == 4
+    net.proj_max_delay = [11]          # beyond max_delay: refused
+    with pytest.raises(ValueError):
+        oracle.forward(net, off, st, ne, [W], [D])
+
+
 # ---------------------------------------------------------------- P-1 closed-form PSP
 
 
@@ -127,7 +144,112 @@ def test_subthreshold_dw_dd_closed_forms(mode):
     assert deg == 0
 
 
+def test_max_readout_subthreshold_closed_forms():
+    """LI only, max-over-time readout, linear loss L = sum_k c_k z_k: the loss
+    source sits at the first maximiser n* = m + k* (k* maximises kappa(k dt)),
+    so dW_k = c_k kappa(k* dt) and dD_k (per step, the right-derivative in the
+    arrival time) = -w_k c_k kappa'(k* dt) dt, exactly on the grid; a source
+    one step early or late gives kappa((k* -+ 1) dt) instead.  An output whose
+    voltage never rises above 0 keeps n* = 0 (strict >) and a zero gradient."""
+    T, s0 = 60, 3
+    net = net_of(((1, INPUT, 0), (2, LI, 0)), T=T, max_delay=10, loss=LOSS_CE_MAX, scale=1.0)
+    off, st, ne = one_sample_csr([(s0, 0)])
+    w = np.array([[0.7, -0.4]], np.float32)
+    W, D = [w], [np.array([[5.0, 2.0]], np.float32)]
+    f = oracle.forward(net, off, st, ne, W, D)
+    c = np.array([[1.0, -0.5]], np.float32)
+    dW, dD, deg = oracle.backward(net, off, st, ne, W, D, f, c)
+    ks = max(range(1, T), key=lambda k: kappa(float(k)))
+    assert ks == 9 and int(f.nstar[0, 0]) == s0 + 5 + ks and int(f.nstar[0, 1]) == 0
+    assert abs(dW[0][0, 0] - kappa(ks)) <= 1e-12 * kappa(ks)
+    ref_d = -float(w[0, 0]) * dkappa(ks)
+    assert abs(dD[0][0, 0] - ref_d) <= 1e-10 * abs(ref_d)
+    assert dW[0][0, 1] == 0.0 and dD[0][0, 1] == 0.0
+    for k in (ks - 1, ks + 1):          # what a misplaced source would give
+        assert abs(kappa(k) - kappa(ks)) > 1e-4 * kappa(ks)
+
+
 # ---------------------------------------------------------------- P-5 grid -> continuous
+
+
+def _grid_vs_continuous(layers, projs, inp, T_ms, dt, loss, c):
+    """Grid oracle gradients (fp64) of L = sum_k c_k z_k on the continuous net's
+    parameters: z the sum readout with scale dt (so z ~ the integral of V) or
+    the max readout; delays and input times on the grid, dD per ms."""
+    T = int(round(T_ms / dt))
+    md = max(int(round(float(np.max(d)) / dt)) for _, _, _, d in projs)
+    net = oracle.OracleNet(layers, TM, TS, 1.0, dt, md, T, loss, dt)
+    off, st, ne = one_sample_csr([(int(round(t / dt)), i) for t, i in inp])
+    W = [np.array(w, np.float32) for _, _, w, _ in projs]
+    D = [np.array(np.round(np.array(d) / dt), np.float32) for _, _, _, d in projs]
+    f = oracle.forward(net, off, st, ne, W, D)
+    dW, dD, _ = oracle.backward(net, off, st, ne, W, D, f, np.array([c], np.float32))
+    return dW, [x / dt for x in dD], f
+
+
+def _tensor_err(grid, cont):
+    """max |grid - cont| / max |cont| per tensor (absolute where cont is 0)."""
+    out = []
+    for g, r in zip(grid, cont):
+        r = np.asarray(r, np.float64)
+        sc = np.abs(r).max()
+        out.append(np.abs(np.asarray(g) - r).max() / (sc if sc > 0 else 1.0))
+    return out
+
+
+def test_recurrent_delays_grid_converges_to_continuous():
+    """Two recurrent LIF neurons with recurrent delays and two LI readouts
+    (13 hidden spikes in 40 ms, the first cut of the continuous net of the
+    recurrent FD test before a grazing crossing at 45 ms): every dW and dD of
+    the three projections approaches continuous EventProp at first order in
+    dt, which pins the recurrent adjoint ring and the jump sums over
+    recurrent arrivals."""
+    W_in, D_in = [[6.0, 4.5], [3.0, 7.0]], [[1.3, 4.1], [2.2, 0.7]]
+    W_rec, D_rec = [[0.0, 2.5], [1.8, 0.0]], [[0.5, 3.3], [6.1, 1.1]]
+    W_out, D_out = [[1.2, -0.7], [0.4, 0.9]], [[2.5, 0.9], [3.7, 5.2]]
+    projs = [(0, 1, W_in, D_in), (1, 1, W_rec, D_rec), (1, 2, W_out, D_out)]
+    inp = [(0.5, 0), (3.1, 1), (9.4, 0), (17.2, 1)]
+    c = [0.8, -1.3]
+    T = 40.0
+    cont = ContNet([2, 2, 2], projs, T=T)
+    L, rec = cont.forward(inp, "integral", c)
+    assert len(rec["spikes"]) == 13
+    cW, cD = cont.backward(inp, rec)
+    worst = []
+    for dt in (0.1, 0.05, 0.025):
+        gW, gD, f = _grid_vs_continuous(((2, INPUT, 0), (2, LIF, 1), (2, LI, 0)), projs, inp, T, dt,
+                                        LOSS_CE_SUM, c)
+        assert int(f.count.sum()) == 13
+        worst.append(max(_tensor_err(gW, cW) + _tensor_err(gD, cD)))
+    worst = np.array(worst)
+    assert np.all(worst[:-1] / worst[1:] > 1.6), worst
+    assert worst[-1] < 0.1, worst
+
+
+def test_max_readout_grid_converges_to_continuous():
+    """One hidden spike into two LI readouts, max-over-time loss: the readout
+    weights' gradients (the PSP value at the maximum) match continuous
+    EventProp to 1e-3 at dt <= 0.1 ms, and the gradients that vanish in
+    continuous time (a shift of the hidden spike or of an arrival only moves
+    the maximum) shrink with dt."""
+    W_in, D_in = [[9.0]], [[1.5]]
+    W_out, D_out = [[1.1, 0.6]], [[2.0, 6.5]]
+    projs = [(0, 1, W_in, D_in), (1, 2, W_out, D_out)]
+    inp = [(2.0, 0)]
+    c = [1.0, -0.5]
+    cont = ContNet([1, 1, 2], projs, T=60.0)
+    L, rec = cont.forward(inp, "max", c)
+    cW, cD = cont.backward(inp, rec)
+    ro = np.asarray(cW[1], np.float64)
+    zero = [np.asarray(cW[0]), np.asarray(cD[0]), np.asarray(cD[1])]
+    assert all(np.abs(z).max() < 1e-12 for z in zero)
+    vanish = []
+    for dt in (0.1, 0.05):
+        gW, gD, _ = _grid_vs_continuous(((1, INPUT, 0), (1, LIF, 0), (2, LI, 0)), projs, inp, 60.0,
+                                        dt, LOSS_CE_MAX, c)
+        assert np.abs(gW[1] - ro).max() <= 1e-3 * np.abs(ro).max()
+        vanish.append(max(np.abs(gW[0]).max(), np.abs(gD[0]).max(), np.abs(gD[1]).max()))
+    assert vanish[1] < vanish[0] / 2 and vanish[0] < 1e-3 * np.abs(ro).max()
 
 
 def test_grid_converges_to_continuous_eventprop():
