@@ -122,6 +122,22 @@ typedef struct {
  *                   on hip_stream (reported by snn_get_stats)
  * hip_stream:       hipStream_t to enqueue on (NULL: default stream)
  * dmse_delta:       Delta_t of the spike-time loss, in ms (SNN_LOSS_DMSE)
+ * reg_strength:     host array of one strength rho_l >= 0 per LIF layer (in
+ *                   layer order), or NULL: the hidden spike-count
+ *                   regulariser with target reg_target (spikes per neuron and
+ *                   sample) that the Results apply to the hidden layers of
+ *                   the SHD/SSC/Braille models (a target of 14 spikes per
+ *                   example, a layer-wise strength).  With cbar_i the
+ *                   batch-mean spike count of neuron i of layer l, the
+ *                   penalty R = sum_l (rho_l / 2) sum_i (cbar_i - reg_target)^2
+ *                   is reported as snn_stats.reg_loss, and every spike k of
+ *                   neuron i adds dl_p/dt_k = -rho_l (cbar_i - reg_target) / B
+ *                   to the numerator of its lambda_V jump (Table 1 backward
+ *                   transition): the gradient, with the counts held fixed,
+ *                   of -(rho_l / B) sum_i (cbar_i - reg_target) sum_k t_k,
+ *                   which moves the spikes of an over-active neuron later and
+ *                   those of an under-active one earlier; read during
+ *                   snn_create only
  */
 #define SNN_FLAG_HBM_RINGS 1
 #define SNN_FLAG_TIMING 2
@@ -134,6 +150,8 @@ typedef struct {
     void* hip_stream;
     float dmse_delta;
     const int32_t* proj_max_delay;
+    float reg_target;
+    const float* reg_strength;
 } snn_opts;
 
 /* Input spikes, CSR over samples (dev): offsets [batch+1] with offsets[0] = 0
@@ -170,6 +188,7 @@ typedef struct {
      * input_scan, forward_core, readout_forward (forward); readout_adjoint,
      * backward_core, group, gradients (backward) */
     float kernel_ms[8];
+    double reg_loss;           /* spike-count penalty R of the last forward (0 if off) */
 } snn_stats;
 
 /*

@@ -7,13 +7,14 @@ library never imports it.
 
 * ``snn_oracle.c`` (built into ``liboracle.so`` by ``oracle/build.py``): the
   plain single-threaded grid forward (fp32), CE loss (fp64) and backward
-  (fp64 definition, or the fp32 kernel-precision model).
+  (fp64 definition, or an fp32 evaluation of it as a noise floor); the
+  spike-count regulariser's per-spike terms (``grid.spike_count_reg``).
 * ``continuous.py``: an fp64 event-driven simulator of the continuous-time
   system of Table 1 for tiny networks, with the exact EventProp backward and
   a finite-difference check; it pins the grid oracle.
 """
 from .grid import (OracleNet, constants, forward, loss, loss_dmse, first_spike_dlp, backward,
-                   lib_path, ForwardResult, LOSS_DMSE)
+                   spike_count_reg, lib_path, ForwardResult, LOSS_DMSE)
 
 __all__ = ["OracleNet", "constants", "forward", "loss", "loss_dmse", "first_spike_dlp", "backward",
-           "lib_path", "ForwardResult", "LOSS_DMSE"]
+           "spike_count_reg", "lib_path", "ForwardResult", "LOSS_DMSE"]

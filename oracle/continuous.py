@@ -16,8 +16,13 @@ with per-readout weights c_k:
                times t_i of a LIF output layer (T if none; c the label), the
                time-invariant MSE of the Methods (a spike-time loss l_p)
 and optionally a spike-time term coef_l * t_k for every spike of a chosen
-LIF layer l (lp_lin = {l: coef_l}).  A spike-time loss adds dl_p/dt_k to the
-numerator of the jump at spike k (Table 1 backward transition).
+LIF layer l (lp_lin = {l: coef_l}), and the spike-count regulariser
+(spike_reg = {l: (rho, nu)}) read on one sample: with c_i the spike count of
+neuron i of layer l in this run, the term -rho (c_i - nu) t_k for every spike
+k of neuron i (c_i is constant under the small parameter steps of the finite
+differences, so this is the function whose gradient the regulariser's jump
+terms are).  A spike-time loss adds dl_p/dt_k to the numerator of the jump
+at spike k (Table 1 backward transition).
 
 Backward (Table 1 and the Methods): between events the adjoints obey
 tau_m lambda_V' = -lambda_V - dl_V/dV and tau_s lambda_I' = -lambda_I + lambda_V
@@ -109,11 +114,12 @@ class ContNet:
     # ----- forward --------------------------------------------------------------------
     def forward(self, in_spikes: Sequence[Tuple[float, int]], loss: str = "integral",
                 c: Sequence[float] = None, label: int = 0, delta: float = 0.0,
-                lp_lin: Dict[int, float] = None):
+                lp_lin: Dict[int, float] = None, spike_reg: Dict[int, Tuple[float, float]] = None):
         """in_spikes: (time, input neuron).  Returns (L, record) with record the
         spike list [(t, layer, neuron, I_minus)] and the readout t_max list."""
         assert (loss == "dmse") == self.out_lif
         lp_lin = {} if lp_lin is None else dict(lp_lin)
+        spike_reg = {} if spike_reg is None else dict(spike_reg)
         L_ = self.L
         out = L_ - 1
         c = [1.0] * self.sizes[out] if c is None else list(c)
@@ -183,8 +189,15 @@ class ContNet:
             Lval = 0.5 * sum((first[i] - first[label] - delta) ** 2
                              for i in range(self.sizes[out]) if i != label)
         Lval += sum(lp_lin.get(l, 0.0) * ts_ for (ts_, l, _, _) in spikes)
+        counts = {l: [0] * self.sizes[l] for l in spike_reg}
+        for (_, l, j, _) in spikes:
+            if l in counts:
+                counts[l][j] += 1
+        reg_coef = {l: [-rho * (counts[l][j] - nu) for j in range(self.sizes[l])]
+                    for l, (rho, nu) in spike_reg.items()}
+        Lval += sum(reg_coef[l][j] * ts_ for (ts_, l, j, _) in spikes if l in reg_coef)
         return Lval, {"spikes": spikes, "tmax": tmax, "c": c, "loss": loss, "first": first,
-                      "label": label, "delta": delta, "lp_lin": lp_lin}
+                      "label": label, "delta": delta, "lp_lin": lp_lin, "reg_coef": reg_coef}
 
     # ----- backward -------------------------------------------------------------------
     def backward(self, in_spikes, rec):
@@ -219,11 +232,14 @@ class ContNet:
         # spike of each output neuron, and the linear spike-time terms
         dlp = [0.0] * len(allspk)
         lp_lin = rec.get("lp_lin", {})
+        reg_coef = rec.get("reg_coef", {})
         seen = set()
         for k, (tk, l, i, _) in enumerate(allspk):
             if l == 0:
                 continue
             dlp[k] += lp_lin.get(l, 0.0)
+            if l in reg_coef:
+                dlp[k] += reg_coef[l][i]
             if loss == "dmse" and l == out and i not in seen:
                 seen.add(i)
                 f, lab, dl = rec["first"], rec["label"], rec["delta"]

@@ -215,6 +215,36 @@ def first_spike_dlp(net: OracleNet, fwd: ForwardResult, dl: np.ndarray) -> np.nd
     return out
 
 
+def spike_count_reg(net: OracleNet, fwd: ForwardResult, strength: Sequence[float],
+                    target: float):
+    """Hidden spike-count regulariser (Results, SHD/SSC/Braille: a target
+    number of spikes per example and a layer-wise strength), read as: with
+    cbar_i the batch-mean spike count of neuron i of LIF layer l, the penalty
+    R = sum_l strength_l / 2 sum_i (cbar_i - target)^2, and every recorded
+    spike of neuron i carries dl_p/dt_k = -strength_l (cbar_i - target) / B
+    into its jump.  Returns (R, dlp [n_lif][B][cap] fp64)."""
+    nl = max(net.n_lif, 1)
+    B, cap = fwd.count.shape[1], fwd.cap
+    sizes = [l[0] for l in net.layers if l[1] == 1]
+    dlp = np.zeros((nl, B, cap), np.float64)
+    R = 0.0
+    for li, n in enumerate(sizes):
+        rho = float(strength[li])
+        if rho == 0.0:
+            continue
+        counts = np.zeros(n, np.int64)
+        for b in range(B):
+            c = min(int(fwd.count[li, b]), cap)
+            np.add.at(counts, fwd.neuron[li, b, :c], 1)
+        cbar = counts / float(B)
+        R += 0.5 * rho * float(np.sum((cbar - target) ** 2))
+        term = -rho * (cbar - target) / float(B)
+        for b in range(B):
+            c = min(int(fwd.count[li, b]), cap)
+            dlp[li, b, :c] = term[fwd.neuron[li, b, :c]]
+    return R, dlp
+
+
 def backward(net: OracleNet, in_off, in_step, in_neuron, W: Sequence[np.ndarray],
              D: Sequence[np.ndarray], fwd: ForwardResult, g: np.ndarray, mode: str = "f64",
              dlp: Optional[np.ndarray] = None):

@@ -36,7 +36,8 @@ class snn_opts(C.Structure):
     _fields_ = [("batch", C.c_int32), ("T", C.c_int32), ("loss", C.c_int32),
                 ("readout_scale", C.c_float), ("record_capacity", C.c_int32),
                 ("flags", C.c_int32), ("hip_stream", C.c_void_p), ("dmse_delta", C.c_float),
-                ("proj_max_delay", C.c_void_p)]
+                ("proj_max_delay", C.c_void_p), ("reg_target", C.c_float),
+                ("reg_strength", C.c_void_p)]
 
 
 class snn_spikes_in(C.Structure):
@@ -52,7 +53,7 @@ class snn_stats(C.Structure):
     _fields_ = [("input_spikes", C.c_int64), ("lif_spikes", C.c_int64), ("events", C.c_int64),
                 ("clamped_delays", C.c_int64), ("degenerate_jumps", C.c_int64),
                 ("overflow", C.c_int32), ("lds_rings", C.c_int32),
-                ("kernel_ms", C.c_float * 8)]
+                ("kernel_ms", C.c_float * 8), ("reg_loss", C.c_double)]
 
 
 class snn_optim(C.Structure):
@@ -139,7 +140,8 @@ class Network:
     def __init__(self, layers: Sequence[Tuple[int, int, int]], tau_m: float, tau_s: float,
                  theta: float, dt: float, max_delay: int, batch: int, T: int, loss: int,
                  readout_scale: float, record_capacity: int, flags: int = 0, stream=None,
-                 dmse_delta: float = 0.0, proj_max_delay: Optional[Sequence[int]] = None):
+                 dmse_delta: float = 0.0, proj_max_delay: Optional[Sequence[int]] = None,
+                 reg_strength: Optional[Sequence[float]] = None, reg_target: float = 14.0):
         import torch
         self._lib = load_library()
         self.layers = [tuple(int(x) for x in l) for l in layers]
@@ -153,9 +155,16 @@ class Network:
         self.proj_max_delay = None if proj_max_delay is None else [int(x) for x in proj_max_delay]
         pmd = (C.c_int32 * len(self.proj_max_delay))(*self.proj_max_delay) \
             if self.proj_max_delay is not None else None
+        self.reg_strength = None if reg_strength is None else [float(x) for x in reg_strength]
+        n_lif = sum(1 for l in self.layers if l[1] == SNN_LIF)
+        if self.reg_strength is not None and len(self.reg_strength) != n_lif:
+            raise ValueError(f"reg_strength needs one value per LIF layer ({n_lif})")
+        rs = (C.c_float * len(self.reg_strength))(*self.reg_strength) \
+            if self.reg_strength is not None else None
         opts = snn_opts(self.batch, self.T, int(loss), float(readout_scale), self.record_capacity,
                         int(flags), C.c_void_p(stream.cuda_stream), float(dmse_delta),
-                        C.cast(pmd, C.c_void_p) if pmd is not None else None)
+                        C.cast(pmd, C.c_void_p) if pmd is not None else None, float(reg_target),
+                        C.cast(rs, C.c_void_p) if rs is not None else None)
         h = C.c_void_p()
         rc = self._lib.snn_create(arr, len(layers), tau_m, tau_s, theta, dt, int(max_delay),
                                   C.byref(opts), C.byref(h))

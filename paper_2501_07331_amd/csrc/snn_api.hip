@@ -55,6 +55,11 @@ struct snn_net {
     Topo t;
     float tau_m, tau_s, theta, dt;
     double alpha64, beta64, cc64;   // backward propagators, fp64
+    int reg_on;                     // spike-count regulariser on some LIF layer
+    double reg_rho[SNN_MAX_LIF];    // its strength per LIF layer
+    double reg_nu;                  // its target spikes per neuron and sample
+    int* ncount;                    // [lif_total] spikes per neuron over the batch
+    double* nterm;                  // [lif_total] regulariser jump term per neuron
     float dmse_delta;
     int max_delay;
     int core_threads;           // LIF-core workgroup size
@@ -145,7 +150,8 @@ static void free_all(snn_net* n) {
                     n->rec_idx, n->rec_cnt, n->rec_goff, n->rec_gstep, n->z,      n->nstar,
                     n->src,     n->Vf,      n->If,       n->table,     n->tr_lif, n->tr_out,
                     n->A2,       n->in_goff,   n->in_gstep, n->st,
-                    n->gpart,   n->ws,      n->steptab, n->mom,   n->xlp_out};
+                    n->gpart,   n->ws,      n->steptab, n->mom,   n->xlp_out, n->ncount,
+                    n->nterm};
     for (void* p : bufs)
         if (p) (void)hipFree(p);
     for (int p = 0; p < SNN_MAXP; ++p)
@@ -192,6 +198,8 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
                  opts->record_capacity < 1))
         return SNN_EINVAL;
     if (opts->flags & ~(SNN_FLAG_HBM_RINGS | SNN_FLAG_TIMING)) return SNN_EINVAL;
+    if (opts->reg_strength && (!(opts->reg_target >= 0.0f) || isinf(opts->reg_target)))
+        return SNN_EINVAL;
     for (int l = 0; l < n_layers; ++l) {
         const snn_layer& y = layers[l];
         if (y.n < 1) return SNN_EINVAL;
@@ -288,6 +296,19 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         t.dmax[p] = dm;
         t.Sp[p] = dm + 1;
     }
+    // spike-count regulariser strengths, one per LIF layer
+    for (int li = 0; li < t.n_lif && opts->reg_strength; ++li) {
+        const float r = opts->reg_strength[li];
+        if (!(r >= 0.0f) || isinf(r)) {
+            snprintf(g_create_err, sizeof(g_create_err),
+                     "snn_create: reg_strength[%d] must be finite and >= 0", li);
+            free(net);
+            return SNN_EINVAL;
+        }
+        net->reg_rho[li] = (double)r;
+        if (r > 0.0f) net->reg_on = 1;
+    }
+    net->reg_nu = (double)opts->reg_target;
     for (int l = 0; l < n_layers; ++l) t.Sb[l] = 0;
     for (int p = 0; p < t.P; ++p)
         if (t.pre[p] != 0 && t.kind[t.post[p]] == SNN_LIF)
@@ -469,6 +490,16 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     if (net->grad_SB > 1) ALLOC(net->gpart, (size_t)net->grad_SB * 2 * (size_t)net->n_params);
     if (feed != 0 && !t.out_lif) ALLOC(net->A2, B * cap);
     if (t.out_lif) ALLOC(net->xlp_out, B * cap);
+    if (net->reg_on) {
+        ALLOC(net->ncount, (size_t)t.lif_total);
+        ALLOC(net->nterm, (size_t)t.lif_total);
+        // summed jump terms of the regularised layers (the layer feeding an
+        // LI readout adds them into its readout part in place)
+        for (int l = 1; l < n_layers; ++l) {
+            if (t.kind[l] != SNN_LIF || net->reg_rho[t.lif[l]] == 0.0) continue;
+            if (!(!t.out_lif && l == feed)) ALLOC(net->jx[t.lif[l]], B * cap);
+        }
+    }
     ALLOC(net->in_goff, B * (t.n_in + 1));
     ALLOC(net->st, 1);
 #undef ALLOC
@@ -598,6 +629,7 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
     sa.st = net->st;
     TIMED(net, K_SCAN, launch_input_scan(sa, net->lds_scan, s));
 
+    if (net->reg_on) HIP_TRY(net, launch_zero_ints(net->ncount, t.lif_total, s));
     if (t.n_lif > 0) {
         CoreFwdArgs a{};
         a.B = t.B;
@@ -663,6 +695,7 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
             y.rec_idx = net->rec_idx + li * B * (size_t)(t.T + 1);
             y.rec_cnt = net->rec_cnt + li * B;
             y.steptab = net->steptab + li * B * (size_t)t.T * SNN_STEP_ROW;
+            y.ncount = net->reg_on ? net->ncount + t.lif_off[l] : nullptr;
             y.out_count = records[li].count;
             y.out_step = records[li].step;
             y.out_neuron = records[li].neuron;
@@ -673,6 +706,22 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
         a.st = net->st;
         a.mask_off = net->mask_off;
         TIMED(net, K_CORE, launch_forward_core(a, t.n_lif, net->core_threads, net->lds_core_f, s));
+    }
+    if (net->reg_on) {
+        RegArgs ra{};
+        ra.nl = t.n_lif;
+        ra.B = t.B;
+        ra.nu = net->reg_nu;
+        ra.st = net->st;
+        for (int l = 1; l < t.L; ++l) {
+            if (t.kind[l] != SNN_LIF) continue;
+            const int li = t.lif[l];
+            ra.n[li] = t.n[l];
+            ra.rho[li] = net->reg_rho[li];
+            ra.ncount[li] = net->ncount + t.lif_off[l];
+            ra.nterm[li] = net->nterm + t.lif_off[l];
+        }
+        HIP_TRY(net, launch_spike_reg(ra, s));
     }
     if (t.out_lif) {
         // spike-time loss on the first spikes of the LIF output layer
@@ -711,6 +760,7 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
     if (rc) return rc;
     net->stats.input_spikes = in->nnz;
     net->stats.clamped_delays = (int64_t)h.clamped;
+    net->stats.reg_loss = h.reg_loss;
     net->stats.overflow = h.overflow;
     for (int p = 0; p < t.P; ++p)
         if (t.fring[p] >= 0) net->stats.lds_rings |= 1 << p;
@@ -844,13 +894,18 @@ static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW
     // (the layer feeding an LI readout), the spike-time loss's terms (LIF
     // output layer), plus the caller's dl_p/dt
     const double* jump_x[SNN_MAX_LIF] = {nullptr};
+    // and the spike-count regulariser's term of each record's neuron
     for (int l = 1; l < t.L; ++l) {
         if (t.kind[l] != SNN_LIF) continue;
         const int li = t.lif[l];
         const double* own = (!t.out_lif && l == feed) ? net->A2 : (t.out_lif && l == t.out_l) ? net->xlp_out : nullptr;
-        if (has_lp[li]) {
+        const bool reg = net->reg_on && net->reg_rho[li] != 0.0;
+        if (has_lp[li] || reg) {
             double* dst = (own == net->A2 && own) ? net->A2 : net->jx[li];
-            HIP_TRY(net, launch_add_lp(dst, own, dlp[li], net->rec_cnt + (size_t)li * B, t.B, t.cap, s));
+            HIP_TRY(net, launch_add_lp(dst, own, has_lp[li] ? dlp[li] : nullptr,
+                                       reg ? net->nterm + t.lif_off[l] : nullptr,
+                                       net->rec_n + (size_t)li * B * cap,
+                                       net->rec_cnt + (size_t)li * B, t.B, t.cap, s));
             jump_x[li] = dst;
         } else {
             jump_x[li] = own;

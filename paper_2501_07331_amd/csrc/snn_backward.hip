@@ -719,16 +719,18 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
     }
 }
 
-// Extra jump numerator of every record of a LIF layer: dst = base + dlp
-// (either may be absent), for the stored records of each sample.
-__global__ void add_lp_kernel(double* dst, const double* base, const float* dlp, const int* cnt,
-                              int B, int cap) {
+// Extra jump numerator of every record of a LIF layer: dst = base + dlp +
+// nterm[neuron of the record] (each may be absent), for the stored records of
+// each sample.
+__global__ void add_lp_kernel(double* dst, const double* base, const float* dlp, const double* nterm,
+                              const int* rec_n, const int* cnt, int B, int cap) {
     const int b = blockIdx.y;
     const int r = blockIdx.x * blockDim.x + threadIdx.x;
     if (b >= B || r >= min(cnt[b], cap)) return;
     const size_t k = (size_t)b * cap + r;
     double v = base ? base[k] : 0.0;
     if (dlp) v += (double)dlp[k];
+    if (nterm) v += nterm[rec_n[k]];
     dst[k] = v;
 }
 
@@ -829,11 +831,11 @@ hipError_t launch_gradients(const GradArgs& a, int J, int KL, int threads, size_
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_add_lp(double* dst, const double* base, const float* dlp, const int* cnt, int B,
-                         int cap, hipStream_t s) {
+hipError_t launch_add_lp(double* dst, const double* base, const float* dlp, const double* nterm,
+                         const int* rec_n, const int* cnt, int B, int cap, hipStream_t s) {
     if (B <= 0 || cap <= 0) return hipSuccess;
     hipLaunchKernelGGL(add_lp_kernel, dim3(grid_for(cap, 256), B), dim3(256), 0, s, dst, base, dlp,
-                       cnt, B, cap);
+                       nterm, rec_n, cnt, B, cap);
     return hipGetLastError();
 }
 

@@ -12,6 +12,7 @@ __global__ void reset_status_kernel(DevStatus* st) {
         st->overflow = 0;
         st->clamped = 0;
         st->degenerate = 0;
+        st->reg_loss = 0.0;
         for (int l = 0; l < SNN_MAX_LAYERS; ++l) st->layer_spikes[l] = 0;
     }
 }
@@ -470,6 +471,37 @@ __global__ void dmse_mean_kernel(const float* z, const int* labels, int B, int C
     loss_out[B] = (float)(tot / (double)B);
 }
 
+__global__ void zero_ints_kernel(int* p, long long n) {
+    const long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (g < n) p[g] = 0;
+}
+
+// Spike-count regulariser (one workgroup of 256): the per-neuron jump term
+// -rho (cbar - nu) / B and the penalty sum_l (rho_l / 2) sum_i (cbar_i -
+// nu)^2, cbar the neuron's spikes per sample over the batch, in fp64; each
+// thread sums a fixed strided set of neurons, then a fixed-order tree.
+__global__ void __launch_bounds__(256) spike_reg_kernel(RegArgs a) {
+    __shared__ double part[256];
+    if (a.st->bad_input) return;
+    const int tid = threadIdx.x;
+    double acc = 0.0;
+    for (int l = 0; l < a.nl; ++l) {
+        if (a.rho[l] == 0.0) continue;
+        for (int i = tid; i < a.n[l]; i += 256) {
+            const double e = (double)a.ncount[l][i] / (double)a.B - a.nu;
+            a.nterm[l][i] = -a.rho[l] * e / (double)a.B;
+            acc += 0.5 * a.rho[l] * e * e;
+        }
+    }
+    part[tid] = acc;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (tid < w) part[tid] += part[tid + w];
+        __syncthreads();
+    }
+    if (tid == 0) a.st->reg_loss = part[0];
+}
+
 __global__ void copy_state_kernel(const float* src, int stride, int off, int n, int B, float* dst) {
     const long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (g >= (long long)B * n) return;
@@ -546,6 +578,17 @@ hipError_t launch_dmse_loss(const int* rec_cnt, const int* rec_s, const int* rec
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(dmse_mean_kernel, dim3(1), dim3(64), 0, s, z, labels, B, C, delta, loss_out, st);
+    return hipGetLastError();
+}
+
+hipError_t launch_zero_ints(int* p, long long n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(zero_ints_kernel, dim3(grid_for(n, 256)), dim3(256), 0, s, p, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_spike_reg(const RegArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL(spike_reg_kernel, dim3(1), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

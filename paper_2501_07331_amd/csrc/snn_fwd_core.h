@@ -40,6 +40,7 @@ struct FwdCore {
     struct Lane {
         float V[NL], I[NL];
         int cnt[NL];                          // records so far (exact; may pass the capacity)
+        int own[NL];                          // spikes of this lane's neuron
     };
 
     template <typename Ptr>
@@ -210,6 +211,7 @@ struct FwdCore {
                 row[1] = min(cnt0[l], a.cap);
             }
             if (spk[l]) {
+                ++L.own[l];
                 if (rank[l] < SNN_STEP_IDS) row[2 + rank[l]] = tid;
                 const int pos = cnt0[l] + rank[l];
                 if (pos < a.cap) {
@@ -279,6 +281,7 @@ struct FwdCore {
             L.V[l] = 0.0f;
             L.I[l] = 0.0f;
             L.cnt[l] = 0;
+            L.own[l] = 0;
         }
         __syncthreads();
         run_steps(a, b, tid, L);
@@ -290,6 +293,8 @@ struct FwdCore {
             if (tid < y.n) {
                 a.Vf[(size_t)b * a.nstate + a.soff[l] + tid] = L.V[l];
                 a.If[(size_t)b * a.nstate + a.soff[l] + tid] = L.I[l];
+                // integer sums over the samples: exact in any order
+                if (y.ncount && L.own[l]) atomicAdd(&y.ncount[tid], L.own[l]);
             }
             if (tid == 0) {
                 y.rec_idx[(size_t)b * (a.T + 1) + a.T] = min(L.cnt[l], a.cap);

@@ -22,6 +22,7 @@ struct DevStatus {
     unsigned long long clamped;      // delays clamped while rounding
     unsigned long long degenerate;   // skipped jumps (I- <= theta)
     unsigned long long layer_spikes[SNN_MAX_LAYERS];   // per LIF layer, all samples
+    double reg_loss;                 // spike-count penalty of the last forward
 };
 
 // Topology, constants and the LDS plan, passed by value to every kernel.
@@ -90,6 +91,7 @@ struct FwdLayer {
     int* rec_idx;                      // [B][T+1] first record of each step
     int* rec_cnt;                      // [B]
     int* steptab;                      // [B][T][SNN_STEP_ROW]
+    int* ncount;                       // [n] spikes per neuron over the batch (added), or NULL
     int* out_count;                    // caller's records: [B], [B][cap], [B][cap]
     int* out_step;
     int* out_neuron;
@@ -263,8 +265,22 @@ hipError_t launch_optimizer(const OptArgs& a, hipStream_t s);
 hipError_t launch_dmse_loss(const int* rec_cnt, const int* rec_s, const int* rec_n, int cap,
                             const int* labels, int B, int C, int T, float dt, float delta, float* z,
                             float* loss_out, double* xlp, const DevStatus* st, hipStream_t s);
-hipError_t launch_add_lp(double* dst, const double* base, const float* dlp, const int* cnt, int B,
-                         int cap, hipStream_t s);
+hipError_t launch_add_lp(double* dst, const double* base, const float* dlp, const double* nterm,
+                         const int* rec_n, const int* cnt, int B, int cap, hipStream_t s);
+// Spike-count regulariser: per LIF layer l with rho[l] != 0 and neuron i,
+// cbar = ncount[i] / B, nterm[i] = -rho (cbar - nu) / B, and the penalty
+// sum (rho / 2) (cbar - nu)^2 into st->reg_loss.
+struct RegArgs {
+    int nl, B;
+    int n[SNN_MAX_LIF];
+    double rho[SNN_MAX_LIF];
+    const int* ncount[SNN_MAX_LIF];
+    double* nterm[SNN_MAX_LIF];
+    double nu;
+    DevStatus* st;
+};
+hipError_t launch_spike_reg(const RegArgs& a, hipStream_t s);
+hipError_t launch_zero_ints(int* p, long long n, hipStream_t s);
 hipError_t set_forward_lds_limits(size_t bytes, int* bad);
 hipError_t set_core_lds_limits(size_t bytes, int* bad);
 bool launch_forward_core_256(const CoreFwdArgs& a, int n_lif, int np, bool rl, int threads,

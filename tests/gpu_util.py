@@ -30,8 +30,9 @@ def oracle_net(wl: Workload, max_delay=None, per_proj=True):
 
 
 def run_oracle(wl: Workload, cap=None, modes=("f64", "f32"), max_delay=None, dlp=None,
-               per_proj=True):
-    """dlp: extra per-record dl_p/dt_k [n_lif][B][cap] (fp64) or None."""
+               per_proj=True, reg=None):
+    """dlp: extra per-record dl_p/dt_k [n_lif][B][cap] (fp64) or None; reg:
+    (strength per LIF layer, target) of the spike-count regulariser or None."""
     cap = default_cap(wl) if cap is None else cap
     net = oracle_net(wl, max_delay, per_proj)
     f = oracle.forward(net, wl.in_off, wl.in_step, wl.in_neuron, wl.W, wl.D, cap=cap)
@@ -44,6 +45,12 @@ def run_oracle(wl: Workload, cap=None, modes=("f64", "f32"), max_delay=None, dlp
         lo, g = oracle.loss(f.z, wl.labels)
         x = dlp
     out = {"fwd": f, "loss": lo, "g": g}
+    if reg is not None:
+        # the parameter values the library receives (fp32 in its options)
+        R, rd = oracle.spike_count_reg(net, f, [float(np.float32(x)) for x in reg[0]],
+                                       float(np.float32(reg[1])))
+        out["reg_loss"] = R
+        x = rd if x is None else x + rd
     for m in modes:
         dW, dD, deg = oracle.backward(net, wl.in_off, wl.in_step, wl.in_neuron, wl.W, wl.D, f, g,
                                       mode=m, dlp=x)
@@ -51,13 +58,15 @@ def run_oracle(wl: Workload, cap=None, modes=("f64", "f32"), max_delay=None, dlp
     return out
 
 
-def make_gpu_net(wl: Workload, cap=None, flags=0, max_delay=None, per_proj=True):
+def make_gpu_net(wl: Workload, cap=None, flags=0, max_delay=None, per_proj=True, reg=None):
+    """reg: (strength per LIF layer, target) of the spike-count regulariser."""
     import paper_2501_07331_amd as snn
     c = wl.cfg
     cap = default_cap(wl) if cap is None else cap
     md, pm = proj_delays(wl, max_delay, per_proj)
+    kw = {} if reg is None else dict(reg_strength=list(reg[0]), reg_target=float(reg[1]))
     return snn.Network(c.layers, c.tau_m, c.tau_s, c.theta, c.dt, md, wl.B, wl.T, c.loss,
-                       c.readout_scale, cap, flags, dmse_delta=c.dmse_delta, proj_max_delay=pm)
+                       c.readout_scale, cap, flags, dmse_delta=c.dmse_delta, proj_max_delay=pm, **kw)
 
 
 def to_device(wl: Workload):
@@ -73,12 +82,13 @@ def to_device(wl: Workload):
 
 
 def run_gpu(wl: Workload, net=None, cap=None, flags=0, backward=True, max_delay=None, dev_in=None,
-            dlp=None, per_proj=True):
+            dlp=None, per_proj=True, reg=None, noalloc=False):
     """Forward (+ backward) through the library; returns numpy results.
-    dlp: per LIF layer None or an fp32 [B][cap] array of dl_p/dt_k."""
+    dlp: per LIF layer None or an fp32 [B][cap] array of dl_p/dt_k; reg as
+    make_gpu_net; noalloc: the backward through snn_backward_noalloc."""
     import torch
     import paper_2501_07331_amd as snn
-    net = make_gpu_net(wl, cap, flags, max_delay, per_proj) if net is None else net
+    net = make_gpu_net(wl, cap, flags, max_delay, per_proj, reg) if net is None else net
     cap = net.record_capacity
     d = to_device(wl) if dev_in is None else dev_in
     dev = torch.device("cuda")
@@ -120,7 +130,10 @@ def run_gpu(wl: Workload, net=None, cap=None, flags=0, backward=True, max_delay=
     if backward and out["rc"] == 0:
         dW = [torch.full_like(w, np.nan) for w in d["W"]]
         dD = [torch.full_like(w, np.nan) for w in d["W"]]
-        if dlp is None:
+        if noalloc:
+            assert dlp is None
+            net.backward_noalloc(dW, dD)
+        elif dlp is None:
             net.backward(dW, dD)
         else:
             net.backward(dW, dD, [None if x is None else
