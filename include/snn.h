@@ -119,7 +119,10 @@ typedef struct {
  *                   device memory even where it would fit in LDS (same
  *                   results; exercises the HBM ring path);
  *                   SNN_FLAG_TIMING: time the main kernels with HIP events
- *                   on hip_stream (reported by snn_get_stats)
+ *                   on hip_stream (reported by snn_get_stats);
+ *                   SNN_FLAG_SEPARATE_READOUT: run the LI readout as its own
+ *                   kernel after the LIF core even where it fits into the
+ *                   core's workgroup as one more wave (same results)
  * hip_stream:       hipStream_t to enqueue on (NULL: default stream)
  * dmse_delta:       Delta_t of the spike-time loss, in ms (SNN_LOSS_DMSE)
  * reg_strength:     host array of one strength rho_l >= 0 per LIF layer (in
@@ -141,6 +144,7 @@ typedef struct {
  */
 #define SNN_FLAG_HBM_RINGS 1
 #define SNN_FLAG_TIMING 2
+#define SNN_FLAG_SEPARATE_READOUT 4
 
 typedef struct {
     int32_t batch, T, loss;

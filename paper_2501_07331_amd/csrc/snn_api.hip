@@ -62,7 +62,8 @@ struct snn_net {
     double* nterm;                  // [lif_total] regulariser jump term per neuron
     float dmse_delta;
     int max_delay;
-    int core_threads;           // LIF-core workgroup size
+    int core_threads;           // LIF-core workgroup size (without a fused readout wave)
+    int ro_fused, ro_off;       // the LI readout runs as one more wave of the forward core
     int read_threads;           // readout workgroup size
     size_t lds_core_f, lds_core_b, lds_scan, lds_read, lds_grad, lds_radj;
     int mask_off, scan_tb, table_lds;
@@ -197,7 +198,8 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     if (dmse && (!(opts->dmse_delta == opts->dmse_delta) || isinf(opts->dmse_delta) ||
                  opts->record_capacity < 1))
         return SNN_EINVAL;
-    if (opts->flags & ~(SNN_FLAG_HBM_RINGS | SNN_FLAG_TIMING)) return SNN_EINVAL;
+    if (opts->flags & ~(SNN_FLAG_HBM_RINGS | SNN_FLAG_TIMING | SNN_FLAG_SEPARATE_READOUT))
+        return SNN_EINVAL;
     if (opts->reg_strength && (!(opts->reg_target >= 0.0f) || isinf(opts->reg_target)))
         return SNN_EINVAL;
     for (int l = 0; l < n_layers; ++l) {
@@ -337,6 +339,17 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         }
         net->mask_off = (int)align16(used);
         net->lds_core_f = net->mask_off + masks;
+        // the LI readout fed by a LIF layer as one more wave of the core: its
+        // arrival ring [S_out + 1][C] after the masks
+        const int feed_l = t.pre[t.out_p];
+        const size_t ro_ring = (size_t)(t.Sp[t.out_p] + 1) * C * sizeof(float);
+        if (!t.out_lif && feed_l != 0 && net->core_threads <= 256 && C <= 64 &&
+            !(opts->flags & SNN_FLAG_SEPARATE_READOUT) &&
+            align16(net->lds_core_f) + ro_ring <= kLds) {
+            net->ro_fused = 1;
+            net->ro_off = (int)align16(net->lds_core_f);
+            net->lds_core_f = net->ro_off + ro_ring;
+        }
     }
     // backward core: partial jump sums [2][NL][KP][4 NW] and the fp64 adjoint
     // rings [Sb][n] of the LIF layers read by LIF-pre projections (all in
@@ -431,9 +444,30 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
             jblocks += g.jb;
             ++ng;
         }
-        int SB = std::max(1, std::min(t.B, (512 + jblocks - 1) / jblocks));
+        // sample blocks: a workgroup holds a CU (its LDS), so the grid runs in
+        // rounds of n_cu workgroups; take the SB that minimises rounds x
+        // samples per block (the fp64 partials of SB > 1 blocks capped at
+        // 512 MiB)
+        int n_cu = 256, dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            n_cu < 1)
+            n_cu = 256;
+        const long long part_cap = (512ll << 20) / (16ll * std::max<long long>(net->n_params, 1));
+        auto cost_of = [&](int sb) {
+            const int bsz = (t.B + sb - 1) / sb;
+            return (((long long)jblocks * sb + n_cu - 1) / n_cu) * bsz;
+        };
+        long long best = -1;
+        for (int sb = 1; sb <= t.B && (sb == 1 || sb <= part_cap); ++sb) {
+            const long long c = cost_of(sb);
+            if (best < 0 || c < best) best = c;
+        }
+        // the fewest blocks (least partial-sum traffic) within 3 % of it
+        int SB = 1;
+        while (SB < t.B && cost_of(SB) * 100 > best * 103) ++SB;
         const int bs = (t.B + SB - 1) / SB;
-        SB = (t.B + bs - 1) / bs;
+        SB = (t.B + bs - 1) / bs;                            // no empty trailing block
         int blk = 0;
         for (int g = 0; g < ng; ++g) {
             GradGroup& G = net->grad_grp[g];
@@ -655,6 +689,9 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
                 const int pre = t.pre[p];
                 y.in_l[y.nin] = (pre == 0) ? -1 : t.lif[pre];
                 y.in_pp[y.nin] = 0;
+                y.in_S[y.nin] = t.Sp[p];
+                y.in_ring_lds[y.nin] = t.fring[p];
+                y.in_ring[y.nin] = net->fring[p];
                 if (pre != 0) {
                     // position of p among the LIF-post projections of its source layer
                     int k = 0;
@@ -705,7 +742,20 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
         a.If = net->If;
         a.st = net->st;
         a.mask_off = net->mask_off;
-        TIMED(net, K_CORE, launch_forward_core(a, t.n_lif, net->core_threads, net->lds_core_f, s));
+        if (net->ro_fused) {
+            a.ro_C = C;
+            a.ro_feed = t.lif[t.pre[t.out_p]];
+            a.ro_nfeed = t.n[t.pre[t.out_p]];
+            a.ro_S = t.Sp[t.out_p];
+            a.ro_off = net->ro_off;
+            a.ro_loss = t.loss;
+            a.ro_scale = t.rscale;
+            a.ro_ws = net->ws + t.woff[t.out_p];
+            a.z = net->z;
+            a.nstar = net->nstar;
+        }
+        TIMED(net, K_CORE, launch_forward_core(a, t.n_lif, net->core_threads + (net->ro_fused ? 64 : 0),
+                                               net->lds_core_f, s));
     }
     if (net->reg_on) {
         RegArgs ra{};
@@ -730,21 +780,23 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
                                       net->rec_n + li * B * cap, t.cap, labels, t.B, C, t.T, t.dt,
                                       net->dmse_delta, net->z, loss, net->xlp_out, net->st, s));
     } else {
-        ReadoutArgs r{};
-        r.t = t;
-        r.ws = net->ws + t.woff[t.out_p];
-        r.A_in = net->A_in;
-        r.rec_n = net->rec_n;
-        r.rec_s = net->rec_s;
-        r.rec_idx = net->rec_idx;
-        r.table = net->table;
-        r.table_lds = net->table_lds;
-        r.z = net->z;
-        r.nstar = net->nstar;
-        r.Vf = net->Vf;
-        r.If = net->If;
-        r.st = net->st;
-        TIMED(net, K_READ, launch_readout_forward(r, net->read_threads, net->lds_read, s));
+        if (!net->ro_fused) {
+            ReadoutArgs r{};
+            r.t = t;
+            r.ws = net->ws + t.woff[t.out_p];
+            r.A_in = net->A_in;
+            r.rec_n = net->rec_n;
+            r.rec_s = net->rec_s;
+            r.rec_idx = net->rec_idx;
+            r.table = net->table;
+            r.table_lds = net->table_lds;
+            r.z = net->z;
+            r.nstar = net->nstar;
+            r.Vf = net->Vf;
+            r.If = net->If;
+            r.st = net->st;
+            TIMED(net, K_READ, launch_readout_forward(r, net->read_threads, net->lds_read, s));
+        }
         HIP_TRY(net, launch_loss(net->z, labels, t.B, C, t.loss, t.rscale, net->tau_m, loss,
                                  net->src, net->st, s));
     }

@@ -158,6 +158,31 @@ __device__ __forceinline__ void word_ids(const unsigned long long (&m)[NWM],
 // s_waitcnt vmcnt(0), expcnt and lgkmcnt left at their maximum (gfx9 encoding)
 constexpr int kWaitVm0 = 0x0F70;
 
+// One leaky-integrator neuron (a LIF neuron without threshold).
+struct LiState {
+    float V, I, acc, best;
+    int nst;
+};
+
+// One LI step n: V- = fma(alpha, V, gamma I), I- = beta I, the readout
+// statistic of V- (running sum, or first maximum and its step), then the
+// step's arrivals x added to I.
+template <bool SUM>
+__device__ __forceinline__ void li_update(float alpha, float beta, float gamma, int n, float x,
+                                          LiState& q) {
+    const float gi = __fmul_rn(gamma, q.I);
+    const float Vm = __fmaf_rn(alpha, q.V, gi);
+    q.I = __fmul_rn(beta, q.I);
+    q.V = Vm;
+    if (SUM) {
+        q.acc = __fadd_rn(q.acc, Vm);
+    } else if (n == 0 || Vm > q.best) {
+        q.best = Vm;
+        q.nst = n;
+    }
+    q.I = __fadd_rn(q.I, x);
+}
+
 // Adds w[k] to cell row[k] of one lane's column (cell r at col[r * stride])
 // for k = 0 .. K-1 in order, where every row is valid (out-of-range entries
 // point at a dummy row that is never read out).  Reads first, equal rows

@@ -252,27 +252,9 @@ __global__ void __launch_bounds__(64) input_scan_kernel(InScanArgs a) {
 
 // ------------------------------------------------------------------ readout
 
-struct LiState {
-    float V, I, acc, best;
-    int nst;
-};
-
-// One LI step: V- = alpha V + gamma I, I- = beta I, the loss statistic of V-
-// (running sum, or first maximum and its step), then the arrivals x of the
-// step added to I.
 template <bool SUM>
 __device__ __forceinline__ void li_step(const Topo& t, int n, float x, LiState& q) {
-    const float gi = __fmul_rn(t.gamma, q.I);
-    const float Vm = __fmaf_rn(t.alpha, q.V, gi);
-    q.I = __fmul_rn(t.beta, q.I);
-    q.V = Vm;
-    if (SUM) {
-        q.acc = __fadd_rn(q.acc, Vm);
-    } else if (n == 0 || Vm > q.best) {
-        q.best = Vm;
-        q.nst = n;
-    }
-    q.I = __fadd_rn(q.I, x);
+    li_update<SUM>(t.alpha, t.beta, t.gamma, n, x, q);
 }
 
 // The LI layer over T steps of one lane's arrival column (step n at
@@ -614,7 +596,11 @@ hipError_t set_forward_lds_limits(size_t bytes, int* bad) {
 
 hipError_t launch_forward_core(const CoreFwdArgs& a, int n_lif, int threads, size_t lds,
                                hipStream_t s) {
-    if (n_lif < 1 || n_lif > SNN_MAX_LIF || threads != 64 * a.NW) return hipErrorInvalidValue;
+    // the core waves, and one more for a fused readout (cores of up to 256 threads)
+    const int core = 64 * a.NW;
+    if (n_lif < 1 || n_lif > SNN_MAX_LIF || threads != core + (a.ro_C > 0 ? 64 : 0) ||
+        (a.ro_C > 0 && (core > 256 || a.ro_C > 64 || a.ro_feed < 0 || a.ro_feed >= n_lif)))
+        return hipErrorInvalidValue;
     int np = 0;
     bool rl = true;
     for (int l = 0; l < n_lif; ++l) {
@@ -622,8 +608,8 @@ hipError_t launch_forward_core(const CoreFwdArgs& a, int n_lif, int threads, siz
         for (int pp = 0; pp < a.ly[l].npost; ++pp)
             if (a.ly[l].ring_lds[pp] < 0) rl = false;
     }
-    const bool ok = (threads <= 256) ? launch_forward_core_256(a, n_lif, np, rl, threads, lds, s)
-                                     : launch_forward_core_1024(a, n_lif, np, rl, threads, lds, s);
+    const bool ok = (core <= 256) ? launch_forward_core_256(a, n_lif, np, rl, threads, lds, s)
+                                  : launch_forward_core_1024(a, n_lif, np, rl, threads, lds, s);
     if (!ok) return hipErrorInvalidValue;
     return hipGetLastError();
 }
@@ -632,7 +618,7 @@ hipError_t set_core_lds_limits(size_t bytes, int* bad) {
     hipError_t e = set_core_lds_limits_256(bytes, bad);
     if (e == hipSuccess) {
         e = set_core_lds_limits_1024(bytes, bad);
-        if (e != hipSuccess && bad) *bad += 16;   // 1024-thread kernels: 16 .. 31
+        if (e != hipSuccess && bad) *bad += 32;   // 1024-thread kernels: 32 .. 47
     }
     return e;
 }

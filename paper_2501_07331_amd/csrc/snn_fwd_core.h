@@ -16,6 +16,16 @@
 // the weights a step ahead and scattered them one step later, adding
 // zero-delay synapses from per-lane lists, was slower on gfx950 and is
 // gone.)
+//
+// With RO, one more wave runs the leaky-integrator readout fed by a LIF
+// layer, in its own loop with one barrier per step like the core waves:
+// after the barrier of step n it reads that layer's spike masks of step n,
+// adds the spikes' readout weights to the ring cells of their arrivals (an
+// LDS ring of S_out + 1 rows, emission order per cell) and runs the LI step
+// n.  Its work overlaps the core waves' own scatter instead of following the
+// core as a separate kernel.  (Running it one step behind, with the weights
+// of a step loaded a step ahead, was slower: 1.41 against 1.33 ms on the
+// 700-256rec-20 step.)
 #pragma once
 
 #include <type_traits>
@@ -24,7 +34,7 @@
 
 namespace {
 
-template <int MAXT, int NL, int NP, bool RL>
+template <int MAXT, int NL, int NP, bool RL, bool RO>
 struct FwdCore {
     static constexpr int NWM = MAXT / 64;
     // spikes per chunk of the scatter: with rings in device memory every
@@ -143,6 +153,110 @@ struct FwdCore {
         }
     }
 
+    // ---- the fused readout wave (RO)
+
+    // This lane's readout column in the LDS ring; lanes past C add to the
+    // dummy row of column C - 1 (stride 0).
+    static __device__ __forceinline__ lds_f32* ro_col(const CoreFwdArgs& a, int lane, int& stride) {
+        const int C = a.ro_C;
+        lds_f32* col = (lds_f32*)(smem + a.ro_off) + min(lane, C - 1);
+        stride = (lane < C) ? C : 0;
+        return (lane < C) ? col : col + a.ro_S * C;
+    }
+
+    // Readout weights of spikes ids[0 .. KB) of the feeding layer for this
+    // lane's output (rows clamped into the matrix; entries past a step's
+    // count are not used).
+    static __device__ __forceinline__ void ro_load(const CoreFwdArgs& a, int lane, const int (&ids)[KB],
+                                                   uint2 (&w)[KB]) {
+        const int C = a.ro_C;
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)a.ro_ws, (short)0, a.ro_nfeed * C * 8, 0x00020000);
+        const int col8 = min(lane, C - 1) * 8, rmax = a.ro_nfeed - 1;
+#pragma unroll
+        for (int k = 0; k < KB; ++k) {
+            const int r = min(max(ids[k], 0), rmax);
+            const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, col8, r * C * 8, 0);
+            w[k] = make_uint2((unsigned)v[0], (unsigned)v[1]);
+        }
+    }
+
+    // Adds one chunk of step e's spikes (readout weights w, count left from
+    // the chunk on `left`) to the ring cells of their arrivals.
+    static __device__ __forceinline__ void ro_add(const CoreFwdArgs& a, int e, int left,
+                                                  const uint2 (&w)[KB], lds_f32* col, int stride) {
+        const int S = a.ro_S, e_mod = e % S;
+        int rw[KB];
+        float wv[KB];
+#pragma unroll
+        for (int k = 0; k < KB; ++k) {
+            // slots below lim arrive before T (none past the count); a masked
+            // spike adds -0 to its own row (x + -0 = x exactly)
+            const int s = (int)w[k].y;
+            const int lim = (k < left) ? a.T - e : 0;
+            const unsigned r = (unsigned)(e_mod + s);
+            rw[k] = (int)min(r, r - (unsigned)S);
+            wv[k] = (s < lim) ? __uint_as_float(w[k].x) : -0.0f;
+        }
+        column_add(col, stride, rw, wv);
+    }
+
+    // Step e of the readout (after the step's barrier): the feeding layer's
+    // spikes of step e (masks row `row`) into the ring, chunk by chunk, then
+    // the LI step with the arrivals of row e.
+    template <bool SUM>
+    static __device__ __forceinline__ void ro_step(const CoreFwdArgs& a, int lane, int e,
+                                                   const unsigned long long* row, LiState& q) {
+        const int C = a.ro_C;
+        unsigned long long mw[NWM];
+        row_words<NWM>(row, a.NW, mw);
+        int total = 0;
+#pragma unroll
+        for (int w = 0; w < NWM; ++w) total += __popcll(mw[w]);
+        int stride;
+        lds_f32* col = ro_col(a, lane, stride);
+        for (int q0 = 0; q0 < total; q0 += KB) {
+            int ids[KB];
+            word_ids<NWM, KB>(mw, row, a.NW, q0, ids);
+            uint2 w[KB];
+            ro_load(a, lane, ids, w);
+            ro_add(a, e, total - q0, w, col, stride);
+        }
+        // arrivals of step e (then the row is free for step e + S)
+        float x = 0.0f;
+        const int e_mod = e % a.ro_S;
+        if (lane < C) {
+            x = col[e_mod * C];
+            col[e_mod * C] = 0.0f;
+        }
+        li_update<SUM>(a.alpha, a.beta, a.gamma, e, x, q);
+    }
+
+    // The readout wave's loop: one barrier per step, as the core waves' steps
+    // (the branch is per wave, so every wave reaches every barrier); then the
+    // results.
+    template <bool SUM>
+    static __device__ __forceinline__ void ro_run(const CoreFwdArgs& a, int b, int lane) {
+        const unsigned long long* masks = reinterpret_cast<const unsigned long long*>(smem + a.mask_off);
+        LiState q{};
+        for (int n = 0; n < a.T; ++n) {
+            __syncthreads();
+            ro_step<SUM>(a, lane, n, masks + (size_t)((n % 3) * NL + a.ro_feed) * a.NW, q);
+        }
+        ro_finish(a, b, lane, q);
+    }
+
+    static __device__ __forceinline__ void ro_finish(const CoreFwdArgs& a, int b, int lane,
+                                                     const LiState& q) {
+        const int C = a.ro_C;
+        if (lane >= C) return;
+        const bool sum = a.ro_loss == SNN_LOSS_CE_SUM;
+        a.z[(size_t)b * C + lane] = sum ? __fmul_rn(a.ro_scale, q.acc) : q.best;
+        a.nstar[(size_t)b * C + lane] = sum ? -1 : q.nst;
+        a.Vf[(size_t)b * a.nstate + (a.nstate - C) + lane] = q.V;
+        a.If[(size_t)b * a.nstate + (a.nstate - C) + lane] = q.I;
+    }
+
     static __device__ __forceinline__ void step(const CoreFwdArgs& a, int b, int tid, int n,
                                                 const Pre& P, Pre& N, Lane& L) {
         const int lane = tid & 63, wave = tid >> 6;
@@ -239,9 +353,13 @@ struct FwdCore {
                 if (sl < 0) {
                     add = P.ain;
                 } else {
-                    const int pp = y.in_pp[e];
-                    const int n_mod = n % a.ly[sl].S[pp];
-                    RingPtr c = ring_col<RingPtr>(a, b, sl, pp, tid) + n_mod * y.n;
+                    const int S = y.in_S[e], n_mod = n % S;
+                    RingPtr c;
+                    if constexpr (RL)
+                        c = (lds_f32*)(reinterpret_cast<float*>(smem) + y.in_ring_lds[e]) + tid;
+                    else
+                        c = (global_f32*)(y.in_ring[e] + (size_t)b * (S + 1) * y.n) + tid;
+                    c += n_mod * y.n;
                     add = *c;
                     *c = 0.0f;
                 }
@@ -283,6 +401,22 @@ struct FwdCore {
             L.cnt[l] = 0;
             L.own[l] = 0;
         }
+        if constexpr (RO) {
+            if ((tid >> 6) == a.NW) {
+                // the readout wave: its ring's columns, rows 0 .. S (row S:
+                // dummy), then its own loop
+                if ((tid & 63) < a.ro_C) {
+                    lds_f32* c = (lds_f32*)(smem + a.ro_off) + (tid & 63);
+                    for (int r = 0; r <= a.ro_S; ++r) c[r * a.ro_C] = 0.0f;
+                }
+                __syncthreads();
+                if (a.ro_loss == SNN_LOSS_CE_SUM)
+                    ro_run<true>(a, b, tid & 63);
+                else
+                    ro_run<false>(a, b, tid & 63);
+                return;
+            }
+        }
         __syncthreads();
         run_steps(a, b, tid, L);
 
@@ -306,17 +440,27 @@ struct FwdCore {
     }
 };
 
-template <int MAXT, int NL, int NP, bool RL>
-__global__ void __launch_bounds__(MAXT) forward_core_kernel(CoreFwdArgs a) {
-    FwdCore<MAXT, NL, NP, RL>::run(a);
+// MAXT: the most LIF neurons per layer (threads of the core waves); with RO
+// the workgroup has one more wave.
+template <int MAXT, int NL, int NP, bool RL, bool RO>
+__global__ void __launch_bounds__(MAXT + (RO ? 64 : 0)) forward_core_kernel(CoreFwdArgs a) {
+    FwdCore<MAXT, NL, NP, RL, RO>::run(a);
 }
 
 template <int MAXT, int NL, int NP>
 void launch_f3(const CoreFwdArgs& a, bool rl, int threads, size_t lds, hipStream_t s) {
-    if (rl)
-        hipLaunchKernelGGL((forward_core_kernel<MAXT, NL, NP, true>), dim3(a.B), dim3(threads), lds, s, a);
-    else
-        hipLaunchKernelGGL((forward_core_kernel<MAXT, NL, NP, false>), dim3(a.B), dim3(threads), lds, s, a);
+    constexpr bool ro = MAXT <= 256;       // a fused readout adds a wave (at most 1024 threads)
+    if (ro && a.ro_C > 0) {
+        if (rl)
+            hipLaunchKernelGGL((forward_core_kernel<MAXT, NL, NP, true, ro>), dim3(a.B), dim3(threads), lds, s, a);
+        else
+            hipLaunchKernelGGL((forward_core_kernel<MAXT, NL, NP, false, ro>), dim3(a.B), dim3(threads), lds, s, a);
+    } else {
+        if (rl)
+            hipLaunchKernelGGL((forward_core_kernel<MAXT, NL, NP, true, false>), dim3(a.B), dim3(threads), lds, s, a);
+        else
+            hipLaunchKernelGGL((forward_core_kernel<MAXT, NL, NP, false, false>), dim3(a.B), dim3(threads), lds, s, a);
+    }
 }
 
 // Launches the instantiation for n_lif LIF layers with at most np LIF-post
@@ -336,13 +480,13 @@ bool launch_ft(const CoreFwdArgs& a, int n_lif, int np, bool rl, int threads, si
     }
 }
 
-template <int M, bool R>
+template <int M, bool R, bool O>
 hipError_t set_lds_limits_t(size_t bytes, int* bad) {
     const void* fns[] = {
-        (const void*)forward_core_kernel<M, 1, 0, R>, (const void*)forward_core_kernel<M, 1, 1, R>,
-        (const void*)forward_core_kernel<M, 2, 1, R>, (const void*)forward_core_kernel<M, 2, 2, R>,
-        (const void*)forward_core_kernel<M, 3, 1, R>, (const void*)forward_core_kernel<M, 3, 2, R>,
-        (const void*)forward_core_kernel<M, 4, 1, R>, (const void*)forward_core_kernel<M, 4, 2, R>};
+        (const void*)forward_core_kernel<M, 1, 0, R, O>, (const void*)forward_core_kernel<M, 1, 1, R, O>,
+        (const void*)forward_core_kernel<M, 2, 1, R, O>, (const void*)forward_core_kernel<M, 2, 2, R, O>,
+        (const void*)forward_core_kernel<M, 3, 1, R, O>, (const void*)forward_core_kernel<M, 3, 2, R, O>,
+        (const void*)forward_core_kernel<M, 4, 1, R, O>, (const void*)forward_core_kernel<M, 4, 2, R, O>};
     for (int i = 0; i < (int)(sizeof(fns) / sizeof(fns[0])); ++i) {
         const hipError_t e =
             hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);

@@ -7,9 +7,9 @@ bool launch_forward_core_1024(const CoreFwdArgs& a, int n_lif, int np, bool rl, 
 }
 
 hipError_t set_core_lds_limits_1024(size_t bytes, int* bad) {
-    hipError_t e = set_lds_limits_t<1024, true>(bytes, bad);
+    hipError_t e = set_lds_limits_t<1024, true, false>(bytes, bad);
     if (e == hipSuccess) {
-        e = set_lds_limits_t<1024, false>(bytes, bad);
+        e = set_lds_limits_t<1024, false, false>(bytes, bad);
         if (e != hipSuccess && bad) *bad += 8;   // kernels with rings in HBM: 8 .. 15
     }
     return e;

@@ -7,10 +7,22 @@ bool launch_forward_core_256(const CoreFwdArgs& a, int n_lif, int np, bool rl, i
 }
 
 hipError_t set_core_lds_limits_256(size_t bytes, int* bad) {
-    hipError_t e = set_lds_limits_t<256, true>(bytes, bad);
+    // kernels 0 .. 7: LDS rings; 8 .. 15: rings in HBM; 16 .. 31: the same
+    // with the fused readout wave
+    hipError_t e = set_lds_limits_t<256, true, false>(bytes, bad);
+    int base = 0;
     if (e == hipSuccess) {
-        e = set_lds_limits_t<256, false>(bytes, bad);
-        if (e != hipSuccess && bad) *bad += 8;   // kernels with rings in HBM: 8 .. 15
+        base = 8;
+        e = set_lds_limits_t<256, false, false>(bytes, bad);
     }
+    if (e == hipSuccess) {
+        base = 16;
+        e = set_lds_limits_t<256, true, true>(bytes, bad);
+    }
+    if (e == hipSuccess) {
+        base = 24;
+        e = set_lds_limits_t<256, false, true>(bytes, bad);
+    }
+    if (e != hipSuccess && bad) *bad += base;
     return e;
 }

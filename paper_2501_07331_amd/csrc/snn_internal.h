@@ -77,6 +77,9 @@ struct FwdLayer {
     int nin;                           // projections into the layer, in projection order:
     int in_l[2];                       //   source LIF layer (0-based), -1: the input projection
     int in_pp[2];                      //   index among the source layer's LIF-post projections
+    int in_S[2];                       //   LIF sources: that projection's ring slots,
+    int in_ring_lds[2];                //   its ring (LDS float offset, or the HBM ring
+    float* in_ring[2];                 //   [B][S+1][n])
     int npost;                         // LIF-post projections out of the layer (recurrent, then
                                        // feed-forward); entries past npost repeat a valid one
     int nq[2];                         //   post neurons
@@ -107,6 +110,14 @@ struct CoreFwdArgs {
     float* If;
     DevStatus* st;
     int mask_off;                      // byte offset of the ballot masks [3][NL][NW] in LDS
+    // the LI readout fused into the core as one extra wave (ro_C > 0): lane
+    // k < ro_C owns output k; arrivals in an LDS ring [ro_S + 1][ro_C] (row
+    // ro_S: dummy) at byte offset ro_off
+    int ro_C, ro_feed, ro_nfeed, ro_S, ro_off, ro_loss;
+    float ro_scale;
+    const uint2* ro_ws;                // readout projection (weight bits, slot) [ro_nfeed][ro_C]
+    float* z;                          // [B][C]
+    int* nstar;                        // [B][C]
 };
 
 struct ReadoutArgs {

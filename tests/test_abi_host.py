@@ -91,12 +91,36 @@ GOOD = [(3, 0, 0), (4, 1, 1), (2, 2, 0)]
     (GOOD, {"batch": 0}),
     (GOOD, {"T": 0}),
     (GOOD, {"loss": 7}),
-    (GOOD, {"flags": 4}),
+    (GOOD, {"flags": 8}),
     (GOOD, {"record_capacity": -1}),
+    (GOOD, {"T": 65537}),                                # past SNN_MAX_T
+    ([(16385, 0, 0), (4, 1, 0), (2, 2, 0)], {}),         # past SNN_MAX_INPUT
 ])
 def test_create_rejects_bad_arguments(lib, layers, kw):
     rc, h = _create(lib, layers, **kw)
     assert rc == -1 and not h.value
+
+
+@pytest.mark.parametrize("pmax,reg", [
+    ([10, 11, 10], None),                 # a projection's largest delay above max_delay
+    ([10, -1, 10], None),
+    (None, [-1.0]),                       # negative regulariser strength
+    (None, [float("nan")]),
+])
+def test_create_rejects_bad_per_projection_options(lib, pmax, reg):
+    kw = {}
+    keep = []
+    if pmax is not None:
+        arr = (C.c_int32 * len(pmax))(*pmax)
+        keep.append(arr)
+        kw["proj_max_delay"] = C.cast(arr, C.c_void_p)
+    if reg is not None:
+        arr = (C.c_float * len(reg))(*reg)
+        keep.append(arr)
+        kw["reg_strength"] = C.cast(arr, C.c_void_p)
+    rc, h = _create(lib, GOOD, **kw)
+    assert rc == -1 and not h.value
+    assert lib.snn_last_error(None)
 
 
 def test_null_handles(lib):

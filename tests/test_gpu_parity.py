@@ -62,6 +62,23 @@ def test_parity_network_wide_ring_depth(cid, B):
         assert np.array_equal(x.view(np.uint32), y.view(np.uint32))
 
 
+@pytest.mark.parametrize("cid,B", [(2, 64), (4, 16), (1, 32)])
+def test_fused_readout_equals_separate_readout_kernel(cid, B):
+    """The LI readout run as one more wave of the forward core gives what the
+    separate readout kernel gives, bit for bit: records, z, the LI state, the
+    loss and the gradients (max readout on config 2, sum readout on 1 and 4)."""
+    import paper_2501_07331_amd as snn
+    wl = make_workload(cid, B=B, weight_scale=6.0 if cid == 1 else 1.0)
+    a = run_gpu(wl)
+    b = run_gpu(wl, flags=snn.SNN_FLAG_SEPARATE_READOUT)
+    for k in ("count", "step", "neuron", "z", "V", "I", "loss"):
+        assert np.array_equal(np.asarray(a[k]).view(np.uint8), np.asarray(b[k]).view(np.uint8)), k
+    for x, y in zip(a["dW"] + a["dD"], b["dW"] + b["dD"]):
+        assert np.array_equal(x.view(np.uint32), y.view(np.uint32))
+    orc = run_oracle(wl, modes=("f64",))
+    assert_forward_bitexact(a, orc, wl)
+
+
 def test_per_projection_delay_clamp():
     """Delays past their projection's own largest delay are clamped to it
     (and counted) exactly as by the oracle, on a recurrent net whose
