@@ -444,6 +444,9 @@ def main():
     if avg.get("readout_forward", 0.0) == 0.0:
         # the readout ran as a wave of the forward core
         kb["forward_core"] += kb["readout_forward"]
+    if avg.get("readout_adjoint", 0.0) == 0.0:
+        # and its adjoint as a wave of the backward core
+        kb["backward_core"] += kb["readout_adjoint"]
     avg = {k: v for k, v in avg.items() if v > 0.0}
     dom = max(avg, key=avg.get)
     ach = kb[dom] / (avg[dom] * 1e-3) / 1e9
