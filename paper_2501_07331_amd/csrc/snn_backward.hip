@@ -668,34 +668,50 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
                     double pu = su[k], pd = sd[k];
                     // four spikes at a time: their reads issued together, their
                     // terms added in spike order; the arrivals ascend, so the
-                    // window's spikes are a prefix from the cursor
+                    // window's spikes are a prefix from the cursor.  The loop
+                    // comes in two copies, spike steps in LDS or in device
+                    // memory (one choice per sample), and a term past the
+                    // window adds +0 (the sums start at +0, so they never hold
+                    // -0 and +0 changes nothing): no branch inside.
                     int x = lo[k];
-                    for (; x < hi[k]; x += 4) {
-                        int m[4];
+                    const int h = hi[k];
+                    auto spikes = [&](auto in_lds_tag) {
+                        constexpr bool SPL = decltype(in_lds_tag)::value;
+                        for (; x < h; x += 4) {
+                            // the four reads unconditional and issued together
+                            // (the empty asm keeps the compiler from moving each
+                            // behind its own branch and wait)
+                            int t[4], m[4];
 #pragma unroll
-                        for (int u = 0; u < 4; ++u) {
-                            const int xc = min(x + u, hi[k] - 1);
-                            const int t = in_lds ? (int)sp[xc + off] : gs[xc];
-                            m[u] = (x + u < hi[k]) ? t + sl : T;     // T: no arrival
-                        }
-                        double2 ud[4];
+                            for (int u = 0; u < 4; ++u) {
+                                const int xc = min(x + u, h - 1);
+                                t[u] = SPL ? (int)sp[xc + off] : gs[xc];
+                            }
+                            asm volatile("" : "+v"(t[0]), "+v"(t[1]), "+v"(t[2]), "+v"(t[3]));
 #pragma unroll
-                        for (int u = 0; u < 4; ++u) ud[u] = stk[(m[u] < wend) ? m[u] - w0 : 0];
+                            for (int u = 0; u < 4; ++u) m[u] = (x + u < h) ? t[u] + sl : T;   // T: no arrival
+                            double2 ud[4];
 #pragma unroll
-                        for (int u = 0; u < 4; ++u) {
-                            if (m[u] < wend) {
-                                pu = __dadd_rn(pu, ud[u].x);
-                                pd = __dadd_rn(pd, ud[u].y);
+                            for (int u = 0; u < 4; ++u) ud[u] = stk[(m[u] < wend) ? m[u] - w0 : 0];
+#pragma unroll
+                            for (int u = 0; u < 4; ++u) {
+                                const bool ok = m[u] < wend;
+                                pu = __dadd_rn(pu, ok ? ud[u].x : 0.0);
+                                pd = __dadd_rn(pd, ok ? ud[u].y : 0.0);
+                            }
+                            if constexpr (WIN) {
+                                if (m[3] >= wend) {
+                                    x += (m[0] < wend) + (m[1] < wend) + (m[2] < wend);
+                                    break;
+                                }
                             }
                         }
-                        if constexpr (WIN) {
-                            if (m[3] >= wend) {
-                                x += (m[0] < wend) + (m[1] < wend) + (m[2] < wend);
-                                break;
-                            }
-                        }
-                    }
-                    if constexpr (WIN) lo[k] = min(x, hi[k]);
+                    };
+                    if (in_lds)
+                        spikes(std::true_type{});
+                    else
+                        spikes(std::false_type{});
+                    if constexpr (WIN) lo[k] = min(x, h);
                     su[k] = pu;
                     sd[k] = pd;
                 }
