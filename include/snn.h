@@ -122,7 +122,19 @@ typedef struct {
  *                   on hip_stream (reported by snn_get_stats);
  *                   SNN_FLAG_SEPARATE_READOUT: run the LI readout as its own
  *                   kernel after the LIF core even where it fits into the
- *                   core's workgroup as one more wave (same results)
+ *                   core's workgroup as one more wave (same results);
+ *                   SNN_FLAG_CLUSTER: run the LIF cores in cluster mode
+ *                   even where one workgroup per sample would hold the
+ *                   rings in LDS (same forward results, bit for bit; the
+ *                   backward sums its jump terms in another order).  Cluster
+ *                   mode, which the library chooses by itself when a
+ *                   sample's rings do not fit in one workgroup's LDS, spreads
+ *                   a sample over ceil(widest LIF layer / 64) workgroups of
+ *                   64 threads, each holding its neurons' ring columns in
+ *                   LDS, which exchange the spikes (forward) and the partial
+ *                   jump sums (backward) of every step through device memory;
+ *                   it needs cooperative launches.  SNN_FLAG_HBM_RINGS wins
+ *                   over it
  * hip_stream:       hipStream_t to enqueue on (NULL: default stream)
  * dmse_delta:       Delta_t of the spike-time loss, in ms (SNN_LOSS_DMSE)
  * reg_strength:     host array of one strength rho_l >= 0 per LIF layer (in
@@ -145,6 +157,7 @@ typedef struct {
 #define SNN_FLAG_HBM_RINGS 1
 #define SNN_FLAG_TIMING 2
 #define SNN_FLAG_SEPARATE_READOUT 4
+#define SNN_FLAG_CLUSTER 8
 
 typedef struct {
     int32_t batch, T, loss;

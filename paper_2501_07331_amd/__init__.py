@@ -9,12 +9,12 @@ fallback.
 """
 from .binding import (SNNError, SNNOverflow, Network, lib_path, load_library, SNN_INPUT, SNN_LIF,
                       SNN_LI, SNN_LOSS_CE_SUM, SNN_LOSS_CE_MAX, SNN_LOSS_DMSE, SNN_FLAG_HBM_RINGS,
-                      SNN_FLAG_TIMING, SNN_FLAG_SEPARATE_READOUT, SNN_OPT_SGD, SNN_OPT_ADAM, SNN_OK, SNN_EINVAL, SNN_ENOMEM,
+                      SNN_FLAG_TIMING, SNN_FLAG_SEPARATE_READOUT, SNN_FLAG_CLUSTER, SNN_OPT_SGD, SNN_OPT_ADAM, SNN_OK, SNN_EINVAL, SNN_ENOMEM,
                       SNN_ESTATE, SNN_EOVERFLOW, SNN_EDEVICE, SNN_NOALLOC_SCRATCH_BYTES)
 from . import schedules
 
 __all__ = ["SNNError", "SNNOverflow", "Network", "lib_path", "load_library", "SNN_INPUT", "SNN_LIF",
            "SNN_LI", "SNN_LOSS_CE_SUM", "SNN_LOSS_CE_MAX", "SNN_LOSS_DMSE", "SNN_FLAG_HBM_RINGS",
-           "SNN_FLAG_TIMING", "SNN_FLAG_SEPARATE_READOUT", "SNN_OPT_SGD", "SNN_OPT_ADAM", "SNN_OK", "SNN_EINVAL", "SNN_ENOMEM",
+           "SNN_FLAG_TIMING", "SNN_FLAG_SEPARATE_READOUT", "SNN_FLAG_CLUSTER", "SNN_OPT_SGD", "SNN_OPT_ADAM", "SNN_OK", "SNN_EINVAL", "SNN_ENOMEM",
            "SNN_ESTATE", "SNN_EOVERFLOW", "SNN_EDEVICE", "SNN_NOALLOC_SCRATCH_BYTES",
            "schedules"]

@@ -13,6 +13,7 @@ SNN_LOSS_CE_SUM, SNN_LOSS_CE_MAX, SNN_LOSS_DMSE = 0, 1, 2
 SNN_FLAG_HBM_RINGS = 1
 SNN_FLAG_TIMING = 2
 SNN_FLAG_SEPARATE_READOUT = 4
+SNN_FLAG_CLUSTER = 8
 SNN_NOALLOC_SCRATCH_BYTES = 32 << 20
 SNN_OPT_SGD, SNN_OPT_ADAM = 0, 1
 _NAMES = {0: "SNN_OK", -1: "SNN_EINVAL", -2: "SNN_ENOMEM", -3: "SNN_ESTATE", -4: "SNN_EOVERFLOW",

@@ -71,6 +71,14 @@ struct snn_net {
     int bring_mode[SNN_MAX_LAYERS];   // adjoint ring of a LIF layer: -2 none, -1 HBM, >= 0 LDS
                                       // byte offset
     int radj_threads, radj_tab;
+    // cluster mode of the LIF cores (see ClusterArgs): on for the forward /
+    // backward core, workgroups per sample, samples per launch, most
+    // LIF-post projections of a LIF layer, the backward's staging offset,
+    // the next exchange tag (odd) and the exchange words
+    int cl_f, cl_b, cl_G, cl_spp_f, cl_spp_b, cl_np, cl_off_b;
+    int cl_threads_f;           // forward workgroup: the neuron wave and one wave per LIF -> LIF ring
+    unsigned cl_tag;
+    unsigned long long* clx;
     int grad_J, grad_TW, grad_KL, grad_threads, grad_SB, grad_bs, grad_nblk, grad_ngroups, grad_spcap;
     GradGroup grad_grp[SNN_MAX_LAYERS];
     hipStream_t stream;
@@ -152,7 +160,7 @@ static void free_all(snn_net* n) {
                     n->src,     n->Vf,      n->If,       n->table,     n->tr_lif, n->tr_out,
                     n->A2,       n->in_goff,   n->in_gstep, n->st,
                     n->gpart,   n->ws,      n->steptab, n->mom,   n->xlp_out, n->ncount,
-                    n->nterm};
+                    n->nterm,   n->clx};
     for (void* p : bufs)
         if (p) (void)hipFree(p);
     for (int p = 0; p < SNN_MAXP; ++p)
@@ -198,7 +206,8 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     if (dmse && (!(opts->dmse_delta == opts->dmse_delta) || isinf(opts->dmse_delta) ||
                  opts->record_capacity < 1))
         return SNN_EINVAL;
-    if (opts->flags & ~(SNN_FLAG_HBM_RINGS | SNN_FLAG_TIMING | SNN_FLAG_SEPARATE_READOUT))
+    if (opts->flags &
+        ~(SNN_FLAG_HBM_RINGS | SNN_FLAG_TIMING | SNN_FLAG_SEPARATE_READOUT | SNN_FLAG_CLUSTER))
         return SNN_EINVAL;
     if (opts->reg_strength && (!(opts->reg_target >= 0.0f) || isinf(opts->reg_target)))
         return SNN_EINVAL;
@@ -316,12 +325,51 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         if (t.pre[p] != 0 && t.kind[t.post[p]] == SNN_LIF)
             t.Sb[t.post[p]] = std::max(t.Sb[t.post[p]], t.Sp[p]);
 
-    // ---- LDS plans
+    // ---- LDS plans (the kernels' LDS limits first: occupancy depends on them)
+    {
+        int bad = -1;
+        const char* what = "forward LDS limits";
+        hipError_t e = set_forward_lds_limits(kLds, &bad);
+        if (e == hipSuccess) {
+            what = "forward core LDS limits";
+            e = set_core_lds_limits(kLds, &bad);
+        }
+        if (e == hipSuccess) {
+            what = "backward LDS limits";
+            e = set_backward_lds_limits(kLds, &bad);
+        }
+        if (e != hipSuccess) {
+            snprintf(g_create_err, sizeof(g_create_err), "snn_create: %s (kernel %d): %s", what, bad,
+                     hipGetErrorString(e));
+            free(net);
+            return SNN_EDEVICE;
+        }
+    }
     int maxlif = 0;
     for (int l = 1; l < n_layers; ++l)
         if (t.kind[l] == SNN_LIF) maxlif = std::max(maxlif, t.n[l]);
     net->core_threads = std::max(64, ((maxlif + 63) / 64) * 64);
     const int nwaves = net->core_threads / 64;
+    // cluster mode: CUs and cooperative launch support, LIF-post projections
+    const bool want_cl = !hbm && t.n_lif > 0;
+    const bool force_cl = (opts->flags & SNN_FLAG_CLUSTER) != 0;
+    int n_cu = 256, coop = 0;
+    {
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            n_cu < 1)
+            n_cu = 256;
+        if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess) coop = 0;
+    }
+    net->cl_G = (maxlif + 63) / 64;
+    for (int l = 1; l < n_layers; ++l) {
+        if (t.kind[l] != SNN_LIF) continue;
+        int k = 0;
+        for (int p = 0; p < t.P; ++p)
+            if (t.pre[p] == l && t.kind[t.post[p]] == SNN_LIF) ++k;
+        net->cl_np = std::max(net->cl_np, k);
+    }
     // forward core: the delay rings [S+1][n_post] of the LIF->LIF projections
     // (row S: dummy), all in LDS or all in HBM, then the ballot masks [3][NL][NW]
     {
@@ -339,11 +387,40 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         }
         net->mask_off = (int)align16(used);
         net->lds_core_f = net->mask_off + masks;
+        // cluster mode where the rings do not fit (or on request): each
+        // workgroup holds 64 columns of every ring, the masks of all G
+        // workgroups [3][NL][G] and an abort flag
+        if (want_cl && coop && net->cl_np > 0 && (force_cl || !rings_lds)) {
+            const int G = net->cl_G;
+            size_t u = 0;
+            int off[SNN_MAXP], rings = 0;
+            for (int p = 0; p < t.P; ++p) {
+                off[p] = -1;
+                if (t.pre[p] == 0 || t.kind[t.post[p]] != SNN_LIF) continue;
+                off[p] = (int)(u / sizeof(float));
+                u += (size_t)(t.Sp[p] + 1) * 64 * sizeof(float);
+                ++rings;
+            }
+            const size_t mk = align16((size_t)3 * t.n_lif * G * sizeof(unsigned long long)) + 16;
+            const size_t lds = align16(u) + mk;
+            const int threads = 64 * (1 + rings);
+            int nb = 0;
+            if (lds <= kLds &&
+                forward_cluster_occupancy(t.n_lif, net->cl_np, threads, lds, &nb) == hipSuccess &&
+                nb > 0 && (long long)n_cu * nb >= G) {
+                net->cl_threads_f = threads;
+                net->cl_f = 1;
+                net->cl_spp_f = std::min<long long>((long long)n_cu * nb / G, t.B);
+                for (int p = 0; p < t.P; ++p) t.fring[p] = off[p];
+                net->mask_off = (int)align16(u);
+                net->lds_core_f = lds;
+            }
+        }
         // the LI readout fed by a LIF layer as one more wave of the core: its
         // arrival ring [S_out + 1][C] after the masks
         const int feed_l = t.pre[t.out_p];
         const size_t ro_ring = (size_t)(t.Sp[t.out_p] + 1) * C * sizeof(float);
-        if (!t.out_lif && feed_l != 0 && net->core_threads <= 256 && C <= 64 &&
+        if (!t.out_lif && feed_l != 0 && net->core_threads <= 256 && C <= 64 && !net->cl_f &&
             !(opts->flags & SNN_FLAG_SEPARATE_READOUT) &&
             align16(net->lds_core_f) + ro_ring <= kLds) {
             net->ro_fused = 1;
@@ -376,6 +453,34 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
             used = part;
             for (int l = 0; l < n_layers; ++l)
                 if (net->bring_mode[l] >= 0) net->bring_mode[l] = -1;
+        }
+        // cluster mode where the rings do not fit (or on request): partials
+        // [2][NL][KP][4] of the one wave, the exchange staging (slot list and
+        // fetched halves [NL KP][64][2]), then 64 columns of every adjoint ring
+        // (chosen on request only: with rings in device memory the backward
+        // core is faster still on the widest networks)
+        if (want_cl && coop && net->cl_np > 0 && force_cl) {
+            const int KPc = bwd_prefetch_cl(NL);
+            const size_t cpart = align16((size_t)2 * NL * KPc * 4 * sizeof(double));
+            const size_t stage =
+                align16((size_t)NL * KPc * sizeof(int) + (size_t)NL * KPc * (SNN_MAX_NEURONS / 64) * 2 * sizeof(unsigned));
+            size_t u = cpart + stage;
+            int mode[SNN_MAX_LAYERS];
+            for (int l = 0; l < n_layers; ++l) {
+                mode[l] = -2;
+                if (!read_by_lif[l]) continue;
+                mode[l] = (int)u;
+                u += align16((size_t)t.Sb[l] * 64 * sizeof(double));
+            }
+            int nb = 0;
+            if (u <= kLds && backward_cluster_occupancy(NL, net->cl_np, u, &nb) == hipSuccess && nb > 0 &&
+                (long long)n_cu * nb >= net->cl_G) {
+                net->cl_b = 1;
+                net->cl_spp_b = std::min<long long>((long long)n_cu * nb / net->cl_G, t.B);
+                net->cl_off_b = (int)cpart;
+                for (int l = 0; l < n_layers; ++l) net->bring_mode[l] = mode[l];
+                used = u;
+            }
         }
         for (int l = 0; l < n_layers; ++l) t.bring[l] = net->bring_mode[l] >= 0 ? net->bring_mode[l] : -1;
         net->lds_core_b = used;
@@ -536,6 +641,15 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     }
     ALLOC(net->in_goff, B * (t.n_in + 1));
     ALLOC(net->st, 1);
+    if (net->cl_f || net->cl_b) {
+        // exchange words of every cluster slot, two parities (zero: no tag)
+        const size_t fw = net->cl_f ? (size_t)net->cl_spp_f * 2 * nl * net->cl_G : 0;
+        const size_t bw = net->cl_b ? (size_t)net->cl_spp_b * net->cl_G * 2 * nl * bwd_prefetch_cl((int)nl) : 0;
+        const size_t words = 2 * std::max(fw, bw);
+        ALLOC(net->clx, words);
+        if (e == hipSuccess) e = hipMemset(net->clx, 0, words * sizeof(unsigned long long));
+        net->cl_tag = 1;
+    }
 #undef ALLOC
     const char* what = "device allocation";
     int bad = -1;   // index of the kernel whose LDS limit was refused
@@ -543,18 +657,6 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     if (e == hipSuccess) {
         what = "scratch symbol address";
         e = scratch_address(&net->scratch);
-    }
-    if (e == hipSuccess) {
-        what = "forward LDS limits";
-        e = set_forward_lds_limits(kLds, &bad);
-    }
-    if (e == hipSuccess) {
-        what = "forward core LDS limits";
-        e = set_core_lds_limits(kLds, &bad);
-    }
-    if (e == hipSuccess) {
-        what = "backward LDS limits";
-        e = set_backward_lds_limits(kLds, &bad);
     }
     if (e == hipSuccess) {
         what = "auxiliary stream";
@@ -617,6 +719,45 @@ static int collect_times(snn_net* net, int k0, int k1) {
         HIP_TRY(net, hipEventElapsedTime(&net->stats.kernel_ms[k], net->ev[2 * k], net->ev[2 * k + 1]));
     }
     return SNN_OK;
+}
+
+// The cluster-mode cores: one cooperative launch per pass of cl_spp samples,
+// each with tags of its own (the tag advances by 2 per exchange: one per
+// step forward, at most ceil(widest layer / KP) per step backward).
+static hipError_t launch_forward_clusters(snn_net* net, CoreFwdArgs& a, hipStream_t s) {
+    const Topo& t = net->t;
+    a.NW = net->cl_G;
+    a.ro_C = 0;
+    a.cl.G = net->cl_G;
+    a.cl.x = net->clx;
+    for (int b0 = 0; b0 < t.B; b0 += net->cl_spp_f) {
+        const int nc = std::min(net->cl_spp_f, t.B - b0);
+        a.cl.b0 = b0;
+        a.cl.tag0 = net->cl_tag;
+        net->cl_tag += 2u * (unsigned)t.T;
+        const hipError_t e = launch_forward_core_cluster(a, t.n_lif, net->cl_np, nc * net->cl_G,
+                                                         net->cl_threads_f, net->lds_core_f, s);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+static hipError_t launch_backward_clusters(snn_net* net, CoreBwdArgs& a, hipStream_t s) {
+    const Topo& t = net->t;
+    const int KPc = bwd_prefetch_cl(t.n_lif);
+    a.NW = 1;
+    a.cl.G = net->cl_G;
+    a.cl.x = net->clx;
+    a.cl_off = net->cl_off_b;
+    hipError_t e = launch_clear_abort(net->st, s);
+    for (int b0 = 0; b0 < t.B && e == hipSuccess; b0 += net->cl_spp_b) {
+        const int nc = std::min(net->cl_spp_b, t.B - b0);
+        a.cl.b0 = b0;
+        a.cl.tag0 = net->cl_tag;
+        net->cl_tag += 2u * ((unsigned)t.T * (unsigned)((t.maxn + KPc - 1) / KPc) + 1u);
+        e = launch_backward_core_cluster(a, t.n_lif, net->cl_np, nc * net->cl_G, net->lds_core_b, s);
+    }
+    return e;
 }
 
 extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* const* W,
@@ -754,8 +895,11 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
             a.z = net->z;
             a.nstar = net->nstar;
         }
-        TIMED(net, K_CORE, launch_forward_core(a, t.n_lif, net->core_threads + (net->ro_fused ? 64 : 0),
-                                               net->lds_core_f, s));
+        if (net->cl_f)
+            TIMED(net, K_CORE, launch_forward_clusters(net, a, s));
+        else
+            TIMED(net, K_CORE, launch_forward_core(a, t.n_lif, net->core_threads + (net->ro_fused ? 64 : 0),
+                                                   net->lds_core_f, s));
     }
     if (net->reg_on) {
         RegArgs ra{};
@@ -807,6 +951,8 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
     const DevStatus& h = *net->st_host;
     if (h.bad_input)
         return fail(net, SNN_EINVAL, "input spikes or labels invalid (offsets, range, order)");
+    if (h.cl_abort)
+        return fail(net, SNN_EDEVICE, "forward core: a cluster exchange timed out (results void)");
     memset(&net->stats, 0, sizeof(net->stats));
     rc = collect_times(net, K_SCAN, K_RADJ);
     if (rc) return rc;
@@ -1015,8 +1161,11 @@ static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW
         a.traj = net->tr_lif;
         a.st = net->st;
         a.part_off = net->bpart_off;
-        TIMED(net, K_BCORE,
-              launch_backward_core(a, t.n_lif, net->core_threads, net->lds_core_b, s));
+        if (net->cl_b)
+            TIMED(net, K_BCORE, launch_backward_clusters(net, a, s));
+        else
+            TIMED(net, K_BCORE,
+                  launch_backward_core(a, t.n_lif, net->core_threads, net->lds_core_b, s));
     }
     HIP_TRY(net, hipStreamWaitEvent(s, net->join, 0));
     GradArgs ga{};
@@ -1058,6 +1207,8 @@ static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW
     if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GRAD + 1], s));
     int rc = read_status(net);
     if (rc) return rc;
+    if (net->st_host->cl_abort)
+        return fail(net, SNN_EDEVICE, "backward core: a cluster exchange timed out (results void)");
     rc = collect_times(net, K_RADJ, K_N);
     if (rc) return rc;
     net->stats.degenerate_jumps = (int64_t)net->st_host->degenerate;

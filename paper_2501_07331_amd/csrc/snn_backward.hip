@@ -130,9 +130,11 @@ struct BwdState {
     double A2[NL];
 };
 
-template <int MAXT, int NL, int KP, int NP, bool RL>
+template <int MAXT, int NL, int KP, int NP, bool RL, bool CL>
 struct BwdCore {
+    static_assert(!CL || (MAXT == 64 && RL && NP > 0), "cluster mode: one wave, LDS rings");
     static constexpr int NPA = NP > 0 ? NP : 1;
+    static constexpr int GM = SNN_MAX_NEURONS / 64;    // most workgroups of a cluster
     static constexpr int ROW4 = (2 + KP + 3) / 4;      // int4 loads of a spike-table row
     typedef BwdState<NL, KP, NPA> State;
 
@@ -166,7 +168,7 @@ struct BwdCore {
     // (valid for q < cnt; record index of ids[0] is ri + r0).  Only the
     // chunks of 4 that hold spikes are loaded; ids are made uniform so that
     // a row's address is scalar and the lane adds its column.
-    static __device__ __forceinline__ void load_step(const CoreBwdArgs& a, int b, int tid, int l,
+    static __device__ __forceinline__ void load_step(const CoreBwdArgs& a, int b, int j, int l,
                                                      int ri, int cnt, const int (&ids)[KP], int r0,
                                                      uint2 (&ws)[NPA][KP], int& mine, float& I,
                                                      double& A2) {
@@ -190,7 +192,7 @@ struct BwdCore {
                 // than y.n) read as zero; such entries are masked anyway
                 const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
                     (void*)y.ws[pp], (short)0, y.npre[pp] * nq * 8, 0x00020000);
-                const int col8 = min(tid, nq - 1) * 8;
+                const int col8 = min(j, nq - 1) * 8;
 #pragma unroll
                 for (int q = q0; q < q0 + 4; ++q) {
                     // (unsigned: a stale entry's offset wraps instead of overflowing)
@@ -201,7 +203,7 @@ struct BwdCore {
             }
 #pragma unroll
             for (int q = q0; q < q0 + 4; ++q)
-                if (q < cnt && idc[q] == tid) mine = q + 1;
+                if (q < cnt && idc[q] == j) mine = q + 1;
         }
         if (mine) {
             const size_t r = (size_t)b * a.cap + (ri + r0 + mine - 1);
@@ -211,7 +213,7 @@ struct BwdCore {
     }
 
     // Issue the loads of B from A (processing step n).
-    static __device__ __forceinline__ void advance(const CoreBwdArgs& a, int b, int tid, int n,
+    static __device__ __forceinline__ void advance(const CoreBwdArgs& a, int b, int j, int n,
                                                    const State& A, State& B) {
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
@@ -220,7 +222,7 @@ struct BwdCore {
             B.ri3[l] = __builtin_amdgcn_readfirstlane(A.ri2[l]);
 #pragma unroll
             for (int q = 0; q < KP; ++q) B.id3[l][q] = A.id2[l][q];
-            load_step(a, b, tid, l, B.ri3[l], B.cnt3[l], A.id2[l], 0, B.ws[l], B.mine[l], B.I[l],
+            load_step(a, b, j, l, B.ri3[l], B.cnt3[l], A.id2[l], 0, B.ws[l], B.mine[l], B.I[l],
                       B.A2[l]);
         }
     }
@@ -228,7 +230,7 @@ struct BwdCore {
     // Delayed postsynaptic sums of spikes ids[q0 .. q0 + 4) (valid for q < cnt)
     // of layer l, reduced per 16-lane row into part_l[q][wave * 4 + row].
     // n_mod[pp]: n modulo the adjoint-ring slots of projection pp's post layer.
-    static __device__ __forceinline__ void gather4(const CoreBwdArgs& a, int b, int tid, int n,
+    static __device__ __forceinline__ void gather4(const CoreBwdArgs& a, int b, int tid, int j, int n,
                                                    const int (&n_mod)[NPA], int l, int q0, int cnt,
                                                    const int (&ids)[KP], const uint2 (&ws)[NPA][KP],
                                                    double* part_l) {
@@ -257,11 +259,13 @@ struct BwdCore {
                 const int lim = (pp < y.npost && q < cnt) ? a.T - n : 0;
                 const unsigned ru = (unsigned)(n_mod[pp] + sq);
                 const int row = (int)min(ru, ru - (unsigned)S);
-                ok[k][pp] = sq < lim && tid < nq;
+                ok[k][pp] = sq < lim && j < nq;
                 // (in LDS the row is always in the ring and the column is
-                // clamped into it, so the read needs no mask; its value does)
+                // clamped into it, so the read needs no mask; its value does;
+                // a cluster's rings hold its 64 columns)
                 if (RL)
-                    d[k][pp] = ((lds_f64*)(smem + y.qring_lds[pp]))[row * nq + min(tid, nq - 1)];
+                    d[k][pp] = ((lds_f64*)(smem + y.qring_lds[pp]))[CL ? row * 64 + tid
+                                                                       : row * nq + min(tid, nq - 1)];
                 else   // (masked reads share one line of device memory)
                     d[k][pp] = ((global_f64*)(y.qring[pp] +
                                               ((size_t)b * S + (ok[k][pp] ? row : 0)) * nq))[ok[k][pp] ? tid : 0];
@@ -290,13 +294,13 @@ struct BwdCore {
         if (k < 4) part_l[(size_t)(q0 + 2 * (k & 1) + (k >> 1)) * (4 * a.NW) + wave * 4 + (lane >> 4)] = x;
     }
 
-    static __device__ __forceinline__ void gather(const CoreBwdArgs& a, int b, int tid, int n,
+    static __device__ __forceinline__ void gather(const CoreBwdArgs& a, int b, int tid, int j, int n,
                                                   const int (&n_mod)[NPA], int l, int cnt,
                                                   const int (&ids)[KP], const uint2 (&ws)[NPA][KP],
                                                   double* part_l) {
 #pragma unroll
         for (int q0 = 0; q0 < KP; q0 += 4)
-            if (cnt > q0) gather4(a, b, tid, n, n_mod, l, q0, cnt, ids, ws, part_l);
+            if (cnt > q0) gather4(a, b, tid, j, n, n_mod, l, q0, cnt, ids, ws, part_l);
     }
 
     // The lambda_V jump of this lane's spike at position q of a round.
@@ -321,7 +325,14 @@ struct BwdCore {
             }
             A += Ap;
         }
-        // tau_m dV/dt just before the crossing is I- - theta (V- = theta)
+        jump_apply(a, A, I, lv, deg);
+    }
+
+    // lambda_V of a spike with jump numerator A (the extra terms and the
+    // delayed postsynaptic sums): tau_m dV/dt just before the crossing is
+    // I- - theta (V- = theta).
+    static __device__ __forceinline__ void jump_apply(const CoreBwdArgs& a, double A, float I, double& lv,
+                                                      unsigned long long& deg) {
         const double den = __dsub_rn((double)I, a.theta);
         if (den > 0.0) {
             lv = __dadd_rn(lv, __dadd_rn(__dmul_rn(a.theta, lv), A) / den);
@@ -330,15 +341,147 @@ struct BwdCore {
         }
     }
 
+    // Cluster mode, one exchange round (slot l KP + q: spike q of the round in
+    // layer l, partials part_r[slot][4]).  This workgroup's share of every
+    // slot's jump sum, its four row partials added in order, goes out as two
+    // tagged 32-bit halves (word 2 slot + h of its block, blocks G apart in
+    // workgroup order).  The slots of spikes owned here (mine[l] > 0) are
+    // listed in LDS; lanes fetch the G shares of each, one word per request
+    // (request (s G + g') 2 + h: half h of workgroup g's share of listed slot
+    // s), and each owner adds its slot's shares in workgroup order into
+    // sum[l].  Lanes below G also read one word of every block: no workgroup
+    // publishes round r + 2 (which reuses this parity's buffer) before all
+    // have read round r.  false: the wait gave up.
+    static __device__ __forceinline__ bool exchange(const CoreBwdArgs& a, int c, int g, int rnd,
+                                                    const double* part_r, const int (&mine)[NL],
+                                                    double (&sum)[NL]) {
+        constexpr int NS = NL * KP, NWD = 2 * NS;     // slots, words per block
+        constexpr int RM = 4;                          // requests per lane and pass
+        const int lane = threadIdx.x & 63, G = a.cl.G;
+        const unsigned tag = a.cl.tag0 + 2u * (unsigned)rnd;
+        unsigned long long* X = a.cl.x + ((size_t)c * 2 + (rnd & 1)) * (size_t)G * NWD;
+#pragma unroll
+        for (int k0 = 0; k0 < NWD; k0 += 64) {
+            const int k = k0 + lane;
+            if (k < NWD) {
+                const double* pq = part_r + (size_t)(k >> 1) * 4;
+                const double v = ((pq[0] + pq[1]) + pq[2]) + pq[3];
+                const unsigned long long u = (unsigned long long)__double_as_longlong(v);
+                cl_put(X + (size_t)g * NWD + k, tag, (k & 1) ? (unsigned)(u >> 32) : (unsigned)u);
+            }
+        }
+        // own slots, compacted in layer then lane order
+        int* list = reinterpret_cast<int*>(smem + a.cl_off);                 // [NS]
+        unsigned* buf = reinterpret_cast<unsigned*>(smem + a.cl_off) + NS;   // [NS][GM][2]
+        int m = 0, pos[NL];
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            const bool own = mine[l] > 0;
+            const unsigned long long bm = __ballot(own);
+            pos[l] = m + lanes_below(bm);
+            if (own) list[pos[l]] = l * KP + mine[l] - 1;
+            m += __popcll(bm);
+        }
+        __syncthreads();
+        const int nreq = 2 * G * m;
+        for (int r0 = 0; r0 == 0 || r0 < nreq; r0 += 64 * RM) {
+            int adr[RM];
+            bool need[RM];
+#pragma unroll
+            for (int u = 0; u < RM; ++u) {
+                const int r = r0 + u * 64 + lane;
+                need[u] = r < nreq;
+                const int rr = need[u] ? r : 0;
+                const int sl = (m > 0) ? list[rr / (2 * G)] : 0;
+                const int gp = (rr % (2 * G)) >> 1;
+                adr[u] = gp * NWD + 2 * sl + (rr & 1);
+            }
+            bool hdr = r0 == 0 && lane < G;
+            unsigned pay[RM];
+            for (int spin = 0;; ++spin) {
+                unsigned long long w[RM], hw = 0;
+#pragma unroll
+                for (int u = 0; u < RM; ++u)
+                    if (need[u]) w[u] = __hip_atomic_load(X + adr[u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (hdr) hw = __hip_atomic_load(X + (size_t)lane * NWD, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                bool pending = false;
+#pragma unroll
+                for (int u = 0; u < RM; ++u) {
+                    if (need[u] && (unsigned)(w[u] >> 32) == tag) {
+                        pay[u] = (unsigned)w[u];
+                        need[u] = false;
+                        buf[r0 + u * 64 + lane] = pay[u];
+                    }
+                    pending |= need[u];
+                }
+                if (hdr && (unsigned)(hw >> 32) == tag) hdr = false;
+                pending |= hdr;
+                if (__ballot(pending) == 0) break;
+                if ((spin & 255) == 255) {
+                    if (__hip_atomic_load(&a.st->cl_abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return false;
+                    if (spin >= kClusterSpins) {
+                        __hip_atomic_store(&a.st->cl_abort, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        return false;
+                    }
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            sum[l] = 0.0;
+            if (!mine[l]) continue;
+            const unsigned* bs = buf + (size_t)pos[l] * 2 * G;
+            double acc = 0.0;
+            for (int gp = 0; gp < G; ++gp) {
+                const unsigned long long u =
+                    ((unsigned long long)bs[2 * gp + 1] << 32) | (unsigned long long)bs[2 * gp];
+                acc += __longlong_as_double((long long)u);
+            }
+            sum[l] = acc;
+        }
+        return true;
+    }
+
     struct Lane {
         double lv[NL], lI[NL];
         unsigned long long deg;
         int rnd;
+        int xr;                        // cluster exchanges so far
     };
 
-    // One reverse-time step n with the loads of A, issuing those of B.
-    static __device__ __forceinline__ void step(const CoreBwdArgs& a, int b, int tid, int n,
-                                                const State& A, State& B, Lane& L) {
+    // The jumps of a round: this lane's spikes (position mine[l] - 1 among
+    // the round's spikes of layer l) with the round's partials part_r.
+    // Cluster mode exchanges the partials first (rounds without spikes do
+    // not exchange; every workgroup of a cluster sees the same rounds).
+    // false: the exchange gave up.
+    static __device__ __forceinline__ bool jumps(const CoreBwdArgs& a, int c, int g, const double* part_r,
+                                                 bool any, const int (&mine)[NL], const float (&I)[NL],
+                                                 const double (&A2)[NL], Lane& L) {
+        if constexpr (CL) {
+            if (!any) return true;
+            double sm[NL];
+            if (!exchange(a, c, g, L.xr++, part_r, mine, sm)) return false;
+#pragma unroll
+            for (int l = 0; l < NL; ++l)
+                if (mine[l]) jump_apply(a, A2[l] + sm[l], I[l], L.lv[l], L.deg);
+        } else {
+#pragma unroll
+            for (int l = 0; l < NL; ++l) {
+                if (!mine[l]) continue;
+                const double* part_l = part_r + (size_t)l * KP * (4 * a.NW);
+                jump(a, part_l, mine[l] - 1, I[l], A2[l], L.lv[l], L.deg);
+            }
+        }
+        return true;
+    }
+
+    // One reverse-time step n with the loads of A, issuing those of B.  c, g:
+    // cluster and rank of the workgroup (cluster mode; else 0); j: the
+    // lane's neuron.  false: a cluster exchange gave up.
+    static __device__ __forceinline__ bool step(const CoreBwdArgs& a, int b, int c, int g, int tid,
+                                                int j, int n, const State& A, State& B, Lane& L) {
         const int T = a.T, LT = a.lif_total;
         double* part = reinterpret_cast<double*>(smem + a.part_off);   // [2][NL][KP][4 NW]
         // n modulo the adjoint-ring slots of each post layer read by layer l
@@ -351,24 +494,24 @@ struct BwdCore {
         // the loads issued one step ago (A) have landed: wait for them once,
         // here, so that no later use waits for this step's loads
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
-        advance(a, b, tid, n, A, B);
+        advance(a, b, j, n, A, B);
 
         // ---- adjoint free dynamics, trajectory, adjoint ring
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
             const BwdLayer& y = a.ly[l];
-            if (tid >= y.n) continue;
+            if (j >= y.n) continue;
             if (n <= T - 2) {
                 const double v = L.lv[l];
                 L.lI[l] = __dadd_rn(__dmul_rn(a.beta, L.lI[l]), __dmul_rn(a.cc, v));
                 L.lv[l] = __dmul_rn(a.alpha, v);
             }
             const double d = __dsub_rn(L.lI[l], L.lv[l]);
-            a.traj[((size_t)b * T + n) * LT + y.lif_off + tid] = make_double2(L.lI[l], d);
+            a.traj[((size_t)b * T + n) * LT + y.lif_off + j] = make_double2(L.lI[l], d);
             if (y.ring_lds == -2) continue;
             const int n_own = n % y.S;
             if (RL)
-                ((lds_f64*)(smem + y.ring_lds))[n_own * y.n + tid] = d;
+                ((lds_f64*)(smem + y.ring_lds))[n_own * (CL ? 64 : y.n) + tid] = d;
             else
                 ((global_f64*)(y.ring + ((size_t)b * y.S + n_own) * y.n))[tid] = d;
         }
@@ -377,20 +520,18 @@ struct BwdCore {
         {
             const int pb = L.rnd & 1;
             ++L.rnd;
+            bool any = false;
             if (NP > 0) {
 #pragma unroll
                 for (int l = 0; l < NL; ++l) {
                     double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
-                    gather(a, b, tid, n, nm[l], l, A.cnt3[l], A.id3[l], A.ws[l], part_l);
+                    gather(a, b, tid, j, n, nm[l], l, A.cnt3[l], A.id3[l], A.ws[l], part_l);
+                    any |= A.cnt3[l] > 0;
                 }
             }
             __syncthreads();
-#pragma unroll
-            for (int l = 0; l < NL; ++l) {
-                if (!A.mine[l]) continue;
-                const double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
-                jump(a, part_l, A.mine[l] - 1, A.I[l], A.A2[l], L.lv[l], L.deg);
-            }
+            if (!jumps(a, c, g, part + (size_t)pb * NL * KP * (4 * a.NW), any, A.mine, A.I, A.A2, L))
+                return false;
         }
         // ---- further rounds when a step has more than KP spikes
         int rounds = 1;
@@ -412,22 +553,25 @@ struct BwdCore {
                 for (int q = 0; q < KP; ++q)
                     ids[q] = y.recn[(size_t)b * a.cap + min(max(A.ri3[l] + r * KP + q, 0), capm)];
                 uint2 ws[NPA][KP];
-                load_step(a, b, tid, l, A.ri3[l], cnt, ids, r * KP, ws, mine[l], I[l], A2[l]);
+                load_step(a, b, j, l, A.ri3[l], cnt, ids, r * KP, ws, mine[l], I[l], A2[l]);
                 double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
-                if (NP > 0) gather(a, b, tid, n, nm[l], l, cnt, ids, ws, part_l);
+                if (NP > 0) gather(a, b, tid, j, n, nm[l], l, cnt, ids, ws, part_l);
             }
             __syncthreads();
-#pragma unroll
-            for (int l = 0; l < NL; ++l) {
-                if (!mine[l]) continue;
-                const double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
-                jump(a, part_l, mine[l] - 1, I[l], A2[l], L.lv[l], L.deg);
-            }
+            if (!jumps(a, c, g, part + (size_t)pb * NL * KP * (4 * a.NW), true, mine, I, A2, L))
+                return false;
         }
+        return true;
     }
 
     static __device__ void run(const CoreBwdArgs& a) {
-        const int b = blockIdx.x, tid = threadIdx.x;
+        if (CL && a.st->cl_abort) return;
+        const int tid = threadIdx.x;
+        // cluster mode: workgroup g of cluster c serves sample b0 + c
+        int c = 0, g = 0;
+        if (CL) cluster_rank((int)blockIdx.x, a.cl.G, c, g);
+        const int b = CL ? a.cl.b0 + c : (int)blockIdx.x;
+        const int j = CL ? g * 64 + tid : tid;
         const int T = a.T;
         Lane L;
 #pragma unroll
@@ -437,6 +581,7 @@ struct BwdCore {
         }
         L.deg = 0;
         L.rnd = 0;
+        L.xr = 0;
         State A, B;
         // step T - 1's data and step T - 2's table row, before the loop
 #pragma unroll
@@ -445,23 +590,24 @@ struct BwdCore {
             load_row(a.ly[l], b, T, max(T - 2, 0), A.cnt2[l], A.ri2[l], A.id2[l]);
             A.cnt3[l] = __builtin_amdgcn_readfirstlane(A.cnt3[l]);
             A.ri3[l] = __builtin_amdgcn_readfirstlane(A.ri3[l]);
-            load_step(a, b, tid, l, A.ri3[l], A.cnt3[l], A.id3[l], 0, A.ws[l], A.mine[l], A.I[l],
+            load_step(a, b, j, l, A.ri3[l], A.cnt3[l], A.id3[l], 0, A.ws[l], A.mine[l], A.I[l],
                       A.A2[l]);
         }
         int n = T - 1;
         for (; n >= 1; n -= 2) {
-            step(a, b, tid, n, A, B, L);
-            step(a, b, tid, n - 1, B, A, L);
+            if (!step(a, b, c, g, tid, j, n, A, B, L)) return;
+            if (!step(a, b, c, g, tid, j, n - 1, B, A, L)) return;
         }
-        if (n == 0) step(a, b, tid, 0, A, B, L);
+        if (n == 0 && !step(a, b, c, g, tid, j, 0, A, B, L)) return;
         if (L.deg) atomicAdd(&a.st->degenerate, L.deg);
     }
 };
 
-// RL: every adjoint ring lives in LDS (else every one in HBM).
-template <int MAXT, int NL, int KP, int NP, bool RL>
+// RL: every adjoint ring lives in LDS (else every one in HBM).  CL: cluster
+// mode (one wave per workgroup, LDS rings).
+template <int MAXT, int NL, int KP, int NP, bool RL, bool CL = false>
 __global__ void __launch_bounds__(MAXT) backward_core_kernel(CoreBwdArgs a) {
-    BwdCore<MAXT, NL, KP, NP, RL>::run(a);
+    BwdCore<MAXT, NL, KP, NP, RL, CL>::run(a);
 }
 
 // ------------------------------------------------------------------ grouping
@@ -820,6 +966,42 @@ hipError_t launch_backward_core(const CoreBwdArgs& a, int n_lif, int threads, si
     return hipGetLastError();
 }
 
+// Cluster mode: 64-thread workgroups, every adjoint ring in LDS, G
+// workgroups per sample, one cooperative launch (the runtime refuses a grid
+// that cannot be resident at once, so every wait of a cluster ends).
+template <int NL, int NP>
+static const void* bcl_fn() {
+    return (const void*)backward_core_kernel<64, NL, bwd_prefetch_cl(NL), NP, true, true>;
+}
+
+static const void* bcl_kernel(int n_lif, int np) {
+    switch (n_lif * 4 + np) {
+        case 4 + 1: return bcl_fn<1, 1>();
+        case 8 + 1: return bcl_fn<2, 1>();
+        case 8 + 2: return bcl_fn<2, 2>();
+        case 12 + 1: return bcl_fn<3, 1>();
+        case 12 + 2: return bcl_fn<3, 2>();
+        case 16 + 1: return bcl_fn<4, 1>();
+        case 16 + 2: return bcl_fn<4, 2>();
+        default: return nullptr;
+    }
+}
+
+hipError_t launch_backward_core_cluster(const CoreBwdArgs& a, int n_lif, int np, int grid, size_t lds,
+                                        hipStream_t s) {
+    const void* f = bcl_kernel(n_lif, np);
+    if (!f || a.NW != 1 || a.cl.G < 1 || grid < a.cl.G || grid % a.cl.G) return hipErrorInvalidValue;
+    CoreBwdArgs arg = a;
+    void* args[] = {&arg};
+    return hipLaunchCooperativeKernel(f, dim3(grid), dim3(64), args, (unsigned)lds, s);
+}
+
+hipError_t backward_cluster_occupancy(int n_lif, int np, size_t lds, int* blocks_per_cu) {
+    const void* f = bcl_kernel(n_lif, np);
+    if (!f) return hipErrorInvalidValue;
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, f, 64, lds);
+}
+
 hipError_t launch_group(const GroupArgs& a, int B, hipStream_t s) {
     const size_t lds = sizeof(int) * ((size_t)a.n + 1 + 1024);
     hipLaunchKernelGGL(group_kernel, dim3(B), dim3(1024), lds, s, a);
@@ -866,6 +1048,9 @@ hipError_t launch_grad_reduce(const GradArgs& a, int P, hipStream_t s) {
     (const void*)backward_core_kernel<M, 3, 4, 1, R>, (const void*)backward_core_kernel<M, 3, 4, 2, R>, \
     (const void*)backward_core_kernel<M, 4, 4, 1, R>, (const void*)backward_core_kernel<M, 4, 4, 2, R>
 #define CORE_FNS(M) CORE_FNS2(M, true), CORE_FNS2(M, false)
+#define CORE_FNS_CL                                                                               \
+    bcl_fn<1, 1>(), bcl_fn<2, 1>(), bcl_fn<2, 2>(), bcl_fn<3, 1>(), bcl_fn<3, 2>(), bcl_fn<4, 1>(),   \
+        bcl_fn<4, 2>()
 
 hipError_t set_backward_lds_limits(size_t bytes, int* bad) {
     const void* fns[] = {(const void*)readout_adjoint_kernel, CORE_FNS(256), CORE_FNS(1024),
@@ -874,7 +1059,7 @@ hipError_t set_backward_lds_limits(size_t bytes, int* bad) {
                          (const void*)gradients_kernel<4, 8, false>, (const void*)gradients_kernel<2, 4, false>,
                          (const void*)gradients_kernel<2, 8, false>, (const void*)gradients_kernel<1, 4, false>,
                          (const void*)gradients_kernel<1, 8, false>, (const void*)gradients_kernel<8, 4, true>,
-                         (const void*)gradients_kernel<8, 8, true>};
+                         (const void*)gradients_kernel<8, 8, true>, CORE_FNS_CL};
     for (int i = 0; i < (int)(sizeof(fns) / sizeof(fns[0])); ++i) {
         const hipError_t e =
             hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);

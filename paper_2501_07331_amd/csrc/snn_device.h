@@ -118,15 +118,17 @@ __device__ __forceinline__ int nth_bit(unsigned long long word, int r) {
 
 // Set bits of a spike-mask row, ascending: skip the first `skip`, return the
 // next N (-1 past the end), uniform.  Up to four words (m: the row's words,
-// uniform) lane q finds set bit number skip + q branch-free and the ids are
-// read from lanes 0 .. N-1; longer rows (row: the same NW words in LDS) are
-// walked word by word at run time, which keeps the code small.
-template <int NWM, int N>
+// uniform), or any number with LP, lane q finds set bit number skip + q
+// branch-free and the ids are read from lanes 0 .. N-1; longer rows (row: the
+// same NW words in LDS) are otherwise walked word by word at run time, which
+// keeps the code small but puts an LDS round trip on every word (LP suits a
+// lone wave, whose every LDS latency is exposed).
+template <int NWM, int N, bool LP = false>
 __device__ __forceinline__ void word_ids(const unsigned long long (&m)[NWM],
                                          const unsigned long long* row, int NW, int skip,
                                          int (&ids)[N]) {
     static_assert(N <= 64, "one lane per id");
-    if constexpr (NWM > 4) {
+    if constexpr (NWM > 4 && !LP) {
         BitIter it = bits_begin(row, NW);
         for (;;) {
             const int c = __popcll(it.cur);
@@ -157,6 +159,63 @@ __device__ __forceinline__ void word_ids(const unsigned long long (&m)[NWM],
 
 // s_waitcnt vmcnt(0), expcnt and lgkmcnt left at their maximum (gfx9 encoding)
 constexpr int kWaitVm0 = 0x0F70;
+
+// ------------------------------------------------------------------ cluster exchange
+
+// Cluster and rank of workgroup k of a cluster launch (G workgroups per
+// cluster).  Workgroups are dealt to the 8 XCDs round robin (k mod 8), so
+// when G is a multiple of 8 the ranks are dealt the same way: every XCD
+// serves G / 8 ranks, i.e. the same column slices of every weight matrix in
+// all clusters, which its L2 keeps.  Any other G: consecutive workgroups.
+// Either way a bijection onto (cluster, rank).
+__device__ __forceinline__ void cluster_rank(int k, int G, int& c, int& g) {
+    if (G % 8 == 0) {
+        const int per = G / 8, i = k / 8;
+        g = (k % 8) * per + i % per;
+        c = i / per;
+    } else {
+        c = k / G;
+        g = k % G;
+    }
+}
+
+// Polls after which a cluster wait gives up (a poll is one device-memory
+// round trip of about a microsecond, so about two seconds): the wave then
+// raises the abort flag and its kernel returns; every other wait of the
+// launch sees the flag within 256 polls and returns too.
+constexpr int kClusterSpins = 1 << 21;
+
+// Word p <- (tag, payload), one agent-scope atomic store.
+__device__ __forceinline__ void cl_put(unsigned long long* p, unsigned tag, unsigned payload) {
+    __hip_atomic_store(p, ((unsigned long long)tag << 32) | payload, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Every lane with want waits until word X[k] carries tag and takes its
+// payload (the wave polls until all of them have); all 64 lanes call it.
+// false: the wait gave up or another wave did (the abort flag is set).
+__device__ __forceinline__ bool cl_get(const unsigned long long* X, int k, bool want, unsigned tag,
+                                      unsigned& v, int* abort_flag) {
+    bool ok = !want;
+    unsigned long long w = 0;
+    for (int spin = 0;; ++spin) {
+        if (!ok) {
+            w = __hip_atomic_load(X + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            ok = (unsigned)(w >> 32) == tag;
+        }
+        if (__ballot(!ok) == 0) break;
+        if ((spin & 255) == 255) {
+            if (__hip_atomic_load(abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return false;
+            if (spin >= kClusterSpins) {
+                __hip_atomic_store(abort_flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                return false;
+            }
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+    v = (unsigned)w;
+    return true;
+}
 
 // One leaky-integrator neuron (a LIF neuron without threshold).
 struct LiState {

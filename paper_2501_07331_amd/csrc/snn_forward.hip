@@ -13,8 +13,13 @@ __global__ void reset_status_kernel(DevStatus* st) {
         st->clamped = 0;
         st->degenerate = 0;
         st->reg_loss = 0.0;
+        st->cl_abort = 0;
         for (int l = 0; l < SNN_MAX_LAYERS; ++l) st->layer_spikes[l] = 0;
     }
+}
+
+__global__ void clear_abort_kernel(DevStatus* st) {
+    if (threadIdx.x == 0) st->cl_abort = 0;
 }
 
 // One workgroup per sample: offsets, label, ranges, strict (step, neuron) order.
@@ -500,6 +505,11 @@ hipError_t launch_reset_status(DevStatus* st, hipStream_t s) {
     return hipGetLastError();
 }
 
+hipError_t launch_clear_abort(DevStatus* st, hipStream_t s) {
+    hipLaunchKernelGGL(clear_abort_kernel, dim3(1), dim3(64), 0, s, st);
+    return hipGetLastError();
+}
+
 hipError_t launch_validate(const int* off, const int* step, const int* neuron, int nnz, int B, int T,
                            int n_in, const int* labels, int C, DevStatus* st, hipStream_t s) {
     hipLaunchKernelGGL(validate_kernel, dim3(B), dim3(256), 0, s, off, step, neuron, nnz, B, T, n_in,
@@ -619,6 +629,10 @@ hipError_t set_core_lds_limits(size_t bytes, int* bad) {
     if (e == hipSuccess) {
         e = set_core_lds_limits_1024(bytes, bad);
         if (e != hipSuccess && bad) *bad += 32;   // 1024-thread kernels: 32 .. 47
+    }
+    if (e == hipSuccess) {
+        e = set_core_lds_limits_cl(bytes, bad);
+        if (e != hipSuccess && bad) *bad += 48;   // cluster kernels: 48 ..
     }
     return e;
 }

@@ -34,13 +34,18 @@
 
 namespace {
 
-template <int MAXT, int NL, int NP, bool RL, bool RO>
+template <int MAXT, int NL, int NP, bool RL, bool RO, bool CL>
 struct FwdCore {
-    static constexpr int NWM = MAXT / 64;
+    static_assert(!CL || (MAXT == 64 && RL && !RO), "cluster mode: 64 neurons a workgroup, LDS rings");
+    static constexpr int NPA = NP > 0 ? NP : 1;
+    // mask words of a layer: one per wave, or (cluster) one per workgroup
+    static constexpr int NWM = CL ? SNN_MAX_NEURONS / 64 : MAXT / 64;
     // spikes per chunk of the scatter: with rings in device memory every
     // chunk costs serialized round trips (weights, cells, stores), so wide
-    // layers, which carry tens of spikes per step, take larger chunks there
-    static constexpr int KI = (RL || MAXT <= 256) ? KB : 16;
+    // layers, which carry tens of spikes per step, take larger chunks there;
+    // so does a cluster's step, whose weight loads all go out together (a
+    // lone wave has the registers)
+    static constexpr int KI = CL ? (NL <= 2 ? 32 : 16) : (RL || MAXT <= 256) ? KB : 16;
 
     // Load in flight for the next step: its input arrival.
     struct Pre {
@@ -70,16 +75,16 @@ struct FwdCore {
                                                  0x00020000);
     }
 
-    // Weights and slots of spikes ids[0 .. N) of layer l for this lane's post
-    // of projection pp (rows clamped into the matrix; results of ids < 0 or of
+    // Weights and slots of spikes ids[0 .. N) of layer l for post j of
+    // projection pp (rows clamped into the matrix; results of ids < 0 or of
     // unused projection entries are not used).
     template <int N>
-    static __device__ __forceinline__ void load_ws(const CoreFwdArgs& a, int l, int pp, int tid,
+    static __device__ __forceinline__ void load_ws(const CoreFwdArgs& a, int l, int pp, int j,
                                                    const int (&ids)[N], uint2 (&w)[N]) {
         const FwdLayer& y = a.ly[l];
         const int nq = y.nq[pp], rmax = y.npre[pp] - 1;
         const __amdgpu_buffer_rsrc_t rs = ws_rsrc(a, l, pp);
-        const int col8 = min(tid, nq - 1) * 8;
+        const int col8 = min(j, nq - 1) * 8;
 #pragma unroll
         for (int q = 0; q < N; ++q) {
             const int r = min(max(ids[q], 0), rmax);
@@ -90,20 +95,24 @@ struct FwdCore {
 
     // Adds the weights of spikes 0 .. N) (valid below cnt) emitted at step e to
     // the ring cells of their arrivals, arrivals before T, in chunks of C.
+    // The lane's ring column is tid, of post j (the same but in cluster
+    // mode, whose rings hold the workgroup's 64 columns).
     template <int N, int C>
     static __device__ __forceinline__ void scatter(const CoreFwdArgs& a, int b, int l, int pp, int tid,
-                                                   int e, int cnt, const uint2 (&w)[N]) {
+                                                   int j, int e, int cnt, const uint2 (&w)[N]) {
         const FwdLayer& y = a.ly[l];
         const int nq = y.nq[pp], S = y.S[pp];
-        const bool live = pp < y.npost && tid < nq;
+        const int rw = CL ? 64 : nq;                  // ring row width
+        const bool live = pp < y.npost && j < nq;
         const int e_mod = e % S;
-        RingPtr col = ring_col<RingPtr>(a, b, l, pp, min(tid, nq - 1));
-        int stride = nq;
+        RingPtr col = ring_col<RingPtr>(a, b, l, pp, CL ? tid : min(tid, nq - 1));
+        int stride = rw;
         if constexpr (RL) {
-            // lanes past the layer, whose column is another lane's, add
-            // every spike to row S (dummy) of it: stride 0 from that cell
-            col = live ? col : col + S * nq;
-            stride = live ? nq : 0;
+            // lanes past the layer add every spike to row S (dummy) of their
+            // column (outside cluster mode another lane's): stride 0 from that
+            // cell
+            col = live ? col : col + S * rw;
+            stride = live ? rw : 0;
         }
 #pragma unroll
         for (int q0 = 0; q0 < N; q0 += C) {
@@ -130,27 +139,60 @@ struct FwdCore {
                     wv[k] = __uint_as_float(w[q].x);
                 }
             }
-            column_add(col, stride, row, wv);
+            if constexpr (CL) {
+                // a lone wave, whose every LDS latency is exposed: rounds of
+                // 8 (four LDS round trips for 32 spikes; fp32 LDS atomics
+                // would keep the order too but cost about 64 cycles each)
+                column_add_rounds<8>(col, stride, row, wv);
+            } else {
+                column_add(col, stride, row, wv);
+            }
         }
     }
 
     // All spikes of layer l at step e (mask words m), from position `from` on,
     // in chunks of KB with their weights loaded now.
-    static __device__ __forceinline__ void scatter_rest(const CoreFwdArgs& a, int b, int l, int tid, int e,
-                                        const unsigned long long (&m)[NWM],
-                                        const unsigned long long* row, int from, int total) {
+    static __device__ __forceinline__ void scatter_rest(const CoreFwdArgs& a, int b, int l, int tid,
+                                                        int j, int e, const unsigned long long (&m)[NWM],
+                                                        const unsigned long long* row, int from, int total) {
         const FwdLayer& y = a.ly[l];
         for (int q0 = from; q0 < total; q0 += KI) {
             int ids[KI];
-            word_ids<NWM, KI>(m, row, a.NW, q0, ids);
+            word_ids<NWM, KI, CL>(m, row, a.NW, q0, ids);
 #pragma unroll
             for (int pp = 0; pp < NP; ++pp) {
                 if (pp >= y.npost) continue;
                 uint2 w[KI];
-                load_ws<KI>(a, l, pp, tid, ids, w);
-                scatter<KI, KI>(a, b, l, pp, tid, e, total - q0, w);
+                load_ws<KI>(a, l, pp, j, ids, w);
+                scatter<KI, KI>(a, b, l, pp, tid, j, e, total - q0, w);
             }
         }
+    }
+
+    // Cluster mode: this workgroup's ballot masks m[l] of step n go out as
+    // tagged 32-bit halves (word (l G + g) 2 + h of the step's exchange), and
+    // the words of all G workgroups come back into the LDS mask rows of the
+    // step (the same layout: a 64-bit mask word is its two halves).  false:
+    // the wait gave up.
+    static __device__ __forceinline__ bool exchange(const CoreFwdArgs& a, int c, int g, int n,
+                                                    const unsigned long long (&m)[NL], unsigned* lds_rows) {
+        const int lane = threadIdx.x & 63, G = a.cl.G, nw = 2 * NL * G;
+        const unsigned tag = a.cl.tag0 + 2u * (unsigned)n;
+        unsigned long long* X = a.cl.x + ((size_t)c * 2 + (n & 1)) * nw;
+        if (lane < 2 * NL) {
+            unsigned long long ml = m[0];
+#pragma unroll
+            for (int l = 1; l < NL; ++l) ml = ((lane >> 1) == l) ? m[l] : ml;
+            cl_put(X + ((lane >> 1) * G + g) * 2 + (lane & 1), tag,
+                   (lane & 1) ? (unsigned)(ml >> 32) : (unsigned)ml);
+        }
+        for (int k0 = 0; k0 < nw; k0 += 64) {
+            const int k = k0 + lane;
+            unsigned v;
+            if (!cl_get(X, min(k, nw - 1), k < nw, tag, v, &a.st->cl_abort)) return false;
+            if (k < nw) lds_rows[k] = v;
+        }
+        return true;
     }
 
     // ---- the fused readout wave (RO)
@@ -257,94 +299,57 @@ struct FwdCore {
         a.If[(size_t)b * a.nstate + (a.nstate - C) + lane] = q.I;
     }
 
-    static __device__ __forceinline__ void step(const CoreFwdArgs& a, int b, int tid, int n,
-                                                const Pre& P, Pre& N, Lane& L) {
-        const int lane = tid & 63, wave = tid >> 6;
-        const int T = a.T, NW = a.NW;
-        unsigned long long* masks = reinterpret_cast<unsigned long long*>(smem + a.mask_off);
-        const int par = n % 3;
-
-        // ---- free dynamics over one step, threshold, reset, ballots
-        bool spk[NL];
+    // Free dynamics over one step, threshold, reset and ballots of this
+    // lane's neuron j in every LIF layer: spk[l], and the wave's masks m[l].
+    static __device__ __forceinline__ void dynamics(const CoreFwdArgs& a, int j, Lane& L, bool (&spk)[NL],
+                                                    unsigned long long (&m)[NL]) {
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
             spk[l] = false;
-            if (tid < a.ly[l].n) {
+            if (j < a.ly[l].n) {
                 const float gi = __fmul_rn(a.gamma, L.I[l]);
                 const float Vm = __fmaf_rn(a.alpha, L.V[l], gi);
                 L.I[l] = __fmul_rn(a.beta, L.I[l]);
                 spk[l] = Vm >= a.theta;
                 L.V[l] = spk[l] ? 0.0f : Vm;
             }
-            const unsigned long long m = __ballot(spk[l]);
-            if (lane == 0) masks[(size_t)(par * NL + l) * NW + wave] = m;
+            m[l] = __ballot(spk[l]);
         }
-        __syncthreads();
+    }
 
-        // ---- counts and this lane's rank among the step's spikes
-        // (ascending neuron order)
-        unsigned long long mw[NL][NWM];
-        int tot[NL], rank[NL], cnt0[NL];
+    // Spikes of every layer at the step (LDS mask rows `rows`), and this
+    // lane's rank among them (ascending neuron order; the lane's mask word
+    // wv: its wave's, or in cluster mode its workgroup's, with own bits m).
+    static __device__ __forceinline__ void counts(const CoreFwdArgs& a, const unsigned long long* rows, int wv,
+                                                  const unsigned long long (&m)[NL],
+                                                  unsigned long long (&mw)[NL][NWM], int (&tot)[NL],
+                                                  int (&rank)[NL], int (&cnt0)[NL], Lane& L) {
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
-            row_words<NWM>(masks + (size_t)(par * NL + l) * NW, NW, mw[l]);
+            row_words<NWM>(rows + (size_t)l * a.NW, a.NW, mw[l]);
             int before = 0, total = 0;
-            unsigned long long own = 0;
 #pragma unroll
             for (int w = 0; w < NWM; ++w) {
-                const int c = __popcll(mw[l][w]);
-                total += c;
-                before += (w < wave) ? c : 0;
-                own = (w == wave) ? mw[l][w] : own;
+                const int cw = __popcll(mw[l][w]);
+                total += cw;
+                before += (w < wv) ? cw : 0;
             }
-            rank[l] = before + lanes_below(own);
+            rank[l] = before + lanes_below(m[l]);
             cnt0[l] = L.cnt[l];
             L.cnt[l] += total;
             tot[l] = total;
         }
+    }
 
-        // the input arrival loaded a step ago (P) has landed
-        __builtin_amdgcn_s_waitcnt(kWaitVm0);
-
-        // ---- this step's spikes into the rings (all delays)
-#pragma unroll
-        for (int l = 0; l < NL; ++l)
-            scatter_rest(a, b, l, tid, n, mw[l], masks + (size_t)(par * NL + l) * NW, 0, tot[l]);
-        N.ain = a.A_in[((size_t)b * T + min(n + 1, T - 1)) * a.n1 + min(tid, a.n1 - 1)];
-
-        // ---- spike records (I- of this step), step table, overflow
+    // Arrivals at step n: per projection into the layer, in projection order
+    // (P.ain: the input projection's, loaded a step ahead); the lane's ring
+    // column is tid, 64 wide in cluster mode.
+    static __device__ __forceinline__ void arrivals(const CoreFwdArgs& a, int b, int tid, int j, int n,
+                                                    const Pre& P, Lane& L) {
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
             const FwdLayer& y = a.ly[l];
-            int* row = y.steptab + ((size_t)b * T + n) * SNN_STEP_ROW;
-            if (tid == 0) {
-                // internal record indices never pass the capacity (the
-                // caller's count stays exact)
-                y.rec_idx[(size_t)b * (T + 1) + n] = min(cnt0[l], a.cap);
-                row[0] = tot[l];
-                row[1] = min(cnt0[l], a.cap);
-            }
-            if (spk[l]) {
-                ++L.own[l];
-                if (rank[l] < SNN_STEP_IDS) row[2 + rank[l]] = tid;
-                const int pos = cnt0[l] + rank[l];
-                if (pos < a.cap) {
-                    const size_t r = (size_t)b * a.cap + pos;
-                    y.rec_n[r] = tid;
-                    y.rec_s[r] = n;
-                    y.rec_I[r] = L.I[l];
-                    y.out_step[r] = n;
-                    y.out_neuron[r] = tid;
-                }
-            }
-            if (tid == 0 && cnt0[l] + tot[l] > a.cap) a.st->overflow = 1;
-        }
-
-        // ---- arrivals at step n: per projection into the layer, in projection order
-#pragma unroll
-        for (int l = 0; l < NL; ++l) {
-            const FwdLayer& y = a.ly[l];
-            if (tid >= y.n) continue;
+            if (j >= y.n) continue;
 #pragma unroll
             for (int e = 0; e < 2; ++e) {
                 if (e >= y.nin) continue;
@@ -354,18 +359,86 @@ struct FwdCore {
                     add = P.ain;
                 } else {
                     const int S = y.in_S[e], n_mod = n % S;
-                    RingPtr c;
+                    RingPtr rc;
                     if constexpr (RL)
-                        c = (lds_f32*)(reinterpret_cast<float*>(smem) + y.in_ring_lds[e]) + tid;
+                        rc = (lds_f32*)(reinterpret_cast<float*>(smem) + y.in_ring_lds[e]) + tid;
                     else
-                        c = (global_f32*)(y.in_ring[e] + (size_t)b * (S + 1) * y.n) + tid;
-                    c += n_mod * y.n;
-                    add = *c;
-                    *c = 0.0f;
+                        rc = (global_f32*)(y.in_ring[e] + (size_t)b * (S + 1) * y.n) + tid;
+                    rc += n_mod * (CL ? 64 : y.n);
+                    add = *rc;
+                    *rc = 0.0f;
                 }
                 L.I[l] = __fadd_rn(L.I[l], add);
             }
         }
+    }
+
+    // Spike records of step n (neuron, step, I- of this step), the step
+    // table row, the overflow flag.
+    static __device__ __forceinline__ void records(const CoreFwdArgs& a, int b, int g, int tid, int j, int n,
+                                                   const bool (&spk)[NL], const int (&rank)[NL],
+                                                   const int (&cnt0)[NL], const int (&tot)[NL], Lane& L) {
+        const int T = a.T;
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            const FwdLayer& y = a.ly[l];
+            int* row = y.steptab + ((size_t)b * T + n) * SNN_STEP_ROW;
+            if (tid == 0 && g == 0) {
+                // internal record indices never pass the capacity (the
+                // caller's count stays exact)
+                y.rec_idx[(size_t)b * (T + 1) + n] = min(cnt0[l], a.cap);
+                row[0] = tot[l];
+                row[1] = min(cnt0[l], a.cap);
+            }
+            if (spk[l]) {
+                ++L.own[l];
+                if (rank[l] < SNN_STEP_IDS) row[2 + rank[l]] = j;
+                const int pos = cnt0[l] + rank[l];
+                if (pos < a.cap) {
+                    const size_t r = (size_t)b * a.cap + pos;
+                    y.rec_n[r] = j;
+                    y.rec_s[r] = n;
+                    y.rec_I[r] = L.I[l];
+                    y.out_step[r] = n;
+                    y.out_neuron[r] = j;
+                }
+            }
+            if (tid == 0 && cnt0[l] + tot[l] > a.cap) a.st->overflow = 1;
+        }
+    }
+
+    // One step n of one workgroup per sample.
+    static __device__ __forceinline__ void step(const CoreFwdArgs& a, int b, int tid, int n, const Pre& P,
+                                                Pre& N, Lane& L) {
+        const int lane = tid & 63, wave = tid >> 6;
+        const int T = a.T, NW = a.NW;
+        unsigned long long* masks = reinterpret_cast<unsigned long long*>(smem + a.mask_off);
+        const int par = n % 3;
+
+        bool spk[NL];
+        unsigned long long mine[NL];
+        dynamics(a, tid, L, spk, mine);
+        if (lane == 0) {
+#pragma unroll
+            for (int l = 0; l < NL; ++l) masks[(size_t)(par * NL + l) * NW + wave] = mine[l];
+        }
+        __syncthreads();
+
+        unsigned long long mw[NL][NWM];
+        int tot[NL], rank[NL], cnt0[NL];
+        counts(a, masks + (size_t)par * NL * NW, wave, mine, mw, tot, rank, cnt0, L);
+
+        // the input arrival loaded a step ago (P) has landed
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+
+        // ---- this step's spikes into the rings (all delays)
+#pragma unroll
+        for (int l = 0; l < NL; ++l)
+            scatter_rest(a, b, l, tid, tid, n, mw[l], masks + (size_t)(par * NL + l) * NW, 0, tot[l]);
+        N.ain = a.A_in[((size_t)b * T + min(n + 1, T - 1)) * a.n1 + min(tid, a.n1 - 1)];
+
+        records(a, b, 0, tid, tid, n, spk, rank, cnt0, tot, L);
+        arrivals(a, b, tid, tid, n, P, L);
     }
 
     static __device__ __forceinline__ void run_steps(const CoreFwdArgs& a, int b, int tid, Lane& L) {
@@ -379,8 +452,166 @@ struct FwdCore {
         if (n < a.T) step(a, b, tid, n, A, B, L);
     }
 
+    // ---- cluster mode: wave 0 of a workgroup runs its 64 neurons of every
+    // LIF layer (dynamics, the exchange, records, arrivals), wave 1 + r ring
+    // r (the LIF-post projections of the LIF layers, in layer then
+    // projection order): the step's spike ids of its source layer, their
+    // weights for its 64 posts and the ordered adds.  The rings fill in
+    // parallel on the CU's SIMDs, each from one wave in emission order.  Per
+    // step two barriers: after the exchange (the masks are in LDS) and after
+    // the adds (the rings hold the step's arrivals); a wait that gives up
+    // raises an LDS flag before the first, and every wave returns after it.
+
+    // A workgroup barrier over LDS only: this wave's LDS accesses complete,
+    // its device-memory ones may stay in flight.
+    static __device__ __forceinline__ void lds_barrier() {
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0xC07F);       // lgkmcnt(0); vmcnt, expcnt at their maximum
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    }
+
+    // Ring r = (source layer l, its LIF-post projection pp) of this wave
+    // (1 + r), r counted in layer then projection order; false: none.
+    static __device__ __forceinline__ bool ring_of(const CoreFwdArgs& a, int r, int& rl, int& rpp) {
+        int k = 0;
+#pragma unroll
+        for (int l = 0; l < NL; ++l)
+#pragma unroll
+            for (int pp = 0; pp < NP; ++pp)
+                if (pp < a.ly[l].npost) {
+                    if (k == r) {
+                        rl = l;
+                        rpp = pp;
+                        return true;
+                    }
+                    ++k;
+                }
+        return false;
+    }
+
+    static __device__ __forceinline__ int* cl_flag(const CoreFwdArgs& a) {
+        return reinterpret_cast<int*>(smem + a.mask_off + (size_t)3 * NL * a.NW * sizeof(unsigned long long));
+    }
+
+    // The neuron wave's step n.  false: the exchange gave up.
+    static __device__ __forceinline__ bool step_cl(const CoreFwdArgs& a, int b, int c, int g, int lane,
+                                                   int n, const Pre& P, Pre& N, Lane& L) {
+        const int j = g * 64 + lane, T = a.T, NW = a.NW;
+        unsigned long long* masks = reinterpret_cast<unsigned long long*>(smem + a.mask_off);
+        const int par = n % 3;
+        bool spk[NL];
+        unsigned long long mine[NL];
+        dynamics(a, j, L, spk, mine);
+        const bool ok = exchange(a, c, g, n, mine, reinterpret_cast<unsigned*>(masks + (size_t)par * NL * NW));
+        // the next step's input arrival goes out right after the exchange,
+        // so that no load of this wave is in flight when the next exchange
+        // waits for its own (a wait covers every older access)
+        N.ain = a.A_in[((size_t)b * T + min(n + 1, T - 1)) * a.n1 + min(j, a.n1 - 1)];
+        if (!ok && lane == 0) *cl_flag(a) = 1;
+        lds_barrier();                                   // the masks of step n are in
+        if (!ok) return false;
+        unsigned long long mw[NL][NWM];
+        int tot[NL], rank[NL], cnt0[NL];
+        counts(a, masks + (size_t)par * NL * NW, g, mine, mw, tot, rank, cnt0, L);
+        records(a, b, g, lane, j, n, spk, rank, cnt0, tot, L);
+        lds_barrier();                                   // every ring holds step n's arrivals
+        arrivals(a, b, lane, j, n, P, L);
+        return true;
+    }
+
+    // A ring wave: every step, the spikes of its source layer in chunks of
+    // KI, each chunk's weight loads issued together, then added in order.
+    static __device__ __forceinline__ void ring_wave(const CoreFwdArgs& a, int b, int g, int lane, int l,
+                                                     int pp) {
+        const int j = g * 64 + lane;
+        const unsigned long long* masks = reinterpret_cast<const unsigned long long*>(smem + a.mask_off);
+        const int* flag = cl_flag(a);
+        for (int n = 0; n < a.T; ++n) {
+            lds_barrier();                               // the masks of step n are in
+            if (*flag) return;
+            const unsigned long long* row = masks + (size_t)((n % 3) * NL + l) * a.NW;
+            unsigned long long mw[NWM];
+            row_words<NWM>(row, a.NW, mw);
+            int tot = 0;
+#pragma unroll
+            for (int w = 0; w < NWM; ++w) tot += __popcll(mw[w]);
+            for (int q0 = 0; q0 < tot; q0 += KI) {
+                int ids[KI];
+                word_ids<NWM, KI, true>(mw, row, a.NW, q0, ids);
+                uint2 w[KI];
+                load_ws<KI>(a, l, pp, j, ids, w);
+                scatter<KI, KI>(a, b, l, pp, lane, j, n, tot - q0, w);
+            }
+            lds_barrier();                               // every ring holds step n's arrivals
+        }
+    }
+
+    static __device__ __forceinline__ void run_cl(const CoreFwdArgs& a) {
+        const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+        int c, g;
+        cluster_rank((int)blockIdx.x, a.cl.G, c, g);
+        const int b = a.cl.b0 + c, j = g * 64 + lane;
+        int rl = 0, rpp = 0;
+        const bool ring = wave > 0 && ring_of(a, wave - 1, rl, rpp);
+        if (ring) {
+            // the ring's columns, rows 0 .. S (row S: dummy)
+            lds_f32* rc = ring_col<lds_f32*>(a, b, rl, rpp, lane);
+            for (int r = 0; r <= a.ly[rl].S[rpp]; ++r) rc[r * 64] = 0.0f;
+        } else if (wave == 0 && lane == 0) {
+            *cl_flag(a) = 0;
+        }
+        __syncthreads();
+        if (wave > 0) {
+            if (ring) ring_wave(a, b, g, lane, rl, rpp);
+            return;
+        }
+        Lane L;
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            L.V[l] = 0.0f;
+            L.I[l] = 0.0f;
+            L.cnt[l] = 0;
+            L.own[l] = 0;
+        }
+        Pre A, B;
+        A.ain = a.A_in[(size_t)b * a.T * a.n1 + min(j, a.n1 - 1)];
+        int n = 0;
+        for (; n + 1 < a.T; n += 2) {
+            if (!step_cl(a, b, c, g, lane, n, A, B, L)) return;
+            if (!step_cl(a, b, c, g, lane, n + 1, B, A, L)) return;
+        }
+        if (n < a.T && !step_cl(a, b, c, g, lane, n, A, B, L)) return;
+        finish(a, b, g, lane, j, L);
+    }
+
+    // Final state, spike counts per neuron, record counts.
+    static __device__ __forceinline__ void finish(const CoreFwdArgs& a, int b, int g, int tid, int j,
+                                                  const Lane& L) {
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            const FwdLayer& y = a.ly[l];
+            if (j < y.n) {
+                a.Vf[(size_t)b * a.nstate + a.soff[l] + j] = L.V[l];
+                a.If[(size_t)b * a.nstate + a.soff[l] + j] = L.I[l];
+                // integer sums over the samples: exact in any order
+                if (y.ncount && L.own[l]) atomicAdd(&y.ncount[j], L.own[l]);
+            }
+            if (tid == 0 && g == 0) {
+                y.rec_idx[(size_t)b * (a.T + 1) + a.T] = min(L.cnt[l], a.cap);
+                y.rec_cnt[b] = min(L.cnt[l], a.cap);
+                y.out_count[b] = L.cnt[l];
+                atomicAdd(&a.st->layer_spikes[l], (unsigned long long)L.cnt[l]);
+            }
+        }
+    }
+
     static __device__ __forceinline__ void run(const CoreFwdArgs& a) {
-        if (a.st->bad_input) return;
+        if (a.st->bad_input || (CL && a.st->cl_abort)) return;
+        if constexpr (CL) {
+            run_cl(a);
+            return;
+        }
         const int b = blockIdx.x, tid = threadIdx.x;
         // ---- zero the ring columns this lane owns (rows 0 .. S, row S: dummy)
 #pragma unroll
@@ -419,32 +650,17 @@ struct FwdCore {
         }
         __syncthreads();
         run_steps(a, b, tid, L);
-
-        // ---- final state and record counts
-#pragma unroll
-        for (int l = 0; l < NL; ++l) {
-            const FwdLayer& y = a.ly[l];
-            if (tid < y.n) {
-                a.Vf[(size_t)b * a.nstate + a.soff[l] + tid] = L.V[l];
-                a.If[(size_t)b * a.nstate + a.soff[l] + tid] = L.I[l];
-                // integer sums over the samples: exact in any order
-                if (y.ncount && L.own[l]) atomicAdd(&y.ncount[tid], L.own[l]);
-            }
-            if (tid == 0) {
-                y.rec_idx[(size_t)b * (a.T + 1) + a.T] = min(L.cnt[l], a.cap);
-                y.rec_cnt[b] = min(L.cnt[l], a.cap);
-                y.out_count[b] = L.cnt[l];
-                atomicAdd(&a.st->layer_spikes[l], (unsigned long long)L.cnt[l]);
-            }
-        }
+        finish(a, b, 0, tid, tid, L);
     }
 };
 
 // MAXT: the most LIF neurons per layer (threads of the core waves); with RO
-// the workgroup has one more wave.
-template <int MAXT, int NL, int NP, bool RL, bool RO>
-__global__ void __launch_bounds__(MAXT + (RO ? 64 : 0)) forward_core_kernel(CoreFwdArgs a) {
-    FwdCore<MAXT, NL, NP, RL, RO>::run(a);
+// the workgroup has one more wave.  CL: cluster mode (MAXT = 64: the neuron
+// wave, then one wave per ring).
+template <int MAXT, int NL, int NP, bool RL, bool RO, bool CL = false>
+__global__ void __launch_bounds__(CL ? 64 * (1 + NL * NP) : MAXT + (RO ? 64 : 0))
+    forward_core_kernel(CoreFwdArgs a) {
+    FwdCore<MAXT, NL, NP, RL, RO, CL>::run(a);
 }
 
 template <int MAXT, int NL, int NP>

@@ -23,6 +23,7 @@ struct DevStatus {
     unsigned long long degenerate;   // skipped jumps (I- <= theta)
     unsigned long long layer_spikes[SNN_MAX_LAYERS];   // per LIF layer, all samples
     double reg_loss;                 // spike-count penalty of the last forward
+    int cl_abort;                    // a cluster exchange gave up waiting (the results are void)
 };
 
 // Topology, constants and the LDS plan, passed by value to every kernel.
@@ -51,6 +52,24 @@ struct Topo {
     int bring[SNN_MAX_LAYERS];
 };
 
+// Cluster mode of the per-sample cores, for layers whose rings do not fit in
+// one workgroup's LDS: G workgroups of one wave serve one sample, workgroup g
+// owning neurons [64 g, 64 g + 64) of every LIF layer and the LDS ring
+// columns of its neurons.  One launch covers the samples [b0, b0 + gridDim.x
+// / G).  Per step (forward) or per round of spikes (backward) the workgroups
+// of a sample exchange data through device memory as 64-bit words, each a
+// 32-bit payload with a 32-bit tag in the high half: agent-scope atomic
+// stores and loads (coherent across the XCDs' L2 caches), so a word is
+// either old or whole, and a reader knows it is current when its tag is.
+// Tags are odd and advance by 2 per exchange (tag0 at the first), so the
+// zeroed buffer never matches and no stale word of an earlier call does.
+struct ClusterArgs {
+    int G;                             // workgroups per sample; 0: one workgroup per sample
+    int b0;                            // first sample of this launch
+    unsigned tag0;                     // tag of the first exchange of this launch
+    unsigned long long* x;             // exchange words, [clusters][2 (parity)][words per exchange]
+};
+
 // Input projection arrivals: A_in[b][n][j] = sum, in emission order, of the
 // input-projection weights arriving at post j of layer 1 at step n.
 struct InScanArgs {
@@ -70,6 +89,9 @@ struct InScanArgs {
 // covers nearly every step of a 256-neuron layer at 14 spikes per neuron
 // while its input is active (8 left a quarter of them to an extra round).
 constexpr int bwd_prefetch(int n_lif) { return n_lif == 1 ? 16 : 4; }
+// The same in cluster mode, whose one-wave workgroups have registers to
+// spare: a round of spikes costs an exchange between the workgroups there.
+constexpr int bwd_prefetch_cl(int n_lif) { return n_lif <= 2 ? 16 : 8; }
 
 // One LIF layer as seen by the forward core.
 struct FwdLayer {
@@ -118,6 +140,7 @@ struct CoreFwdArgs {
     const uint2* ro_ws;                // readout projection (weight bits, slot) [ro_nfeed][ro_C]
     float* z;                          // [B][C]
     int* nstar;                        // [B][C]
+    ClusterArgs cl;                    // cluster mode (cl.G > 0): every ring in LDS, row width 64
 };
 
 struct ReadoutArgs {
@@ -185,6 +208,8 @@ struct CoreBwdArgs {
     double2* traj;                     // [B][T][lif_total] (lambda_I, lambda_I - lambda_V)
     DevStatus* st;
     int part_off;                      // LDS byte offset of the partial jump sums
+    ClusterArgs cl;                    // cluster mode (cl.G > 0): adjoint rings in LDS, row width 64
+    int cl_off;                        // cluster mode: LDS byte offset of the exchange staging
 };
 
 // Spikes of each sample grouped by presynaptic neuron, in step order.
@@ -301,3 +326,15 @@ bool launch_forward_core_1024(const CoreFwdArgs& a, int n_lif, int np, bool rl, 
 hipError_t set_core_lds_limits_256(size_t bytes, int* bad);
 hipError_t set_core_lds_limits_1024(size_t bytes, int* bad);
 hipError_t set_backward_lds_limits(size_t bytes, int* bad);
+// Cluster mode (CoreFwdArgs::cl, CoreBwdArgs::cl): grid = clusters x G
+// workgroups, launched cooperatively; occupancy in workgroups per CU.  A
+// forward workgroup has 64 (1 + LIF -> LIF rings) threads (a neuron wave and
+// one wave per ring), a backward one 64.
+hipError_t launch_forward_core_cluster(const CoreFwdArgs& a, int n_lif, int np, int grid, int threads,
+                                       size_t lds, hipStream_t s);
+hipError_t forward_cluster_occupancy(int n_lif, int np, int threads, size_t lds, int* blocks_per_cu);
+hipError_t set_core_lds_limits_cl(size_t bytes, int* bad);
+hipError_t launch_backward_core_cluster(const CoreBwdArgs& a, int n_lif, int np, int grid, size_t lds,
+                                        hipStream_t s);
+hipError_t backward_cluster_occupancy(int n_lif, int np, size_t lds, int* blocks_per_cu);
+hipError_t launch_clear_abort(DevStatus* st, hipStream_t s);

@@ -91,7 +91,7 @@ GOOD = [(3, 0, 0), (4, 1, 1), (2, 2, 0)]
     (GOOD, {"batch": 0}),
     (GOOD, {"T": 0}),
     (GOOD, {"loss": 7}),
-    (GOOD, {"flags": 8}),
+    (GOOD, {"flags": 16}),
     (GOOD, {"record_capacity": -1}),
     (GOOD, {"T": 65537}),                                # past SNN_MAX_T
     ([(16385, 0, 0), (4, 1, 0), (2, 2, 0)], {}),         # past SNN_MAX_INPUT
