@@ -76,7 +76,7 @@ struct snn_net {
     // LIF-post projections of a LIF layer, the backward's staging offset,
     // the next exchange tag (odd) and the exchange words
     int cl_f, cl_b, cl_G, cl_spp_f, cl_spp_b, cl_np, cl_off_b;
-    int cl_threads_f;           // forward workgroup: the neuron wave and one wave per LIF -> LIF ring
+    int cl_threads;             // workgroup: the neuron wave and one wave per LIF -> LIF projection
     unsigned cl_tag;
     unsigned long long* clx;
     int grad_J, grad_TW, grad_KL, grad_threads, grad_SB, grad_bs, grad_nblk, grad_ngroups, grad_spcap;
@@ -408,7 +408,7 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
             if (lds <= kLds &&
                 forward_cluster_occupancy(t.n_lif, net->cl_np, threads, lds, &nb) == hipSuccess &&
                 nb > 0 && (long long)n_cu * nb >= G) {
-                net->cl_threads_f = threads;
+                net->cl_threads = threads;
                 net->cl_f = 1;
                 net->cl_spp_f = std::min<long long>((long long)n_cu * nb / G, t.B);
                 for (int p = 0; p < t.P; ++p) t.fring[p] = off[p];
@@ -454,17 +454,18 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
             for (int l = 0; l < n_layers; ++l)
                 if (net->bring_mode[l] >= 0) net->bring_mode[l] = -1;
         }
-        // cluster mode where the rings do not fit (or on request): partials
-        // [2][NL][KP][4] of the one wave, the exchange staging (slot list and
-        // fetched halves [NL KP][64][2]), then 64 columns of every adjoint ring
-        // (chosen on request only: with rings in device memory the backward
-        // core is faster still on the widest networks)
-        if (want_cl && coop && net->cl_np > 0 && force_cl) {
-            const int KPc = bwd_prefetch_cl(NL);
-            const size_t cpart = align16((size_t)2 * NL * KPc * 4 * sizeof(double));
-            const size_t stage =
-                align16((size_t)NL * KPc * sizeof(int) + (size_t)NL * KPc * (SNN_MAX_NEURONS / 64) * 2 * sizeof(unsigned));
-            size_t u = cpart + stage;
+        // cluster mode where the rings do not fit (or on request): the
+        // exchange staging (shares [NL NP][KC][4], slot totals [NL KC],
+        // own positions [NL][64], a flag), then 64 columns of every adjoint ring
+        if (want_cl && coop && net->cl_np > 0 && (force_cl || !all_lds)) {
+            const size_t stage = align16((size_t)NL * net->cl_np * kClKC * 4 * sizeof(double) +
+                                         (size_t)NL * kClKC * sizeof(double) + (size_t)NL * 64 * sizeof(int) +
+                                         sizeof(int));
+            int rings = 0;
+            for (int p = 0; p < t.P; ++p)
+                if (t.pre[p] != 0 && t.kind[t.post[p]] == SNN_LIF) ++rings;
+            const int threads = 64 * (1 + rings);
+            size_t u = stage;
             int mode[SNN_MAX_LAYERS];
             for (int l = 0; l < n_layers; ++l) {
                 mode[l] = -2;
@@ -473,11 +474,12 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
                 u += align16((size_t)t.Sb[l] * 64 * sizeof(double));
             }
             int nb = 0;
-            if (u <= kLds && backward_cluster_occupancy(NL, net->cl_np, u, &nb) == hipSuccess && nb > 0 &&
-                (long long)n_cu * nb >= net->cl_G) {
+            if (u <= kLds && backward_cluster_occupancy(NL, net->cl_np, threads, u, &nb) == hipSuccess &&
+                nb > 0 && (long long)n_cu * nb >= net->cl_G) {
                 net->cl_b = 1;
+                net->cl_threads = threads;
                 net->cl_spp_b = std::min<long long>((long long)n_cu * nb / net->cl_G, t.B);
-                net->cl_off_b = (int)cpart;
+                net->cl_off_b = 0;
                 for (int l = 0; l < n_layers; ++l) net->bring_mode[l] = mode[l];
                 used = u;
             }
@@ -644,7 +646,7 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     if (net->cl_f || net->cl_b) {
         // exchange words of every cluster slot, two parities (zero: no tag)
         const size_t fw = net->cl_f ? (size_t)net->cl_spp_f * 2 * nl * net->cl_G : 0;
-        const size_t bw = net->cl_b ? (size_t)net->cl_spp_b * net->cl_G * 2 * nl * bwd_prefetch_cl((int)nl) : 0;
+        const size_t bw = net->cl_b ? (size_t)net->cl_spp_b * net->cl_G * 2 * nl * kClKC : 0;
         const size_t words = 2 * std::max(fw, bw);
         ALLOC(net->clx, words);
         if (e == hipSuccess) e = hipMemset(net->clx, 0, words * sizeof(unsigned long long));
@@ -736,7 +738,7 @@ static hipError_t launch_forward_clusters(snn_net* net, CoreFwdArgs& a, hipStrea
         a.cl.tag0 = net->cl_tag;
         net->cl_tag += 2u * (unsigned)t.T;
         const hipError_t e = launch_forward_core_cluster(a, t.n_lif, net->cl_np, nc * net->cl_G,
-                                                         net->cl_threads_f, net->lds_core_f, s);
+                                                         net->cl_threads, net->lds_core_f, s);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -744,7 +746,6 @@ static hipError_t launch_forward_clusters(snn_net* net, CoreFwdArgs& a, hipStrea
 
 static hipError_t launch_backward_clusters(snn_net* net, CoreBwdArgs& a, hipStream_t s) {
     const Topo& t = net->t;
-    const int KPc = bwd_prefetch_cl(t.n_lif);
     a.NW = 1;
     a.cl.G = net->cl_G;
     a.cl.x = net->clx;
@@ -754,8 +755,9 @@ static hipError_t launch_backward_clusters(snn_net* net, CoreBwdArgs& a, hipStre
         const int nc = std::min(net->cl_spp_b, t.B - b0);
         a.cl.b0 = b0;
         a.cl.tag0 = net->cl_tag;
-        net->cl_tag += 2u * ((unsigned)t.T * (unsigned)((t.maxn + KPc - 1) / KPc) + 1u);
-        e = launch_backward_core_cluster(a, t.n_lif, net->cl_np, nc * net->cl_G, net->lds_core_b, s);
+        net->cl_tag += 2u * ((unsigned)t.T * (unsigned)((t.maxn + kClKC - 1) / kClKC) + 1u);
+        e = launch_backward_core_cluster(a, t.n_lif, net->cl_np, nc * net->cl_G, net->cl_threads,
+                                         net->lds_core_b, s);
     }
     return e;
 }

@@ -130,11 +130,9 @@ struct BwdState {
     double A2[NL];
 };
 
-template <int MAXT, int NL, int KP, int NP, bool RL, bool CL>
+template <int MAXT, int NL, int KP, int NP, bool RL>
 struct BwdCore {
-    static_assert(!CL || (MAXT == 64 && RL && NP > 0), "cluster mode: one wave, LDS rings");
     static constexpr int NPA = NP > 0 ? NP : 1;
-    static constexpr int GM = SNN_MAX_NEURONS / 64;    // most workgroups of a cluster
     static constexpr int ROW4 = (2 + KP + 3) / 4;      // int4 loads of a spike-table row
     typedef BwdState<NL, KP, NPA> State;
 
@@ -168,7 +166,7 @@ struct BwdCore {
     // (valid for q < cnt; record index of ids[0] is ri + r0).  Only the
     // chunks of 4 that hold spikes are loaded; ids are made uniform so that
     // a row's address is scalar and the lane adds its column.
-    static __device__ __forceinline__ void load_step(const CoreBwdArgs& a, int b, int j, int l,
+    static __device__ __forceinline__ void load_step(const CoreBwdArgs& a, int b, int tid, int l,
                                                      int ri, int cnt, const int (&ids)[KP], int r0,
                                                      uint2 (&ws)[NPA][KP], int& mine, float& I,
                                                      double& A2) {
@@ -192,7 +190,7 @@ struct BwdCore {
                 // than y.n) read as zero; such entries are masked anyway
                 const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
                     (void*)y.ws[pp], (short)0, y.npre[pp] * nq * 8, 0x00020000);
-                const int col8 = min(j, nq - 1) * 8;
+                const int col8 = min(tid, nq - 1) * 8;
 #pragma unroll
                 for (int q = q0; q < q0 + 4; ++q) {
                     // (unsigned: a stale entry's offset wraps instead of overflowing)
@@ -203,7 +201,7 @@ struct BwdCore {
             }
 #pragma unroll
             for (int q = q0; q < q0 + 4; ++q)
-                if (q < cnt && idc[q] == j) mine = q + 1;
+                if (q < cnt && idc[q] == tid) mine = q + 1;
         }
         if (mine) {
             const size_t r = (size_t)b * a.cap + (ri + r0 + mine - 1);
@@ -213,7 +211,7 @@ struct BwdCore {
     }
 
     // Issue the loads of B from A (processing step n).
-    static __device__ __forceinline__ void advance(const CoreBwdArgs& a, int b, int j, int n,
+    static __device__ __forceinline__ void advance(const CoreBwdArgs& a, int b, int tid, int n,
                                                    const State& A, State& B) {
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
@@ -222,7 +220,7 @@ struct BwdCore {
             B.ri3[l] = __builtin_amdgcn_readfirstlane(A.ri2[l]);
 #pragma unroll
             for (int q = 0; q < KP; ++q) B.id3[l][q] = A.id2[l][q];
-            load_step(a, b, j, l, B.ri3[l], B.cnt3[l], A.id2[l], 0, B.ws[l], B.mine[l], B.I[l],
+            load_step(a, b, tid, l, B.ri3[l], B.cnt3[l], A.id2[l], 0, B.ws[l], B.mine[l], B.I[l],
                       B.A2[l]);
         }
     }
@@ -230,7 +228,7 @@ struct BwdCore {
     // Delayed postsynaptic sums of spikes ids[q0 .. q0 + 4) (valid for q < cnt)
     // of layer l, reduced per 16-lane row into part_l[q][wave * 4 + row].
     // n_mod[pp]: n modulo the adjoint-ring slots of projection pp's post layer.
-    static __device__ __forceinline__ void gather4(const CoreBwdArgs& a, int b, int tid, int j, int n,
+    static __device__ __forceinline__ void gather4(const CoreBwdArgs& a, int b, int tid, int n,
                                                    const int (&n_mod)[NPA], int l, int q0, int cnt,
                                                    const int (&ids)[KP], const uint2 (&ws)[NPA][KP],
                                                    double* part_l) {
@@ -259,13 +257,11 @@ struct BwdCore {
                 const int lim = (pp < y.npost && q < cnt) ? a.T - n : 0;
                 const unsigned ru = (unsigned)(n_mod[pp] + sq);
                 const int row = (int)min(ru, ru - (unsigned)S);
-                ok[k][pp] = sq < lim && j < nq;
+                ok[k][pp] = sq < lim && tid < nq;
                 // (in LDS the row is always in the ring and the column is
-                // clamped into it, so the read needs no mask; its value does;
-                // a cluster's rings hold its 64 columns)
+                // clamped into it, so the read needs no mask; its value does)
                 if (RL)
-                    d[k][pp] = ((lds_f64*)(smem + y.qring_lds[pp]))[CL ? row * 64 + tid
-                                                                       : row * nq + min(tid, nq - 1)];
+                    d[k][pp] = ((lds_f64*)(smem + y.qring_lds[pp]))[row * nq + min(tid, nq - 1)];
                 else   // (masked reads share one line of device memory)
                     d[k][pp] = ((global_f64*)(y.qring[pp] +
                                               ((size_t)b * S + (ok[k][pp] ? row : 0)) * nq))[ok[k][pp] ? tid : 0];
@@ -294,13 +290,13 @@ struct BwdCore {
         if (k < 4) part_l[(size_t)(q0 + 2 * (k & 1) + (k >> 1)) * (4 * a.NW) + wave * 4 + (lane >> 4)] = x;
     }
 
-    static __device__ __forceinline__ void gather(const CoreBwdArgs& a, int b, int tid, int j, int n,
+    static __device__ __forceinline__ void gather(const CoreBwdArgs& a, int b, int tid, int n,
                                                   const int (&n_mod)[NPA], int l, int cnt,
                                                   const int (&ids)[KP], const uint2 (&ws)[NPA][KP],
                                                   double* part_l) {
 #pragma unroll
         for (int q0 = 0; q0 < KP; q0 += 4)
-            if (cnt > q0) gather4(a, b, tid, j, n, n_mod, l, q0, cnt, ids, ws, part_l);
+            if (cnt > q0) gather4(a, b, tid, n, n_mod, l, q0, cnt, ids, ws, part_l);
     }
 
     // The lambda_V jump of this lane's spike at position q of a round.
@@ -325,14 +321,7 @@ struct BwdCore {
             }
             A += Ap;
         }
-        jump_apply(a, A, I, lv, deg);
-    }
-
-    // lambda_V of a spike with jump numerator A (the extra terms and the
-    // delayed postsynaptic sums): tau_m dV/dt just before the crossing is
-    // I- - theta (V- = theta).
-    static __device__ __forceinline__ void jump_apply(const CoreBwdArgs& a, double A, float I, double& lv,
-                                                      unsigned long long& deg) {
+        // tau_m dV/dt just before the crossing is I- - theta (V- = theta)
         const double den = __dsub_rn((double)I, a.theta);
         if (den > 0.0) {
             lv = __dadd_rn(lv, __dadd_rn(__dmul_rn(a.theta, lv), A) / den);
@@ -341,147 +330,15 @@ struct BwdCore {
         }
     }
 
-    // Cluster mode, one exchange round (slot l KP + q: spike q of the round in
-    // layer l, partials part_r[slot][4]).  This workgroup's share of every
-    // slot's jump sum, its four row partials added in order, goes out as two
-    // tagged 32-bit halves (word 2 slot + h of its block, blocks G apart in
-    // workgroup order).  The slots of spikes owned here (mine[l] > 0) are
-    // listed in LDS; lanes fetch the G shares of each, one word per request
-    // (request (s G + g') 2 + h: half h of workgroup g's share of listed slot
-    // s), and each owner adds its slot's shares in workgroup order into
-    // sum[l].  Lanes below G also read one word of every block: no workgroup
-    // publishes round r + 2 (which reuses this parity's buffer) before all
-    // have read round r.  false: the wait gave up.
-    static __device__ __forceinline__ bool exchange(const CoreBwdArgs& a, int c, int g, int rnd,
-                                                    const double* part_r, const int (&mine)[NL],
-                                                    double (&sum)[NL]) {
-        constexpr int NS = NL * KP, NWD = 2 * NS;     // slots, words per block
-        constexpr int RM = 4;                          // requests per lane and pass
-        const int lane = threadIdx.x & 63, G = a.cl.G;
-        const unsigned tag = a.cl.tag0 + 2u * (unsigned)rnd;
-        unsigned long long* X = a.cl.x + ((size_t)c * 2 + (rnd & 1)) * (size_t)G * NWD;
-#pragma unroll
-        for (int k0 = 0; k0 < NWD; k0 += 64) {
-            const int k = k0 + lane;
-            if (k < NWD) {
-                const double* pq = part_r + (size_t)(k >> 1) * 4;
-                const double v = ((pq[0] + pq[1]) + pq[2]) + pq[3];
-                const unsigned long long u = (unsigned long long)__double_as_longlong(v);
-                cl_put(X + (size_t)g * NWD + k, tag, (k & 1) ? (unsigned)(u >> 32) : (unsigned)u);
-            }
-        }
-        // own slots, compacted in layer then lane order
-        int* list = reinterpret_cast<int*>(smem + a.cl_off);                 // [NS]
-        unsigned* buf = reinterpret_cast<unsigned*>(smem + a.cl_off) + NS;   // [NS][GM][2]
-        int m = 0, pos[NL];
-#pragma unroll
-        for (int l = 0; l < NL; ++l) {
-            const bool own = mine[l] > 0;
-            const unsigned long long bm = __ballot(own);
-            pos[l] = m + lanes_below(bm);
-            if (own) list[pos[l]] = l * KP + mine[l] - 1;
-            m += __popcll(bm);
-        }
-        __syncthreads();
-        const int nreq = 2 * G * m;
-        for (int r0 = 0; r0 == 0 || r0 < nreq; r0 += 64 * RM) {
-            int adr[RM];
-            bool need[RM];
-#pragma unroll
-            for (int u = 0; u < RM; ++u) {
-                const int r = r0 + u * 64 + lane;
-                need[u] = r < nreq;
-                const int rr = need[u] ? r : 0;
-                const int sl = (m > 0) ? list[rr / (2 * G)] : 0;
-                const int gp = (rr % (2 * G)) >> 1;
-                adr[u] = gp * NWD + 2 * sl + (rr & 1);
-            }
-            bool hdr = r0 == 0 && lane < G;
-            unsigned pay[RM];
-            for (int spin = 0;; ++spin) {
-                unsigned long long w[RM], hw = 0;
-#pragma unroll
-                for (int u = 0; u < RM; ++u)
-                    if (need[u]) w[u] = __hip_atomic_load(X + adr[u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                if (hdr) hw = __hip_atomic_load(X + (size_t)lane * NWD, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                bool pending = false;
-#pragma unroll
-                for (int u = 0; u < RM; ++u) {
-                    if (need[u] && (unsigned)(w[u] >> 32) == tag) {
-                        pay[u] = (unsigned)w[u];
-                        need[u] = false;
-                        buf[r0 + u * 64 + lane] = pay[u];
-                    }
-                    pending |= need[u];
-                }
-                if (hdr && (unsigned)(hw >> 32) == tag) hdr = false;
-                pending |= hdr;
-                if (__ballot(pending) == 0) break;
-                if ((spin & 255) == 255) {
-                    if (__hip_atomic_load(&a.st->cl_abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return false;
-                    if (spin >= kClusterSpins) {
-                        __hip_atomic_store(&a.st->cl_abort, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        return false;
-                    }
-                }
-                __builtin_amdgcn_s_sleep(1);
-            }
-        }
-        __syncthreads();
-#pragma unroll
-        for (int l = 0; l < NL; ++l) {
-            sum[l] = 0.0;
-            if (!mine[l]) continue;
-            const unsigned* bs = buf + (size_t)pos[l] * 2 * G;
-            double acc = 0.0;
-            for (int gp = 0; gp < G; ++gp) {
-                const unsigned long long u =
-                    ((unsigned long long)bs[2 * gp + 1] << 32) | (unsigned long long)bs[2 * gp];
-                acc += __longlong_as_double((long long)u);
-            }
-            sum[l] = acc;
-        }
-        return true;
-    }
-
     struct Lane {
         double lv[NL], lI[NL];
         unsigned long long deg;
         int rnd;
-        int xr;                        // cluster exchanges so far
     };
 
-    // The jumps of a round: this lane's spikes (position mine[l] - 1 among
-    // the round's spikes of layer l) with the round's partials part_r.
-    // Cluster mode exchanges the partials first (rounds without spikes do
-    // not exchange; every workgroup of a cluster sees the same rounds).
-    // false: the exchange gave up.
-    static __device__ __forceinline__ bool jumps(const CoreBwdArgs& a, int c, int g, const double* part_r,
-                                                 bool any, const int (&mine)[NL], const float (&I)[NL],
-                                                 const double (&A2)[NL], Lane& L) {
-        if constexpr (CL) {
-            if (!any) return true;
-            double sm[NL];
-            if (!exchange(a, c, g, L.xr++, part_r, mine, sm)) return false;
-#pragma unroll
-            for (int l = 0; l < NL; ++l)
-                if (mine[l]) jump_apply(a, A2[l] + sm[l], I[l], L.lv[l], L.deg);
-        } else {
-#pragma unroll
-            for (int l = 0; l < NL; ++l) {
-                if (!mine[l]) continue;
-                const double* part_l = part_r + (size_t)l * KP * (4 * a.NW);
-                jump(a, part_l, mine[l] - 1, I[l], A2[l], L.lv[l], L.deg);
-            }
-        }
-        return true;
-    }
-
-    // One reverse-time step n with the loads of A, issuing those of B.  c, g:
-    // cluster and rank of the workgroup (cluster mode; else 0); j: the
-    // lane's neuron.  false: a cluster exchange gave up.
-    static __device__ __forceinline__ bool step(const CoreBwdArgs& a, int b, int c, int g, int tid,
-                                                int j, int n, const State& A, State& B, Lane& L) {
+    // One reverse-time step n with the loads of A, issuing those of B.
+    static __device__ __forceinline__ void step(const CoreBwdArgs& a, int b, int tid, int n,
+                                                const State& A, State& B, Lane& L) {
         const int T = a.T, LT = a.lif_total;
         double* part = reinterpret_cast<double*>(smem + a.part_off);   // [2][NL][KP][4 NW]
         // n modulo the adjoint-ring slots of each post layer read by layer l
@@ -494,24 +351,24 @@ struct BwdCore {
         // the loads issued one step ago (A) have landed: wait for them once,
         // here, so that no later use waits for this step's loads
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
-        advance(a, b, j, n, A, B);
+        advance(a, b, tid, n, A, B);
 
         // ---- adjoint free dynamics, trajectory, adjoint ring
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
             const BwdLayer& y = a.ly[l];
-            if (j >= y.n) continue;
+            if (tid >= y.n) continue;
             if (n <= T - 2) {
                 const double v = L.lv[l];
                 L.lI[l] = __dadd_rn(__dmul_rn(a.beta, L.lI[l]), __dmul_rn(a.cc, v));
                 L.lv[l] = __dmul_rn(a.alpha, v);
             }
             const double d = __dsub_rn(L.lI[l], L.lv[l]);
-            a.traj[((size_t)b * T + n) * LT + y.lif_off + j] = make_double2(L.lI[l], d);
+            a.traj[((size_t)b * T + n) * LT + y.lif_off + tid] = make_double2(L.lI[l], d);
             if (y.ring_lds == -2) continue;
             const int n_own = n % y.S;
             if (RL)
-                ((lds_f64*)(smem + y.ring_lds))[n_own * (CL ? 64 : y.n) + tid] = d;
+                ((lds_f64*)(smem + y.ring_lds))[n_own * y.n + tid] = d;
             else
                 ((global_f64*)(y.ring + ((size_t)b * y.S + n_own) * y.n))[tid] = d;
         }
@@ -520,18 +377,20 @@ struct BwdCore {
         {
             const int pb = L.rnd & 1;
             ++L.rnd;
-            bool any = false;
             if (NP > 0) {
 #pragma unroll
                 for (int l = 0; l < NL; ++l) {
                     double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
-                    gather(a, b, tid, j, n, nm[l], l, A.cnt3[l], A.id3[l], A.ws[l], part_l);
-                    any |= A.cnt3[l] > 0;
+                    gather(a, b, tid, n, nm[l], l, A.cnt3[l], A.id3[l], A.ws[l], part_l);
                 }
             }
             __syncthreads();
-            if (!jumps(a, c, g, part + (size_t)pb * NL * KP * (4 * a.NW), any, A.mine, A.I, A.A2, L))
-                return false;
+#pragma unroll
+            for (int l = 0; l < NL; ++l) {
+                if (!A.mine[l]) continue;
+                const double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
+                jump(a, part_l, A.mine[l] - 1, A.I[l], A.A2[l], L.lv[l], L.deg);
+            }
         }
         // ---- further rounds when a step has more than KP spikes
         int rounds = 1;
@@ -553,25 +412,22 @@ struct BwdCore {
                 for (int q = 0; q < KP; ++q)
                     ids[q] = y.recn[(size_t)b * a.cap + min(max(A.ri3[l] + r * KP + q, 0), capm)];
                 uint2 ws[NPA][KP];
-                load_step(a, b, j, l, A.ri3[l], cnt, ids, r * KP, ws, mine[l], I[l], A2[l]);
+                load_step(a, b, tid, l, A.ri3[l], cnt, ids, r * KP, ws, mine[l], I[l], A2[l]);
                 double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
-                if (NP > 0) gather(a, b, tid, j, n, nm[l], l, cnt, ids, ws, part_l);
+                if (NP > 0) gather(a, b, tid, n, nm[l], l, cnt, ids, ws, part_l);
             }
             __syncthreads();
-            if (!jumps(a, c, g, part + (size_t)pb * NL * KP * (4 * a.NW), true, mine, I, A2, L))
-                return false;
+#pragma unroll
+            for (int l = 0; l < NL; ++l) {
+                if (!mine[l]) continue;
+                const double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
+                jump(a, part_l, mine[l] - 1, I[l], A2[l], L.lv[l], L.deg);
+            }
         }
-        return true;
     }
 
     static __device__ void run(const CoreBwdArgs& a) {
-        if (CL && a.st->cl_abort) return;
-        const int tid = threadIdx.x;
-        // cluster mode: workgroup g of cluster c serves sample b0 + c
-        int c = 0, g = 0;
-        if (CL) cluster_rank((int)blockIdx.x, a.cl.G, c, g);
-        const int b = CL ? a.cl.b0 + c : (int)blockIdx.x;
-        const int j = CL ? g * 64 + tid : tid;
+        const int b = blockIdx.x, tid = threadIdx.x;
         const int T = a.T;
         Lane L;
 #pragma unroll
@@ -581,7 +437,6 @@ struct BwdCore {
         }
         L.deg = 0;
         L.rnd = 0;
-        L.xr = 0;
         State A, B;
         // step T - 1's data and step T - 2's table row, before the loop
 #pragma unroll
@@ -590,24 +445,478 @@ struct BwdCore {
             load_row(a.ly[l], b, T, max(T - 2, 0), A.cnt2[l], A.ri2[l], A.id2[l]);
             A.cnt3[l] = __builtin_amdgcn_readfirstlane(A.cnt3[l]);
             A.ri3[l] = __builtin_amdgcn_readfirstlane(A.ri3[l]);
-            load_step(a, b, j, l, A.ri3[l], A.cnt3[l], A.id3[l], 0, A.ws[l], A.mine[l], A.I[l],
+            load_step(a, b, tid, l, A.ri3[l], A.cnt3[l], A.id3[l], 0, A.ws[l], A.mine[l], A.I[l],
                       A.A2[l]);
         }
         int n = T - 1;
         for (; n >= 1; n -= 2) {
-            if (!step(a, b, c, g, tid, j, n, A, B, L)) return;
-            if (!step(a, b, c, g, tid, j, n - 1, B, A, L)) return;
+            step(a, b, tid, n, A, B, L);
+            step(a, b, tid, n - 1, B, A, L);
         }
-        if (n == 0 && !step(a, b, c, g, tid, j, 0, A, B, L)) return;
+        if (n == 0) step(a, b, tid, 0, A, B, L);
         if (L.deg) atomicAdd(&a.st->degenerate, L.deg);
     }
 };
 
-// RL: every adjoint ring lives in LDS (else every one in HBM).  CL: cluster
-// mode (one wave per workgroup, LDS rings).
-template <int MAXT, int NL, int KP, int NP, bool RL, bool CL = false>
+// RL: every adjoint ring lives in LDS (else every one in HBM).
+template <int MAXT, int NL, int KP, int NP, bool RL>
 __global__ void __launch_bounds__(MAXT) backward_core_kernel(CoreBwdArgs a) {
-    BwdCore<MAXT, NL, KP, NP, RL, CL>::run(a);
+    BwdCore<MAXT, NL, KP, NP, RL>::run(a);
+}
+
+// ------------------------------------------------------------------ backward core, cluster mode
+
+// Cluster mode (the LIF layers' adjoint rings exceed one workgroup's LDS): G
+// workgroups per sample, workgroup g holding the adjoint-ring columns of its
+// neurons [64 g, 64 g + 64) of every LIF layer.  Wave 0, the neuron wave,
+// runs lambda of those neurons (free dynamics, trajectories, ring rows, the
+// exchange, the jumps); wave 1 + r, one per LIF -> LIF projection r (source
+// layers in order, then projection order), the delayed postsynaptic sums of
+// the step's spikes of its source layer over the workgroup's 64 posts.  The
+// spike data of every wave is prefetched three steps deep (count and first
+// record, then the ids, then a gather wave's weights and slots), so a step
+// waits for memory once.  The spikes of a step go in rounds of at most KC
+// per layer (steps without spikes have none); per round two barriers (the
+// ring rows are written or the previous round's shares read; the shares are
+// written) and one exchange of the shares between the workgroups: slot k
+// (the round's spikes of every layer, in layer order) goes out as two
+// tagged halves of word pair k of the workgroup's block, and lane k adds the
+// G shares of slot k in workgroup order, which also keeps any workgroup from
+// publishing twice into a buffer the others still read.
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
+constexpr int kSc1 = 16;        // buffer access cache policy: agent scope (sc1)
+
+template <int NL, int NP>
+struct BwdCluster {
+    static_assert(NP > 0, "cluster mode serves layers with LIF -> LIF projections");
+    static constexpr int KC = kClKC;
+    static constexpr int NS = NL * KC;            // exchange slots of a round
+    static constexpr int NWD = 2 * NS;            // words of a workgroup's block
+
+    // The staging in LDS at cl_off: shares [NL NP][KC][4] (fp64), slot
+    // totals [NS] (fp64), own positions [NL][64] (int), the abort flag.
+    static __device__ __forceinline__ double* shares(const CoreBwdArgs& a) {
+        return reinterpret_cast<double*>(smem + a.cl_off);
+    }
+    static __device__ __forceinline__ double* totals(const CoreBwdArgs& a) {
+        return shares(a) + NL * NP * KC * 4;
+    }
+    static __device__ __forceinline__ int* positions(const CoreBwdArgs& a) {
+        return reinterpret_cast<int*>(totals(a) + NS);
+    }
+    static __device__ __forceinline__ int* flag(const CoreBwdArgs& a) { return positions(a) + NL * 64; }
+
+    // Barrier over LDS only (device-memory accesses may stay in flight).
+    static __device__ __forceinline__ void lds_barrier() {
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0xC07F);       // lgkmcnt(0); vmcnt, expcnt at their maximum
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    }
+
+    // Spike count and first record index of layer l at step x (a per-lane
+    // zero in the address keeps the compiler from making the load scalar and
+    // waiting for it where it lands).
+    static __device__ __forceinline__ int2 load_cr(const CoreBwdArgs& a, int b, int l, int x) {
+        int zero;
+        asm volatile("v_mov_b32 %0, 0" : "=v"(zero));
+        return reinterpret_cast<const int2*>(a.ly[l].steptab + ((size_t)b * a.T + x) * SNN_STEP_ROW)[zero];
+    }
+
+    // Lane q: the neuron of spike q0 + q of a step with records [ri, ri +
+    // cnt) (clamped into them; -1 for a step without spikes).
+    static __device__ __forceinline__ int load_id(const CoreBwdArgs& a, int b, int l, int ri, int cnt, int q0) {
+        const int q = min(q0 + (int)(threadIdx.x & 63), max(cnt - 1, 0));
+        const int idx = min(max(ri + q, 0), max(a.cap - 1, 0));
+        return (cnt > 0 && a.cap > 0) ? a.ly[l].recn[(size_t)b * a.cap + idx] : -1;
+    }
+
+    // Weights and slots of spikes q < KC (ids in lanes q of `ids`) for post
+    // j of projection pp of layer l (rows clamped into the matrix).
+    static __device__ __forceinline__ void load_ws(const CoreBwdArgs& a, int l, int pp, int j, int ids,
+                                                   uint2 (&w)[KC]) {
+        const BwdLayer& y = a.ly[l];
+        const int nq = y.nq[pp], rmax = y.npre[pp] - 1;
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)y.ws[pp], (short)0, y.npre[pp] * nq * 8, 0x00020000);
+        const int col8 = min(j, nq - 1) * 8;
+#pragma unroll
+        for (int q = 0; q < KC; ++q) {
+            const int r = min(max(__builtin_amdgcn_readlane(ids, q), 0), rmax);
+            const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, col8, r * nq * 8, 0);
+            w[q] = make_uint2((unsigned)v[0], (unsigned)v[1]);
+        }
+    }
+
+    // Rounds of a step: the most ceil(count / KC) over the layers.
+    static __device__ __forceinline__ int rounds_of(const int (&cnt)[NL]) {
+        int r = 0;
+#pragma unroll
+        for (int l = 0; l < NL; ++l) r = max(r, (cnt[l] + KC - 1) / KC);
+        return r;
+    }
+
+    // ---- a gather wave: projection pp of layer l (post layer: its adjoint
+    // ring qring, S rows, 64 columns)
+
+    // Prefetch state entering step n: every layer's spike count and first
+    // record at n (uniform), loaded ones at n - 1 and n - 2, the ids of
+    // layer l at n - 1 (loaded; lane q: spike q).
+    struct GState {
+        int cn[NL], rn[NL];
+        int2 c1[NL], c2[NL];
+        int i1;
+    };
+
+    // Step n with this step's weights wc (landed); issues step n - 1's into
+    // wn.  false: the cluster gave up (the flag was raised).
+    static __device__ __forceinline__ bool gstep(const CoreBwdArgs& a, int b, int g, int r, int l, int pp,
+                                                 int n, GState& st, uint2 (&wc)[KC], uint2 (&wn)[KC]) {
+        const int lane = threadIdx.x & 63, j = g * 64 + lane, T = a.T;
+        const BwdLayer& y = a.ly[l];
+        const int nq = y.nq[pp], S = y.qS[pp];
+        const bool live = j < nq;
+        lds_f64* ring = (lds_f64*)(smem + y.qring_lds[pp]) + lane;
+        double* sh = shares(a) + (size_t)r * KC * 4;
+        int cnt = 0, ri = 0;
+#pragma unroll
+        for (int m = 0; m < NL; ++m)
+            if (m == l) {
+                cnt = st.cn[m];
+                ri = st.rn[m];
+            }
+        const int rounds = rounds_of(st.cn);
+        const int n_mod = n % S;
+        for (int rd = 0; rd < rounds; ++rd) {
+            lds_barrier();                                       // ring rows in, shares free
+            if (*flag(a)) return false;
+            const int q0 = rd * KC, nr = min(max(cnt - q0, 0), KC);
+            if (rd > 0 && nr > 0) {
+                // spikes past the prefetched ones: ids, then weights, now
+                const int idr = load_id(a, b, l, ri, cnt, q0);
+                load_ws(a, l, pp, j, idr, wc);
+            }
+            // (unrolled over the KC slots, so that the weights stay in
+            // registers; chunks past the round's spikes are skipped)
+#pragma unroll
+            for (int k0 = 0; k0 < KC; k0 += 4) {
+                if (k0 >= nr) break;
+                double d[4], v[4];
+                bool ok[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int sq = (int)wc[k0 + k].y;
+                    const int lim = (k0 + k < nr) ? T - n : 0;
+                    const unsigned ru = (unsigned)(n_mod + sq);
+                    const int row = (int)min(ru, ru - (unsigned)S);
+                    ok[k] = sq < lim && live;
+                    d[k] = ring[row * 64];
+                }
+                asm volatile("" : "+v"(d[0]), "+v"(d[1]), "+v"(d[2]), "+v"(d[3]));
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    // a masked term is +0 (0 - 0 = +0)
+                    const double t = __dmul_rn((double)__uint_as_float(wc[k0 + k].x), d[k]);
+                    v[k] = __dsub_rn(0.0, ok[k] ? t : 0.0);
+                }
+                const double x = row_sum4(v, lane);
+                const int k = lane & 15;
+                if (k < 4) sh[(size_t)(k0 + 2 * (k & 1) + (k >> 1)) * 4 + (lane >> 4)] = x;
+            }
+            lds_barrier();                                       // shares written
+        }
+        // the next loads, issued while the neuron wave exchanges: counts three
+        // steps ahead, ids two, weights one
+        int2 c3[NL];
+#pragma unroll
+        for (int m = 0; m < NL; ++m) c3[m] = load_cr(a, b, m, max(n - 3, 0));
+        int i2 = 0;
+#pragma unroll
+        for (int m = 0; m < NL; ++m)
+            if (m == l)
+                i2 = load_id(a, b, l, __builtin_amdgcn_readfirstlane(st.c2[m].y),
+                             __builtin_amdgcn_readfirstlane(st.c2[m].x), 0);
+        if (n > 0) load_ws(a, l, pp, j, st.i1, wn);
+#pragma unroll
+        for (int m = 0; m < NL; ++m) {
+            st.cn[m] = __builtin_amdgcn_readfirstlane(st.c1[m].x);
+            st.rn[m] = __builtin_amdgcn_readfirstlane(st.c1[m].y);
+            st.c1[m] = st.c2[m];
+            st.c2[m] = c3[m];
+        }
+        st.i1 = i2;
+        return true;
+    }
+
+    static __device__ void gather_wave(const CoreBwdArgs& a, int b, int g, int r, int l, int pp) {
+        const int j = g * 64 + (int)(threadIdx.x & 63), T = a.T;
+        GState st;
+        int2 c0[NL];
+#pragma unroll
+        for (int m = 0; m < NL; ++m) {
+            c0[m] = load_cr(a, b, m, T - 1);
+            st.c1[m] = load_cr(a, b, m, max(T - 2, 0));
+            st.c2[m] = load_cr(a, b, m, max(T - 3, 0));
+        }
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        int i0 = 0;
+#pragma unroll
+        for (int m = 0; m < NL; ++m) {
+            st.cn[m] = __builtin_amdgcn_readfirstlane(c0[m].x);
+            st.rn[m] = __builtin_amdgcn_readfirstlane(c0[m].y);
+            if (m == l) {
+                i0 = load_id(a, b, l, st.rn[m], st.cn[m], 0);
+                st.i1 = load_id(a, b, l, __builtin_amdgcn_readfirstlane(st.c1[m].y),
+                                __builtin_amdgcn_readfirstlane(st.c1[m].x), 0);
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        uint2 wa[KC], wb[KC];
+        load_ws(a, l, pp, j, i0, wa);
+        int n = T - 1;
+        for (; n >= 1; n -= 2) {
+            if (!gstep(a, b, g, r, l, pp, n, st, wa, wb)) return;
+            if (!gstep(a, b, g, r, l, pp, n - 1, st, wb, wa)) return;
+        }
+        if (n == 0) gstep(a, b, g, r, l, pp, 0, st, wa, wb);
+    }
+
+    // ---- the neuron wave
+
+    // Exchange of one round: K slots (uniform).  false: the wait gave up.
+    static __device__ __forceinline__ bool exchange(const CoreBwdArgs& a, int c, int g, int rnd, int K,
+                                                    const int (&off)[NL], const int (&nr)[NL],
+                                                    const int (&rof)[NL], const int (&nring)[NL]) {
+        const int lane = threadIdx.x & 63, G = a.cl.G;
+        const unsigned tag = a.cl.tag0 + 2u * (unsigned)rnd;
+        unsigned long long* X = a.cl.x + ((size_t)c * 2 + (rnd & 1)) * (size_t)G * NWD;
+        const __amdgpu_buffer_rsrc_t rs =
+            __builtin_amdgcn_make_buffer_rsrc((void*)X, (short)0, G * NWD * 8, 0x00020000);
+        const double* sh = shares(a);
+        double* tot = totals(a);
+        for (int k0 = 0; k0 < K; k0 += 64) {
+            const int k = k0 + lane;
+            const bool mine = k < K;
+            // this workgroup's share of slot k: its projections' four row
+            // partials, each added in order, projections in order
+            if (mine) {
+                int l = 0;
+#pragma unroll
+                for (int m = 1; m < NL; ++m) l = (k >= off[m]) ? m : l;
+                int q = k, rr = 0, nrg = 0;
+#pragma unroll
+                for (int m = 0; m < NL; ++m)
+                    if (m == l) {
+                        q = k - off[m];
+                        rr = rof[m];
+                        nrg = nring[m];
+                    }
+                double v = 0.0;
+                for (int p = 0; p < nrg; ++p) {
+                    const double* pq = sh + ((size_t)(rr + p) * KC + q) * 4;
+                    v += ((pq[0] + pq[1]) + pq[2]) + pq[3];
+                }
+                // both tagged halves in one 16-byte agent-scope store
+                const unsigned long long u = (unsigned long long)__double_as_longlong(v);
+                const v4u wd = {(unsigned)u, tag, (unsigned)(u >> 32), tag};
+                __builtin_amdgcn_raw_buffer_store_b128(wd, rs, (g * NWD + 2 * k) * 8, 0, kSc1);
+            }
+            // every workgroup's share of slot k, added in workgroup order: one
+            // 16-byte load per workgroup (each 8-byte half single-copy atomic
+            // with its own tag; a torn pair is read again)
+            unsigned need = mine ? (unsigned)((1ull << G) - 1) : 0u;
+            unsigned lo[SNN_MAX_NEURONS / 64], hi[SNN_MAX_NEURONS / 64];
+            const int kk = 2 * min(k, K - 1);
+            for (int spin = 0;; ++spin) {
+                asm volatile("" ::: "memory");               // the loads are issued anew every poll
+                v4u wv[SNN_MAX_NEURONS / 64];
+#pragma unroll
+                for (int i = 0; i < SNN_MAX_NEURONS / 64; ++i)
+                    if ((need >> i) & 1u) wv[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (i * NWD + kk) * 8, 0, kSc1);
+#pragma unroll
+                for (int i = 0; i < SNN_MAX_NEURONS / 64; ++i)
+                    if (((need >> i) & 1u) && wv[i].y == tag && wv[i].w == tag) {
+                        lo[i] = wv[i].x;
+                        hi[i] = wv[i].z;
+                        need &= ~(1u << i);
+                    }
+                if (__ballot(need != 0) == 0) break;
+                if ((spin & 255) == 255) {
+                    if (__hip_atomic_load(&a.st->cl_abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return false;
+                    if (spin >= kClusterSpins) {
+                        __hip_atomic_store(&a.st->cl_abort, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        return false;
+                    }
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+            if (mine) {
+                double s = 0.0;
+#pragma unroll
+                for (int gp = 0; gp < SNN_MAX_NEURONS / 64; ++gp)
+                    if (gp < G)
+                        s += __longlong_as_double((long long)(((unsigned long long)hi[gp] << 32) | lo[gp]));
+                tot[k] = s;
+            }
+        }
+        return true;
+    }
+
+    static __device__ void neuron_wave(const CoreBwdArgs& a, int b, int c, int g) {
+        const int lane = threadIdx.x & 63, j = g * 64 + lane, T = a.T, LT = a.lif_total;
+        double lv[NL], lI[NL];
+        unsigned long long deg = 0;
+        int rnd = 0;
+        // gather waves of each layer: the first one's index and how many
+        int rof[NL], nring[NL];
+        {
+            int r = 0;
+#pragma unroll
+            for (int l = 0; l < NL; ++l) {
+                rof[l] = r;
+                nring[l] = a.ly[l].npost;
+                r += a.ly[l].npost;
+            }
+        }
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            lv[l] = 0.0;
+            lI[l] = 0.0;
+        }
+        int* pos = positions(a);
+        const double* tot = totals(a);
+        // pipeline: (count, first record) of steps n, n - 1; ids of n
+        int2 c0[NL], c1[NL];
+        int id0[NL];
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            c0[l] = load_cr(a, b, l, T - 1);
+            c1[l] = load_cr(a, b, l, max(T - 2, 0));
+        }
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        int cnt0[NL], ri0[NL];
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            cnt0[l] = __builtin_amdgcn_readfirstlane(c0[l].x);
+            ri0[l] = __builtin_amdgcn_readfirstlane(c0[l].y);
+            id0[l] = load_id(a, b, l, ri0[l], cnt0[l], 0);
+        }
+        for (int n = T - 1; n >= 0; --n) {
+            __builtin_amdgcn_s_waitcnt(kWaitVm0);
+            int cnt1[NL], ri1[NL], id1[NL];
+#pragma unroll
+            for (int l = 0; l < NL; ++l) {
+                cnt1[l] = __builtin_amdgcn_readfirstlane(c1[l].x);
+                ri1[l] = __builtin_amdgcn_readfirstlane(c1[l].y);
+                c1[l] = load_cr(a, b, l, max(n - 2, 0));
+                id1[l] = load_id(a, b, l, ri1[l], cnt1[l], 0);
+            }
+            // ---- adjoint free dynamics, trajectory, adjoint ring
+#pragma unroll
+            for (int l = 0; l < NL; ++l) {
+                const BwdLayer& y = a.ly[l];
+                if (j >= y.n) continue;
+                if (n <= T - 2) {
+                    const double v = lv[l];
+                    lI[l] = __dadd_rn(__dmul_rn(a.beta, lI[l]), __dmul_rn(a.cc, v));
+                    lv[l] = __dmul_rn(a.alpha, v);
+                }
+                const double d = __dsub_rn(lI[l], lv[l]);
+                a.traj[((size_t)b * T + n) * LT + y.lif_off + j] = make_double2(lI[l], d);
+                if (y.ring_lds >= 0) ((lds_f64*)(smem + y.ring_lds))[(n % y.S) * 64 + lane] = d;
+            }
+            const int rounds = rounds_of(cnt0);
+            for (int rd = 0; rd < rounds; ++rd) {
+                // this lane's spike among the round's of each layer (position
+                // + 1, 0: none), its I- and extra jump numerator
+                int mine[NL], off[NL], nr[NL];
+                float I[NL];
+                double A2[NL];
+                int K = 0;
+#pragma unroll
+                for (int l = 0; l < NL; ++l) {
+                    const int q0 = rd * KC;
+                    nr[l] = min(max(cnt0[l] - q0, 0), KC);
+                    off[l] = K;
+                    K += nr[l];
+                    const int id = (rd == 0) ? id0[l] : load_id(a, b, l, ri0[l], cnt0[l], q0);
+                    pos[l * 64 + lane] = 0;
+                    const int o = id - g * 64;
+                    if ((int)lane < nr[l] && o >= 0 && o < 64) pos[l * 64 + o] = lane + 1;
+                    // other lanes wrote this lane's entry: the read must
+                    // not be folded into this lane's own stores (the wave's
+                    // LDS accesses are in order)
+                    asm volatile("" ::: "memory");
+                    mine[l] = pos[l * 64 + lane];
+                    I[l] = 0.0f;
+                    A2[l] = 0.0;
+                    if (mine[l]) {
+                        const size_t rr = (size_t)b * a.cap + (ri0[l] + q0 + mine[l] - 1);
+                        I[l] = a.ly[l].recI[rr];
+                        A2[l] = a.ly[l].A2 ? a.ly[l].A2[rr] : 0.0;
+                    }
+                }
+                lds_barrier();                                   // ring rows in, shares free
+                lds_barrier();                                   // shares written
+                const bool ok = exchange(a, c, g, rnd++, K, off, nr, rof, nring);
+                asm volatile("" ::: "memory");                   // the slot totals of other lanes
+                if (!ok) {
+                    if (lane == 0) *flag(a) = 1;
+                    lds_barrier();                               // the gather waves see the flag
+                    return;
+                }
+#pragma unroll
+                for (int l = 0; l < NL; ++l) {
+                    if (!mine[l]) continue;
+                    const double A = A2[l] + tot[off[l] + mine[l] - 1];
+                    // tau_m dV/dt just before the crossing is I- - theta (V- = theta)
+                    const double den = __dsub_rn((double)I[l], a.theta);
+                    if (den > 0.0)
+                        lv[l] = __dadd_rn(lv[l], __dadd_rn(__dmul_rn(a.theta, lv[l]), A) / den);
+                    else
+                        ++deg;
+                }
+            }
+#pragma unroll
+            for (int l = 0; l < NL; ++l) {
+                cnt0[l] = cnt1[l];
+                ri0[l] = ri1[l];
+                id0[l] = id1[l];
+            }
+        }
+        if (deg) atomicAdd(&a.st->degenerate, deg);
+    }
+
+    static __device__ void run(const CoreBwdArgs& a) {
+        if (a.st->cl_abort) return;
+        const int wave = threadIdx.x >> 6;
+        int c, g;
+        cluster_rank((int)blockIdx.x, a.cl.G, c, g);
+        const int b = a.cl.b0 + c;
+        if (wave == 0 && (threadIdx.x & 63) == 0) *flag(a) = 0;
+        __syncthreads();
+        if (wave == 0) {
+            neuron_wave(a, b, c, g);
+            return;
+        }
+        int r = 0;
+#pragma unroll
+        for (int l = 0; l < NL; ++l)
+#pragma unroll
+            for (int pp = 0; pp < NP; ++pp)
+                if (pp < a.ly[l].npost) {
+                    if (r == wave - 1) {
+                        gather_wave(a, b, g, r, l, pp);
+                        return;
+                    }
+                    ++r;
+                }
+    }
+};
+
+template <int NL, int NP>
+__global__ void __launch_bounds__(64 * (1 + NL * NP)) backward_cluster_kernel(CoreBwdArgs a) {
+    BwdCluster<NL, NP>::run(a);
 }
 
 // ------------------------------------------------------------------ grouping
@@ -966,12 +1275,13 @@ hipError_t launch_backward_core(const CoreBwdArgs& a, int n_lif, int threads, si
     return hipGetLastError();
 }
 
-// Cluster mode: 64-thread workgroups, every adjoint ring in LDS, G
-// workgroups per sample, one cooperative launch (the runtime refuses a grid
-// that cannot be resident at once, so every wait of a cluster ends).
+// Cluster mode: a neuron wave and one gather wave per LIF -> LIF
+// projection per workgroup, G workgroups per sample, one cooperative launch
+// (the runtime refuses a grid that cannot be resident at once, so every wait
+// of a cluster ends).
 template <int NL, int NP>
 static const void* bcl_fn() {
-    return (const void*)backward_core_kernel<64, NL, bwd_prefetch_cl(NL), NP, true, true>;
+    return (const void*)backward_cluster_kernel<NL, NP>;
 }
 
 static const void* bcl_kernel(int n_lif, int np) {
@@ -987,19 +1297,23 @@ static const void* bcl_kernel(int n_lif, int np) {
     }
 }
 
-hipError_t launch_backward_core_cluster(const CoreBwdArgs& a, int n_lif, int np, int grid, size_t lds,
-                                        hipStream_t s) {
+hipError_t launch_backward_core_cluster(const CoreBwdArgs& a, int n_lif, int np, int grid, int threads,
+                                        size_t lds, hipStream_t s) {
     const void* f = bcl_kernel(n_lif, np);
-    if (!f || a.NW != 1 || a.cl.G < 1 || grid < a.cl.G || grid % a.cl.G) return hipErrorInvalidValue;
+    int rings = 0;
+    for (int l = 0; l < n_lif; ++l) rings += a.ly[l].npost;
+    if (!f || a.cl.G < 1 || grid < a.cl.G || grid % a.cl.G || threads != 64 * (1 + rings) ||
+        rings > n_lif * np)
+        return hipErrorInvalidValue;
     CoreBwdArgs arg = a;
     void* args[] = {&arg};
-    return hipLaunchCooperativeKernel(f, dim3(grid), dim3(64), args, (unsigned)lds, s);
+    return hipLaunchCooperativeKernel(f, dim3(grid), dim3(threads), args, (unsigned)lds, s);
 }
 
-hipError_t backward_cluster_occupancy(int n_lif, int np, size_t lds, int* blocks_per_cu) {
+hipError_t backward_cluster_occupancy(int n_lif, int np, int threads, size_t lds, int* blocks_per_cu) {
     const void* f = bcl_kernel(n_lif, np);
     if (!f) return hipErrorInvalidValue;
-    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, f, 64, lds);
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, f, threads, lds);
 }
 
 hipError_t launch_group(const GroupArgs& a, int B, hipStream_t s) {

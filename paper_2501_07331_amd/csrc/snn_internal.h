@@ -89,9 +89,9 @@ struct InScanArgs {
 // covers nearly every step of a 256-neuron layer at 14 spikes per neuron
 // while its input is active (8 left a quarter of them to an extra round).
 constexpr int bwd_prefetch(int n_lif) { return n_lif == 1 ? 16 : 4; }
-// The same in cluster mode, whose one-wave workgroups have registers to
-// spare: a round of spikes costs an exchange between the workgroups there.
-constexpr int bwd_prefetch_cl(int n_lif) { return n_lif <= 2 ? 16 : 8; }
+// Spikes per layer and round of the backward core in cluster mode: a round
+// costs one exchange between the workgroups of a sample.
+constexpr int kClKC = 32;
 
 // One LIF layer as seen by the forward core.
 struct FwdLayer {
@@ -209,7 +209,9 @@ struct CoreBwdArgs {
     DevStatus* st;
     int part_off;                      // LDS byte offset of the partial jump sums
     ClusterArgs cl;                    // cluster mode (cl.G > 0): adjoint rings in LDS, row width 64
-    int cl_off;                        // cluster mode: LDS byte offset of the exchange staging
+    int cl_off;                        // cluster mode: LDS byte offset of the exchange staging (shares
+                                       // [NL NP][kClKC][4] fp64, slot totals [NL kClKC] fp64, own
+                                       // positions [NL][64] int, abort flag)
 };
 
 // Spikes of each sample grouped by presynaptic neuron, in step order.
@@ -327,14 +329,13 @@ hipError_t set_core_lds_limits_256(size_t bytes, int* bad);
 hipError_t set_core_lds_limits_1024(size_t bytes, int* bad);
 hipError_t set_backward_lds_limits(size_t bytes, int* bad);
 // Cluster mode (CoreFwdArgs::cl, CoreBwdArgs::cl): grid = clusters x G
-// workgroups, launched cooperatively; occupancy in workgroups per CU.  A
-// forward workgroup has 64 (1 + LIF -> LIF rings) threads (a neuron wave and
-// one wave per ring), a backward one 64.
+// workgroups of 64 (1 + LIF -> LIF projections) threads (a neuron wave and
+// one wave per ring), launched cooperatively; occupancy in workgroups per CU.
 hipError_t launch_forward_core_cluster(const CoreFwdArgs& a, int n_lif, int np, int grid, int threads,
                                        size_t lds, hipStream_t s);
 hipError_t forward_cluster_occupancy(int n_lif, int np, int threads, size_t lds, int* blocks_per_cu);
 hipError_t set_core_lds_limits_cl(size_t bytes, int* bad);
-hipError_t launch_backward_core_cluster(const CoreBwdArgs& a, int n_lif, int np, int grid, size_t lds,
-                                        hipStream_t s);
-hipError_t backward_cluster_occupancy(int n_lif, int np, size_t lds, int* blocks_per_cu);
+hipError_t launch_backward_core_cluster(const CoreBwdArgs& a, int n_lif, int np, int grid, int threads,
+                                        size_t lds, hipStream_t s);
+hipError_t backward_cluster_occupancy(int n_lif, int np, int threads, size_t lds, int* blocks_per_cu);
 hipError_t launch_clear_abort(DevStatus* st, hipStream_t s);
