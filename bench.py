@@ -264,8 +264,9 @@ def configs_bench(args):
             loss = torch.zeros(wl.B + 1, device=dev)
             dW = [torch.zeros_like(w) for w in W]
             dD = [torch.zeros_like(w) for w in W]
+            flags = snn.SNN_FLAG_TIMING | (snn.SNN_FLAG_HBM_RINGS if args.hbm_rings else 0)
             net = snn.Network(c.layers, c.tau_m, c.tau_s, c.theta, c.dt, c.max_delay, wl.B, wl.T,
-                              c.loss, c.readout_scale, cap, flags=snn.SNN_FLAG_TIMING, stream=stream,
+                              c.loss, c.readout_scale, cap, flags=flags, stream=stream,
                               proj_max_delay=list(c.delay_range))
             el, kt = _time_steps(net, (off, st, ne, W, D, labels, recs, loss), dW, dD, args.steps,
                                  args.warmup)
@@ -277,6 +278,7 @@ def configs_bench(args):
         NS = wl.B * wl.T * sum(l[0] for l in c.layers[1:])
         byt = 34 * E + 16 * NS + 16 * sum(spikes) + 8 * s["input_spikes"]
         print(json.dumps({"sweep": "configs", "config": cid, "workload": c.name, "B": wl.B, "T": wl.T,
+                          "rings": "device memory" if args.hbm_rings else "default",
                           "ms_per_step": round(1e3 * el, 4), "events": E, "events_per_s": E / el,
                           "step_alg_bytes": byt,
                           "step_alg_bytes_frac_of_hbm_peak": round(byt / el / 1e9 / HBM_PEAK_GBS, 4),
@@ -349,6 +351,9 @@ def main():
                          "stated size; one JSON line per point")
     ap.add_argument("--points", type=str, default=None,
                     help="comma-separated sweep points (max delays in steps, or dt in ms)")
+    ap.add_argument("--hbm-rings", action="store_true",
+                    help="with --sweep configs: every ring in device memory, one workgroup per "
+                         "sample (the library's path before its cluster mode)")
     args = ap.parse_args()
     if args.sweep:
         sweep(args)
