@@ -45,6 +45,7 @@ hipError_t scratch_address(int** out) {
 namespace {
 
 constexpr size_t kLds = 160 * 1024;   // gfx950: 160 KiB of LDS per workgroup
+constexpr int kGroupStage = 16384;    // spikes of a sample the grouping stages in LDS (32 KiB)
 enum { K_SCAN, K_CORE, K_READ, K_RADJ, K_BCORE, K_GROUP, K_GRAD, K_N };
 
 size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
@@ -79,7 +80,8 @@ struct snn_net {
     int cl_threads;             // workgroup: the neuron wave and one wave per LIF -> LIF projection
     unsigned cl_tag;
     unsigned long long* clx;
-    int grad_J, grad_TW, grad_KL, grad_threads, grad_SB, grad_bs, grad_nblk, grad_ngroups, grad_spcap;
+    int grad_J, grad_TW, grad_KL, grad_threads, grad_SB, grad_bs, grad_nblk, grad_ngroups, grad_spcap,
+        grad_glcap;
     GradGroup grad_grp[SNN_MAX_LAYERS];
     hipStream_t stream;
     hipStream_t aux;                   // second stream: spike grouping beside the backward sweep
@@ -102,7 +104,7 @@ struct snn_net {
     int* rec_idx;
     int* rec_cnt;
     int* rec_goff;
-    int* rec_gstep;
+    unsigned short* rec_gstep;
     float* z;
     int* nstar;
     double* src;
@@ -119,7 +121,7 @@ struct snn_net {
     int ran[K_N];               // kernels enqueued (and timed) by the last call
     long long adam_steps;
     int* in_goff;
-    int* in_gstep;
+    unsigned short* in_gstep;
     long long in_gstep_cap;
     int* scratch;               // device address of the fixed scratch (snn_backward_noalloc)
     DevStatus* st;
@@ -153,6 +155,9 @@ static int fail(snn_net* net, int code, const char* fmt, ...) {
         if (e_ != hipSuccess)                                                                    \
             return fail((net), SNN_EDEVICE, "%s: %s", #expr, hipGetErrorString(e_));            \
     } while (0)
+
+// Entries per LIF layer of the grouped spike steps (16-bit).
+static size_t gstep_stride(size_t B, size_t cap) { return (B * cap + 7) & ~(size_t)7; }
 
 static void free_all(snn_net* n) {
     void* bufs[] = {n->slot,    n->in_idx,  n->A_in,     n->rec_n,     n->rec_s,  n->rec_I,
@@ -511,25 +516,38 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         }
     }
     // readout adjoint: the [T][C] table of lambda_I - lambda_V (fp64) in LDS when it fits
-    net->radj_threads = std::min(1024, std::max(256, ((C + 63) / 64) * 64));
+    net->radj_threads = 512;
     net->radj_tab = (!hbm && (size_t)t.T * C * sizeof(double) <= kLds) ? 1 : 0;
     net->lds_radj = net->radj_tab ? (size_t)t.T * C * sizeof(double) : 0;
     // gradients: one group per post layer (its projections in projection
     // order), J posts per workgroup, samples split into SB blocks so that the
     // grid has about 512 workgroups; workgroups in units of 4 J-blocks.  LDS:
-    // the J trajectories of a sample [J][T] double2, J = 8, 4 or 2 within
-    // 128 KiB (longer trials: J = 8 in windows of 1024 steps), and the rest of
-    // the LDS for the sample's spike steps (16-bit)
+    // the J trajectories of a sample [T + 1][J] double2 (row T: zeros), J =
+    // 8, 4 or 2 (longer trials: J = 8 in windows of at most 1024 steps); the
+    // spike-list offsets of the sample's presynaptic layers; the rest for its
+    // spike steps (16-bit)
     const size_t grad_total = kLds;
+    int grad_maxpre = 64;
+    for (int q = 1; q < n_layers; ++q) {
+        int v = 0;
+        for (int p = 0; p < t.P; ++p)
+            if (t.post[p] == q) v += t.n[t.pre[p]];
+        grad_maxpre = std::max(grad_maxpre, v);
+    }
+    // the spike-list offsets of both presynaptic layers of a group
+    const int grad_glcap = (grad_maxpre + 2 + 3) & ~3;
     {
-        const size_t tj = (size_t)t.T * sizeof(double2);
+        // the trajectories within 128 KiB, and within what the offsets and
+        // 16 KiB of spike steps leave
+        const size_t tb = std::min<size_t>(128 * 1024, grad_total - (size_t)grad_glcap * sizeof(int) - 16 * 1024);
+        const size_t tj = ((size_t)t.T + 1) * sizeof(double2);
         net->grad_J = 0;
         net->grad_TW = t.T;
         for (int j : {8, 4, 2})
-            if (!net->grad_J && j * tj <= 128 * 1024) net->grad_J = j;
+            if (!net->grad_J && j * tj <= tb) net->grad_J = j;
         if (!net->grad_J) {
             net->grad_J = 8;
-            net->grad_TW = 1024;
+            net->grad_TW = std::min(1024, (int)(tb / (8 * sizeof(double2))) - 1);
         }
         const int J = net->grad_J;
         int ng = 0, jblocks = 0, maxpre = 64;
@@ -590,10 +608,14 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         const int pairs = J * maxpre;
         net->grad_KL = (pairs <= 4 * 1024) ? 4 : 8;
         net->grad_threads = std::min(1024, ((pairs + net->grad_KL - 1) / net->grad_KL + 63) / 64 * 64);
-        const size_t traj = (size_t)J * net->grad_TW * sizeof(double2);
-        const size_t room = (traj < grad_total) ? grad_total - traj : 0;
-        net->grad_spcap = (int)(room / sizeof(unsigned short)) & ~7;
-        net->lds_grad = traj + (size_t)net->grad_spcap * sizeof(unsigned short);
+        const size_t traj = (size_t)J * (net->grad_TW + 1) * sizeof(double2);
+        const size_t gl = (size_t)grad_glcap * sizeof(int);
+        const size_t room = (traj + gl < grad_total) ? grad_total - traj - gl : 0;
+        // (eight entries of slack: a spike loop reads up to three past a list)
+        const size_t ent = room / sizeof(unsigned short);
+        net->grad_spcap = (int)(ent >= 8 ? ent - 8 : 0) & ~7;
+        net->grad_glcap = grad_glcap;
+        net->lds_grad = traj + gl + (size_t)(net->grad_spcap + 8) * sizeof(unsigned short);
     }
 
     // ---- device scratch
@@ -619,7 +641,9 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     ALLOC(net->rec_idx, nl * B * T1);
     ALLOC(net->rec_cnt, nl * B);
     ALLOC(net->rec_goff, nl * B * (t.maxn + 1));
-    ALLOC(net->rec_gstep, nl * B * cap);
+    // (per layer a multiple of 8 entries, so that every layer starts 16-byte
+    // aligned, and slack: the gradient pass copies the 16-bit lists as dwords)
+    ALLOC(net->rec_gstep, nl * gstep_stride(B, cap) + 8);
     ALLOC(net->z, B * C);
     ALLOC(net->nstar, B * C);
     ALLOC(net->src, B * C);
@@ -984,10 +1008,10 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
 }
 
 // The backward pass.  in_goff / in_gstep: where the input spikes grouped by
-// channel go ([B][n_in + 1] and [nnz] int32); NULL: the handle's own buffers
+// channel go ([B][n_in + 1] int32 and [nnz + 8] 16-bit); NULL: the handle's own buffers
 // (in_gstep grown on demand).
 static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW, float* const* dD,
-                         int* in_goff, int* in_gstep) {
+                         int* in_goff, unsigned short* in_gstep) {
     if (!net) return SNN_EINVAL;
     net->err[0] = 0;
     Topo& t = net->t;
@@ -1019,7 +1043,8 @@ static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW
         if (net->in_gstep) HIP_TRY(net, hipFree(net->in_gstep));
         net->in_gstep = nullptr;
         net->in_gstep_cap = 0;
-        const hipError_t e = hipMalloc((void**)&net->in_gstep, (size_t)net->in_nnz * sizeof(int));
+        const hipError_t e =
+            hipMalloc((void**)&net->in_gstep, ((size_t)net->in_nnz + 8) * sizeof(unsigned short));
         if (e != hipSuccess)
             return fail(net, e == hipErrorOutOfMemory ? SNN_ENOMEM : SNN_EDEVICE, "hipMalloc: %s",
                         hipGetErrorString(e));
@@ -1027,42 +1052,6 @@ static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW
     }
     if (!in_goff) in_goff = net->in_goff;
     if (!in_gstep) in_gstep = net->in_gstep;
-    // spikes grouped by presynaptic neuron (inputs, then every LIF layer) on
-    // the second stream: they depend on the forward only, and run beside the
-    // latency-bound adjoint sweeps; the gradients wait for them
-    const hipStream_t g_s = net->aux;
-    HIP_TRY(net, hipEventRecord(net->fork, s));
-    HIP_TRY(net, hipStreamWaitEvent(g_s, net->fork, 0));
-    net->ran[K_GROUP] = 1;
-    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GROUP], g_s));
-    {
-        GroupArgs g{};
-        g.off = net->in_off;
-        g.end = net->in_off;
-        g.step = net->in_step;
-        g.neuron = net->in_neuron;
-        g.n = t.n_in;
-        g.g_off = in_goff;
-        g.g_step = in_gstep;
-        g.st = net->st;
-        HIP_TRY(net, launch_group(g, t.B, g_s));
-    }
-    for (int l = 1; l < t.L; ++l) {
-        if (t.kind[l] != SNN_LIF) continue;
-        const size_t li = (size_t)t.lif[l];
-        GroupArgs g{};
-        g.cnt = net->rec_cnt + li * t.B;
-        g.off_stride = t.cap;
-        g.step = net->rec_s + li * t.B * t.cap;
-        g.neuron = net->rec_n + li * t.B * t.cap;
-        g.n = t.n[l];
-        g.g_off = net->rec_goff + li * t.B * (t.maxn + 1);
-        g.g_step = net->rec_gstep + li * t.B * t.cap;
-        g.st = net->st;
-        HIP_TRY(net, launch_group(g, t.B, g_s));
-    }
-    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GROUP + 1], g_s));
-    HIP_TRY(net, hipEventRecord(net->join, g_s));
     const int C = t.n[t.out_l];
     const int feed = t.pre[t.out_p];
     const size_t B = t.B, cap = t.cap;
@@ -1076,6 +1065,22 @@ static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW
         r.alpha = net->alpha64;
         r.beta = net->beta64;
         r.cc = net->cc64;
+        // chunks of at least 8 steps, one lane per (output, chunk), and the
+        // free propagator over a whole chunk
+        {
+            const int nch = std::max(1, std::min(net->radj_threads / C, (t.T + 7) / 8));
+            r.LC = (t.T + nch - 1) / nch;
+            r.nch = (t.T + r.LC - 1) / r.LC;
+            double p11 = 1.0, p12 = 0.0, p22 = 1.0;
+            for (int j = 0; j < r.LC; ++j) {
+                p12 = r.beta * p12 + r.cc * p22;
+                p11 = r.beta * p11;
+                p22 = r.alpha * p22;
+            }
+            r.P11 = p11;
+            r.P12 = p12;
+            r.P22 = p22;
+        }
         r.ws = net->ws + t.woff[t.out_p];
         if (feed != 0) {
             const size_t li = (size_t)t.lif[feed];
@@ -1090,6 +1095,45 @@ static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW
         r.tab_lds = net->radj_tab;
         TIMED(net, K_RADJ, launch_readout_adjoint(r, net->radj_threads, net->lds_radj, s));
     }
+    // spikes grouped by presynaptic neuron (inputs, then every LIF layer) on
+    // the second stream: they depend on the forward only, and run beside the
+    // latency-bound adjoint core (forked after the readout adjoint, whose
+    // workgroups take a whole CU's LDS); the gradients wait for them
+    const hipStream_t g_s = net->aux;
+    HIP_TRY(net, hipEventRecord(net->fork, s));
+    HIP_TRY(net, hipStreamWaitEvent(g_s, net->fork, 0));
+    net->ran[K_GROUP] = 1;
+    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GROUP], g_s));
+    {
+        GroupArgs g{};
+        g.off = net->in_off;
+        g.end = net->in_off;
+        g.step = net->in_step;
+        g.neuron = net->in_neuron;
+        g.n = t.n_in;
+        g.g_off = in_goff;
+        g.g_step = in_gstep;
+        g.stage_cap = (int)std::min<long long>(net->in_nnz, kGroupStage);
+        g.st = net->st;
+        HIP_TRY(net, launch_group(g, t.B, g_s));
+    }
+    for (int l = 1; l < t.L; ++l) {
+        if (t.kind[l] != SNN_LIF) continue;
+        const size_t li = (size_t)t.lif[l];
+        GroupArgs g{};
+        g.cnt = net->rec_cnt + li * t.B;
+        g.off_stride = t.cap;
+        g.step = net->rec_s + li * t.B * t.cap;
+        g.neuron = net->rec_n + li * t.B * t.cap;
+        g.n = t.n[l];
+        g.g_off = net->rec_goff + li * t.B * (t.maxn + 1);
+        g.g_step = net->rec_gstep + li * gstep_stride(t.B, t.cap);
+        g.stage_cap = std::min(t.cap, kGroupStage);
+        g.st = net->st;
+        HIP_TRY(net, launch_group(g, t.B, g_s));
+    }
+    if (net->timing) HIP_TRY(net, hipEventRecord(net->ev[2 * K_GROUP + 1], g_s));
+    HIP_TRY(net, hipEventRecord(net->join, g_s));
     // extra jump numerators per LIF layer: the readout part of the jump sums
     // (the layer feeding an LI readout), the spike-time loss's terms (LIF
     // output layer), plus the caller's dl_p/dt
@@ -1176,6 +1220,7 @@ static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW
     ga.TW = net->grad_TW;
     ga.SB = net->grad_SB;
     ga.spcap = net->grad_spcap;
+    ga.glcap = net->grad_glcap;
     ga.bs = net->grad_bs;
     ga.lif_total = t.lif_total;
     ga.C = C;
@@ -1198,7 +1243,7 @@ static int backward_impl(snn_net* net, const float* const* dlp, float* const* dW
         if (t.kind[l] != SNN_LIF) continue;
         const size_t li = (size_t)t.lif[l];
         ga.g_off[l] = net->rec_goff + li * t.B * (t.maxn + 1);
-        ga.g_step[l] = net->rec_gstep + li * t.B * t.cap;
+        ga.g_step[l] = net->rec_gstep + li * gstep_stride(t.B, t.cap);
     }
     for (int g = 0; g < net->grad_ngroups; ++g) ga.grp[g] = net->grad_grp[g];
     ga.part = net->gpart;
@@ -1237,7 +1282,8 @@ extern "C" int snn_backward_noalloc(snn_net* net, float* const* dW, float* const
     if (!net->scratch)
         return fail(net, SNN_EDEVICE, "snn_backward_noalloc: no scratch address for this device");
     int* goff = net->scratch;
-    return backward_impl(net, nullptr, dW, dD, goff, goff + (size_t)net->t.B * (net->t.n_in + 1));
+    return backward_impl(net, nullptr, dW, dD, goff,
+                         reinterpret_cast<unsigned short*>(goff + (size_t)net->t.B * (net->t.n_in + 1)));
 }
 
 extern "C" int snn_optimizer_step(snn_net* net, const snn_optim* o, float* const* W, float* const* D,

@@ -33,60 +33,115 @@ namespace {
 
 // ------------------------------------------------------------------ readout adjoint
 
-// Lanes k < C: lambda_I <- beta lambda_I + c lambda_V, lambda_V <- alpha
-// lambda_V (old lambda_V in both), then the step's loss source; the "+"
-// values before the source are the trajectory.  Then every thread takes
-// spikes (n, i) of the feeding LIF layer: A2 = sum_k w_ik (lambda_V -
-// lambda_I)_k at step n + slot_ik, over k ascending.  All fp64.
-__global__ void __launch_bounds__(1024) readout_adjoint_kernel(ReadoutBwdArgs a) {
-    const int b = blockIdx.x, tid = threadIdx.x;
-    const int C = a.C, T = a.T;
+// Per output k, over reverse time: lambda_I <- beta lambda_I + c lambda_V,
+// lambda_V <- alpha lambda_V (old lambda_V in both), then the step's loss
+// source; the values before the source are the trajectory.  The recursion is
+// linear, so it runs in three passes over chunks of LC steps, a lane per
+// (output, chunk): (A) each chunk from a zero state, (B) per output, the
+// state entering each chunk, chunk by chunk from the top (the state after a
+// whole chunk = M^LC (state entering it) + its zero-state response), (C)
+// each chunk again from its entering state, writing the trajectory.  The
+// chunk results pass through the trajectory array itself (the first row of
+// each chunk, rewritten by C).  Then every thread takes spikes (n, i) of the
+// feeding LIF layer: A2 = sum_k w_ik (lambda_V - lambda_I)_k at step n +
+// slot_ik, over k ascending.  All fp64.
+__global__ void __launch_bounds__(512) readout_adjoint_kernel(ReadoutBwdArgs a) {
+    const int b = blockIdx.x, tid = threadIdx.x, nt = blockDim.x;
+    const int C = a.C, T = a.T, LC = a.LC, nch = a.nch;
     lds_f64* tab = (lds_f64*)smem;                                // [T][C] lambda_I - lambda_V
-    if (tid < C) {
-        const double srcv = a.src[(size_t)b * C + tid];
-        const int nst = a.nstar[(size_t)b * C + tid];
-        double2* tr = a.traj + (size_t)b * T * C + tid;
-        double lv = 0.0, lI = 0.0;
-        for (int n = T - 1; n >= 0; --n) {
-            if (n <= T - 2) {
+    double2* trb = a.traj + (size_t)b * T * C;
+    // every thread's first record (the spike pass below), loaded first
+    const int cnt = a.rec_n ? a.rec_cnt[b] : 0;
+    const size_t base = (size_t)b * a.cap;
+    int i = 0, n = 0;
+    if (tid < cnt) {
+        i = a.rec_n[base + tid];
+        n = a.rec_s[base + tid];
+    }
+    auto chunk = [&](int x, bool out) {
+        const int k = x % C, c = x / C;
+        const int lo = c * LC, hi = min(T, lo + LC) - 1;
+        const double srcv = a.src[(size_t)b * C + k];
+        const int nst = a.nstar[(size_t)b * C + k];
+        double lI = 0.0, lv = 0.0;
+        if (out) {
+            const double2 e = trb[(size_t)lo * C + k];
+            lI = e.x;
+            lv = e.y;
+        }
+        for (int m = hi; m >= lo; --m) {
+            if (m <= T - 2) {
                 const double v = lv;
                 lI = __dadd_rn(__dmul_rn(a.beta, lI), __dmul_rn(a.cc, v));
                 lv = __dmul_rn(a.alpha, v);
             }
-            const double d = __dsub_rn(lI, lv);
-            tr[(size_t)n * C] = make_double2(lI, d);
-            if (a.tab_lds) tab[n * C + tid] = d;
-            if (a.loss == SNN_LOSS_CE_SUM || nst == n) lv = __dsub_rn(lv, srcv);
+            if (out) {
+                const double d = __dsub_rn(lI, lv);
+                trb[(size_t)m * C + k] = make_double2(lI, d);
+                if (a.tab_lds) tab[m * C + k] = d;
+            }
+            if (a.loss == SNN_LOSS_CE_SUM || nst == m) lv = __dsub_rn(lv, srcv);
+        }
+        if (!out) trb[(size_t)lo * C + k] = make_double2(lI, lv);
+    };
+    for (int x = tid; x < C * nch; x += nt) chunk(x, false);
+    __syncthreads();
+    for (int k = tid; k < C; k += nt) {
+        double eI = 0.0, ev = 0.0;                                // entering the top chunk
+        for (int c = nch - 1; c >= 0; --c) {
+            double2* p = trb + (size_t)c * LC * C + k;
+            const double2 r = *p;
+            *p = make_double2(eI, ev);
+            const double nI = __dadd_rn(__dadd_rn(__dmul_rn(a.P11, eI), __dmul_rn(a.P12, ev)), r.x);
+            const double nv = __dadd_rn(__dmul_rn(a.P22, ev), r.y);
+            eI = nI;
+            ev = nv;
         }
     }
+    __syncthreads();
+    for (int x = tid; x < C * nch; x += nt) chunk(x, true);
     if (!a.rec_n) return;
     __syncthreads();
-    const int cnt = a.rec_cnt[b];
-    const size_t base = (size_t)b * a.cap;
-    const double2* trb = a.traj + (size_t)b * T * C;
-    for (int r = tid; r < cnt; r += blockDim.x) {
-        const int i = a.rec_n[base + r], n = a.rec_s[base + r];
+    for (int r = tid; r < cnt; r += nt) {
+        // the next record's neuron and step, and the weights of this one in
+        // chunks of 16 outputs, each chunk's loads issued before the last
+        // chunk's terms are added (in output order)
+        int i2 = 0, n2 = 0;
+        if (r + nt < cnt) {
+            i2 = a.rec_n[base + r + nt];
+            n2 = a.rec_s[base + r + nt];
+        }
         const uint2* wsr = a.ws + (size_t)i * C;
+        uint2 e[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) e[u] = wsr[min(u, C - 1)];
         double acc = 0.0;
-        // four outputs at a time: their loads issued together, their terms
-        // added in output order
-        for (int k0 = 0; k0 < C; k0 += 4) {
-            uint2 e[4];
+        for (int k0 = 0; k0 < C; k0 += 16) {
+            const bool more = k0 + 16 < C;
+            uint2 f[16];
+            if (more) {
 #pragma unroll
-            for (int u = 0; u < 4; ++u) e[u] = wsr[min(k0 + u, C - 1)];
-            double d[4];
+                for (int u = 0; u < 16; ++u) f[u] = wsr[min(k0 + 16 + u, C - 1)];
+            }
+            double d[16];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < 16; ++u) {
                 const int k = min(k0 + u, C - 1);
                 const int m = min(n + (int)e[u].y, T - 1);
                 d[u] = a.tab_lds ? (double)tab[m * C + k] : trb[(size_t)m * C + k].y;
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
+            for (int u = 0; u < 16; ++u)
                 if (k0 + u < C && n + (int)e[u].y <= T - 1)
                     acc = __dsub_rn(acc, __dmul_rn((double)__uint_as_float(e[u].x), d[u]));
+            if (more) {
+#pragma unroll
+                for (int u = 0; u < 16; ++u) e[u] = f[u];
+            }
         }
         a.A2[base + r] = acc;
+        i = i2;
+        n = n2;
     }
 }
 
@@ -922,35 +977,43 @@ __global__ void __launch_bounds__(64 * (1 + NL * NP)) backward_cluster_kernel(Co
 // ------------------------------------------------------------------ grouping
 
 // One workgroup per sample: counting sort of the sample's spikes by
-// presynaptic neuron (LDS histogram), then each neuron's steps sorted.
+// presynaptic neuron (LDS histogram, block-wide scan), the steps scattered
+// into LDS (or, for a sample with more spikes than the LDS stage holds, into
+// device memory), each neuron's steps sorted (thread per neuron, insertion
+// sort: the spikes arrive in step order, so a neuron's list is nearly
+// sorted), then written out.
 __global__ void __launch_bounds__(1024) group_kernel(GroupArgs a) {
     if (a.st->bad_input) return;
     const int b = blockIdx.x, tid = threadIdx.x, nt = blockDim.x;
+    const int lane = tid & 63, wv = tid >> 6;
     const int start = a.cnt ? b * a.off_stride : a.off[b];
     const int end = a.cnt ? start + a.cnt[b] : a.end[b + 1];
-    int* h = reinterpret_cast<int*>(smem);        // [n + 1] counts, then cursors
-    int* part = h + a.n + 1;                      // [nt] block scan
+    const int cnt = end - start;
+    int* h = reinterpret_cast<int*>(smem);        // [n + 1] counts, then cursors (segment ends)
+    int* wsum = h + a.n + 1;                      // [16] per-wave sums
+    unsigned short* stage = reinterpret_cast<unsigned short*>(wsum + 16);   // [stage_cap]
+    const bool in_lds = cnt <= a.stage_cap;
+    unsigned short* dst = in_lds ? stage : a.g_step + start;
     for (int i = tid; i <= a.n; i += nt) h[i] = 0;
     __syncthreads();
     for (int e = start + tid; e < end; e += nt) atomicAdd(&h[a.neuron[e]], 1);
     __syncthreads();
-    // exclusive scan of h[0 .. n): thread tid scans a contiguous segment
+    // exclusive scan of h[0 .. n): thread tid sums a contiguous segment, the
+    // segment sums are scanned within each wave (shuffles) and across waves
     const int seg = (a.n + nt - 1) / nt;
     const int i0 = min(tid * seg, a.n), i1 = min(i0 + seg, a.n);
     int s = 0;
     for (int i = i0; i < i1; ++i) s += h[i];
-    part[tid] = s;
-    __syncthreads();
-    if (tid == 0) {
-        int run = 0;
-        for (int w = 0; w < nt; ++w) {
-            const int v = part[w];
-            part[w] = run;
-            run += v;
-        }
+    int incl = s;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int y = __shfl_up(incl, d, 64);
+        if (lane >= d) incl += y;
     }
+    if (lane == 63) wsum[wv] = incl;
     __syncthreads();
-    int run = part[tid];
+    int run = incl - s;
+    for (int w = 0; w < wv; ++w) run += wsum[w];
     int* goff = a.g_off + (size_t)b * (a.n + 1);
     for (int i = i0; i < i1; ++i) {
         const int v = h[i];
@@ -962,21 +1025,25 @@ __global__ void __launch_bounds__(1024) group_kernel(GroupArgs a) {
     __syncthreads();
     for (int e = start + tid; e < end; e += nt) {
         const int pos = atomicAdd(&h[a.neuron[e]], 1);
-        a.g_step[start + pos] = a.step[e];
+        dst[pos] = (unsigned short)a.step[e];
     }
     __syncthreads();
+    // h[i] is now the end of neuron i's segment
     for (int i = tid; i < a.n; i += nt) {
-        const int lo = goff[i], hi = goff[i + 1];
+        const int lo = i ? h[i - 1] : 0, hi = h[i];
         for (int x = lo + 1; x < hi; ++x) {
-            const int v = a.g_step[x];
+            const int v = dst[x];
             int y = x - 1;
-            while (y >= lo && a.g_step[y] > v) {
-                a.g_step[y + 1] = a.g_step[y];
+            while (y >= lo && dst[y] > v) {
+                dst[y + 1] = dst[y];
                 --y;
             }
-            a.g_step[y + 1] = v;
+            dst[y + 1] = (unsigned short)v;
         }
     }
+    if (!in_lds) return;
+    __syncthreads();
+    for (int x = tid; x < cnt; x += nt) a.g_step[start + x] = stage[x];
 }
 
 // ------------------------------------------------------------------ gradients
@@ -991,6 +1058,8 @@ __global__ void __launch_bounds__(1024) group_kernel(GroupArgs a) {
 // (similar spike counts, little divergence) and a lane's neurons lie nt / J
 // apart, so every lane sums about the same number of spikes however the
 // input concentrates on some channels.  Per sample the J post trajectories
+// (step-major, [step][post], so the J lanes of a presynaptic neuron read J
+// consecutive 16-byte cells of a row, in different banks, plus a zero row)
 // and the sample's grouped spike steps are staged in LDS; each lane sums, per
 // synapse, in sample then spike order, lambda_I and lambda_I - lambda_V at
 // the delayed arrivals in fp64; the weight multiplies the delay sum once at
@@ -1000,6 +1069,37 @@ __global__ void __launch_bounds__(1024) group_kernel(GroupArgs a) {
 // Workgroups come in units of four J-post blocks that share lines of the
 // [B][T][N] trajectories; a unit's four blocks have indices 8 apart, so with
 // round-robin dispatch over the 8 XCDs they run on one XCD and share its L2.
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// n dwords from src to dst in LDS (both 4-byte aligned) as direct loads into
+// LDS: wave w of nw takes the 64-dword chunks w, w + nw, ...; the caller
+// waits for them (vmcnt) before a barrier.
+__device__ inline void lds_dwords(const void* src, void* dst, int n, int w, int nw, int lane) {
+    for (int c = w; c * 64 < n; c += nw) {
+        const int i = c * 64 + lane;
+        if (i < n)
+            __builtin_amdgcn_global_load_lds(static_cast<const char*>(src) + (size_t)i * 4,
+                                             (lds_ptr_t)(static_cast<char*>(dst) + (size_t)c * 256), 4, 0, 0);
+    }
+}
+
+// Rows [0, W) of J consecutive posts (row r at src + r ld) into dst [W][J]
+// in LDS as direct 16-byte loads: one wave load covers 64 / J rows (lane:
+// row lane / J, post lane % J; posts past nj repeat the last one, a cell
+// that is never read).
+template <int J>
+__device__ inline void lds_rows(const double2* src, int ld, int nj, double2* dst, int W, int w, int nw,
+                                int lane) {
+    constexpr int R = 64 / J;
+    const int r = lane / J, q = min(lane % J, nj - 1);
+    for (int c = w; c * R < W; c += nw) {
+        const int row = c * R + r;
+        if (row < W)
+            __builtin_amdgcn_global_load_lds(src + (size_t)row * ld + q, (lds_ptr_t)(dst + (size_t)c * 64), 16,
+                                             0, 0);
+    }
+}
+
 template <int J, int KL, bool WIN>
 __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
     const int tid = threadIdx.x, nt = blockDim.x;
@@ -1015,16 +1115,19 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
     const int nq = G.nq, j0 = jb * J, nj = min(J, nq - j0);
     const int T = a.T;
     const int TW = WIN ? a.TW : a.T;                            // steps per trajectory window
-    double2* st = reinterpret_cast<double2*>(smem);            // [J][TW]
-    unsigned short* sp = reinterpret_cast<unsigned short*>(smem + (size_t)J * TW * sizeof(double2));
+    double2* st = reinterpret_cast<double2*>(smem);            // [TW + 1][J]
+    int* gl = reinterpret_cast<int*>(smem + (size_t)J * (TW + 1) * sizeof(double2));   // [glcap]
+    unsigned short* sp = reinterpret_cast<unsigned short*>(gl + a.glcap);               // [spcap + 8]
+    const int lane = tid & 63, nw = nt >> 6;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const double2* tr = G.out ? a.tr_out : a.tr_lif;
     const int LN = G.out ? a.C : a.lif_total;
     const int n0 = G.npre[0], n1 = (G.np > 1) ? G.npre[1] : 0;
     const int vtot = n0 + n1;
     const int* go0 = a.g_off[G.pre[0]];
     const int* go1 = a.g_off[G.pre[G.np > 1 ? 1 : 0]];
-    const int* gs0 = a.g_step[G.pre[0]];
-    const int* gs1 = a.g_step[G.pre[G.np > 1 ? 1 : 0]];
+    const unsigned short* gs0 = a.g_step[G.pre[0]];
+    const unsigned short* gs1 = a.g_step[G.pre[G.np > 1 ? 1 : 0]];
     const int b0 = sb * a.bs, b1 = min(a.B, b0 + a.bs);
     for (int pbase = 0; pbase < J * vtot; pbase += nt * KL) {
         // this lane's synapses, one word each: presynaptic index (bits 0-15),
@@ -1048,65 +1151,63 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
             su[k] = 0.0;
             sd[k] = 0.0;
         }
+        // the list bounds of the first sample (those of the next are loaded
+        // while a sample is staged)
+        int s0 = go0[(size_t)b0 * (n0 + 1)], e0 = go0[(size_t)b0 * (n0 + 1) + n0];
+        int s1 = n1 ? go1[(size_t)b0 * (n1 + 1)] : 0, e1 = n1 ? go1[(size_t)b0 * (n1 + 1) + n1] : 0;
         for (int b = b0; b < b1; ++b) {
+            __syncthreads();                                       // the last sample's reads are done
+            // (LDS stores first: the compiler waits for the direct loads
+            // before any LDS store that follows them)
+            if (tid < J) st[min(TW, T) * J + tid] = make_double2(0.0, 0.0);   // row W: no arrival
+            // Staging, as direct loads into LDS (no registers, all in flight
+            // at once, one memory round trip per sample): the spike-list
+            // offsets of both presynaptic layers, the grouped spike steps
+            // (16-bit, copied as aligned dwords: list 0 from s0 rounded down
+            // to even, list 1 from an even LDS index), the first window of the
+            // J post trajectories.
+            const int a0 = s0 & ~1, a1 = s1 & ~1;
+            const int L0 = e0 - a0, A1 = (L0 + 1) & ~1, L1 = n1 ? e1 - a1 : 0;
+            const bool in_lds = A1 + L1 + 1 <= a.spcap;
+            const int off0 = -a0, off1 = A1 - a1;                 // LDS index = x + off
+            if (b + 1 < b1) {                                      // the next sample's bounds
+                const size_t o0 = (size_t)(b + 1) * (n0 + 1), o1 = (size_t)(b + 1) * (n1 + 1);
+                s0 = go0[o0];
+                e0 = go0[o0 + n0];
+                s1 = n1 ? go1[o1] : 0;
+                e1 = n1 ? go1[o1 + n1] : 0;
+            }
+            lds_dwords(go0 + (size_t)b * (n0 + 1), gl, n0 + 1, wv, nw, lane);
+            if (n1) lds_dwords(go1 + (size_t)b * (n1 + 1), gl + n0 + 1, n1 + 1, wv, nw, lane);
+            if (in_lds) {
+                lds_dwords(gs0 + a0, sp, (L0 + 1) >> 1, wv, nw, lane);
+                if (L1 > 0) lds_dwords(gs1 + a1, sp + A1, (L1 + 1) >> 1, wv, nw, lane);
+            }
+            const size_t base = (size_t)b * T * LN + G.off + j0;
+            lds_rows<J>(tr + base, LN, nj, st, min(TW, T), wv, nw, lane);
+            __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             // spike lists of this lane's neurons (offsets into g_step)
             int lo[KL], hi[KL];
 #pragma unroll
             for (int k = 0; k < KL; ++k) {
                 const int i = dsc[k] & 0xFFFF, pi = (dsc[k] >> 20) & 1;
-                const int* go = pi ? go1 + (size_t)b * (n1 + 1) : go0 + (size_t)b * (n0 + 1);
+                const int* go = gl + (pi ? n0 + 1 : 0);
                 lo[k] = (dsc[k] >= 0) ? go[i] : 0;
                 hi[k] = (dsc[k] >= 0) ? go[i + 1] : 0;
-            }
-            // the sample's grouped spike steps of both presynaptic layers
-            const int s0 = go0[(size_t)b * (n0 + 1)], e0 = go0[(size_t)b * (n0 + 1) + n0];
-            const int s1 = n1 ? go1[(size_t)b * (n1 + 1)] : 0, e1 = n1 ? go1[(size_t)b * (n1 + 1) + n1] : 0;
-            const int c0 = e0 - s0, c1 = e1 - s1;
-            const bool in_lds = c0 + c1 <= a.spcap;
-            // (loads of eight iterations issued before their stores, so that a
-            // sample's staging costs a few memory round trips, not one each)
-            constexpr int U = (KL > 4) ? 4 : 8;
-            if (in_lds) {
-                for (int x0 = tid; x0 < c0 + c1; x0 += U * nt) {
-                    int v[U];
-#pragma unroll
-                    for (int u = 0; u < U; ++u) {
-                        const int x = x0 + u * nt;
-                        const int xc = min(x, c0 + c1 - 1);
-                        v[u] = (xc < c0) ? gs0[s0 + xc] : gs1[s1 + xc - c0];
-                    }
-#pragma unroll
-                    for (int u = 0; u < U; ++u)
-                        if (x0 + u * nt < c0 + c1) sp[x0 + u * nt] = (unsigned short)v[u];
-                }
             }
             // the J post trajectories of the sample, in windows of TW steps
             // (one window unless the trial is long); a synapse's spikes are
             // taken in step order, window by window, from a cursor
-            const size_t base = (size_t)b * T * LN + G.off + j0;
             for (int w0 = 0; w0 < T; w0 += TW) {
                 const int W = min(TW, T - w0), wend = w0 + W;
-                if (w0 > 0) __syncthreads();                        // the last window's reads are done
-                for (int e0 = tid; e0 < W * J; e0 += U * nt) {
-                    double2 x[U];
-#pragma unroll
-                    for (int u = 0; u < U; ++u) {
-                        const int e = min(e0 + u * nt, W * J - 1);
-                        const int m = w0 + e / J, q = e % J;
-                        const int qc = min(q, nj - 1);
-                        x[u] = tr[base + (size_t)m * LN + qc];
-                    }
-#pragma unroll
-                    for (int u = 0; u < U; ++u) {
-                        const int e = e0 + u * nt;
-                        if (e < W * J) {
-                            const int mw = e / J, q = e % J;
-                            st[q * TW + mw] = (q < nj) ? x[u] : make_double2(0.0, 0.0);
-                        }
-                    }
+                if (w0 > 0) {
+                    __syncthreads();                                // the last window's reads are done
+                    if (tid < J) st[W * J + tid] = make_double2(0.0, 0.0);
+                    lds_rows<J>(tr + base + (size_t)w0 * LN, LN, nj, st, W, wv, nw, lane);
+                    __builtin_amdgcn_s_waitcnt(0);
+                    __syncthreads();
                 }
-                __syncthreads();
 #pragma unroll
                 for (int k = 0; k < KL; ++k) {
                     // the descriptor is made opaque here, so that what derives
@@ -1117,17 +1218,18 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
                     asm volatile("" : "+v"(dk));
                     if (dk < 0) continue;
                     const int pi = (dk >> 20) & 1, sl = (dk >> 21) & 0xFF;
-                    const double2* stk = st + ((dk >> 16) & 0xF) * TW;       // index: arrival - w0
-                    const int* gs = pi ? gs1 : gs0;
-                    const int off = pi ? c0 - s1 : -s0;             // LDS index = x + off
+                    const double2* stk = st + ((dk >> 16) & 0xF);            // row: arrival - w0
+                    const unsigned short* gs = pi ? gs1 : gs0;
+                    const int off = pi ? off1 : off0;
                     double pu = su[k], pd = sd[k];
                     // four spikes at a time: their reads issued together, their
                     // terms added in spike order; the arrivals ascend, so the
                     // window's spikes are a prefix from the cursor.  The loop
                     // comes in two copies, spike steps in LDS or in device
                     // memory (one choice per sample), and a term past the
-                    // window adds +0 (the sums start at +0, so they never hold
-                    // -0 and +0 changes nothing): no branch inside.
+                    // window or past the list reads the zero row W and adds +0
+                    // (the sums start at +0, so they never hold -0 and +0
+                    // changes nothing): no branch and no select inside.
                     int x = lo[k];
                     const int h = hi[k];
                     auto spikes = [&](auto in_lds_tag) {
@@ -1139,20 +1241,20 @@ __global__ void __launch_bounds__(1024) gradients_kernel(GradArgs a) {
                             int t[4], m[4];
 #pragma unroll
                             for (int u = 0; u < 4; ++u) {
-                                const int xc = min(x + u, h - 1);
-                                t[u] = SPL ? (int)sp[xc + off] : gs[xc];
+                                // (the LDS list has slack past its end:
+                                // no clamp there)
+                                t[u] = SPL ? (int)sp[x + u + off] : gs[min(x + u, h - 1)];
                             }
                             asm volatile("" : "+v"(t[0]), "+v"(t[1]), "+v"(t[2]), "+v"(t[3]));
 #pragma unroll
                             for (int u = 0; u < 4; ++u) m[u] = (x + u < h) ? t[u] + sl : T;   // T: no arrival
                             double2 ud[4];
 #pragma unroll
-                            for (int u = 0; u < 4; ++u) ud[u] = stk[(m[u] < wend) ? m[u] - w0 : 0];
+                            for (int u = 0; u < 4; ++u) ud[u] = stk[min((unsigned)(m[u] - w0), (unsigned)W) * J];
 #pragma unroll
                             for (int u = 0; u < 4; ++u) {
-                                const bool ok = m[u] < wend;
-                                pu = __dadd_rn(pu, ok ? ud[u].x : 0.0);
-                                pd = __dadd_rn(pd, ok ? ud[u].y : 0.0);
+                                pu = __dadd_rn(pu, ud[u].x);
+                                pd = __dadd_rn(pd, ud[u].y);
                             }
                             if constexpr (WIN) {
                                 if (m[3] >= wend) {
@@ -1317,7 +1419,8 @@ hipError_t backward_cluster_occupancy(int n_lif, int np, int threads, size_t lds
 }
 
 hipError_t launch_group(const GroupArgs& a, int B, hipStream_t s) {
-    const size_t lds = sizeof(int) * ((size_t)a.n + 1 + 1024);
+    if (a.stage_cap < 0) return hipErrorInvalidValue;
+    const size_t lds = sizeof(int) * ((size_t)a.n + 1 + 16) + sizeof(unsigned short) * (size_t)a.stage_cap;
     hipLaunchKernelGGL(group_kernel, dim3(B), dim3(1024), lds, s, a);
     return hipGetLastError();
 }

@@ -166,6 +166,8 @@ struct ReadoutArgs {
 struct ReadoutBwdArgs {
     int B, T, C, cap, loss;
     double alpha, beta, cc;
+    int LC, nch;                       // reverse-time chunks: nch chunks of LC steps
+    double P11, P12, P22;              // M^LC, M = [[beta, cc], [0, alpha]] acting on (lambda_I, lambda_V)
     const uint2* ws;                   // [n_feed][C] (weight bits, slot)
     const int* rec_n;                  // records of the feeding LIF layer [B][cap], or NULL
     const int* rec_s;
@@ -224,7 +226,8 @@ struct GroupArgs {
     const int* neuron;
     int n;                             // presynaptic neurons
     int* g_off;                        // [B][n+1] start of neuron i's steps (absolute index)
-    int* g_step;                       // steps, grouped by neuron
+    unsigned short* g_step;            // steps (< 65536), grouped by neuron
+    int stage_cap;                     // spikes of a sample staged in LDS (more: sorted in place)
     const DevStatus* st;
 };
 
@@ -246,6 +249,7 @@ struct GradArgs {
     int B, T, SB, bs, lif_total, C, ngroups, nblk;
     int TW;                            // trajectory window: steps staged in LDS at a time
     int spcap;                         // LDS capacity for a sample's spike steps (16-bit), 0: none
+    int glcap;                         // LDS ints for a sample's spike-list offsets (multiple of 4)
     float tau_s, dt;
     long long nparams;
     const double2* tr_lif;             // [B][T][lif_total] (lambda_I, lambda_I - lambda_V)
@@ -253,7 +257,7 @@ struct GradArgs {
     const uint2* ws;                   // flat [params] (weight bits, slot)
     long long woff[SNN_MAXP];
     const int* g_off[SNN_MAX_LAYERS];  // per presynaptic layer: [B][n+1]
-    const int* g_step[SNN_MAX_LAYERS];
+    const unsigned short* g_step[SNN_MAX_LAYERS];
     GradGroup grp[SNN_MAX_LAYERS];
     double* part;                      // [SB][2][nparams] per sample block (SB > 1)
     float* dW[SNN_MAXP];
