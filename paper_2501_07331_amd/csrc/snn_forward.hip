@@ -34,13 +34,24 @@ __global__ void validate_kernel(const int* off, const int* step, const int* neur
     const int y = labels[b];
     if (y < 0 || y >= C) bad = true;
     if (!bad) {
-        for (int e = lo + (int)threadIdx.x; e < hi; e += blockDim.x) {
-            const int s = step[e], i = neuron[e];
-            if (s < 0 || s >= T || i < 0 || i >= n_in) bad = true;
-            if (e > lo) {
-                const long long k0 = (long long)step[e - 1] * n_in + neuron[e - 1];
-                const long long k1 = (long long)s * n_in + i;
-                if (k1 <= k0) bad = true;
+        // four events per thread and round, their loads issued together
+        const int nt = blockDim.x;
+        for (int e0 = lo + (int)threadIdx.x; e0 < hi; e0 += 4 * nt) {
+            int s[4], i[4], sp[4], ip[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int e = min(e0 + u * nt, hi - 1), ep = max(e - 1, lo);
+                s[u] = step[e];
+                i[u] = neuron[e];
+                sp[u] = step[ep];
+                ip[u] = neuron[ep];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int e = e0 + u * nt;
+                if (e >= hi) continue;
+                if (s[u] < 0 || s[u] >= T || i[u] < 0 || i[u] >= n_in) bad = true;
+                if (e > lo && (long long)s[u] * n_in + i[u] <= (long long)sp[u] * n_in + ip[u]) bad = true;
             }
         }
     }
@@ -512,7 +523,7 @@ hipError_t launch_clear_abort(DevStatus* st, hipStream_t s) {
 
 hipError_t launch_validate(const int* off, const int* step, const int* neuron, int nnz, int B, int T,
                            int n_in, const int* labels, int C, DevStatus* st, hipStream_t s) {
-    hipLaunchKernelGGL(validate_kernel, dim3(B), dim3(256), 0, s, off, step, neuron, nnz, B, T, n_in,
+    hipLaunchKernelGGL(validate_kernel, dim3(B), dim3(1024), 0, s, off, step, neuron, nnz, B, T, n_in,
                        labels, C, st);
     return hipGetLastError();
 }
