@@ -56,7 +56,29 @@ struct FwdCore {
         float V[NL], I[NL];
         int cnt[NL];                          // records so far (exact; may pass the capacity)
         int own[NL];                          // spikes of this lane's neuron
+        // this sample's record arrays and step table: uniform, but held in
+        // vector registers (in scalar ones, beside the kernel arguments the
+        // step uses, they are spilled and reloaded lane by lane every step)
+        int *rn[NL], *rs[NL], *on[NL], *os[NL], *tab[NL], *idx[NL];
+        float* rI[NL];
     };
+
+    static __device__ __forceinline__ void record_ptrs(const CoreFwdArgs& a, int b, Lane& L) {
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            const FwdLayer& y = a.ly[l];
+            const size_t r0 = (size_t)b * a.cap;
+            L.rn[l] = y.rec_n + r0;
+            L.rs[l] = y.rec_s + r0;
+            L.rI[l] = y.rec_I + r0;
+            L.on[l] = y.out_neuron + r0;
+            L.os[l] = y.out_step + r0;
+            L.tab[l] = y.steptab + (size_t)b * a.T * SNN_STEP_ROW;
+            L.idx[l] = y.rec_idx + (size_t)b * (a.T + 1);
+            asm volatile("" : "+v"(L.rn[l]), "+v"(L.rs[l]), "+v"(L.rI[l]), "+v"(L.on[l]), "+v"(L.os[l]),
+                              "+v"(L.tab[l]), "+v"(L.idx[l]));
+        }
+    }
 
     template <typename Ptr>
     static __device__ __forceinline__ Ptr ring_col(const CoreFwdArgs& a, int b, int l, int pp, int col) {
@@ -375,18 +397,16 @@ struct FwdCore {
 
     // Spike records of step n (neuron, step, I- of this step), the step
     // table row, the overflow flag.
-    static __device__ __forceinline__ void records(const CoreFwdArgs& a, int b, int g, int tid, int j, int n,
+    static __device__ __forceinline__ void records(const CoreFwdArgs& a, int g, int tid, int j, int n,
                                                    const bool (&spk)[NL], const int (&rank)[NL],
                                                    const int (&cnt0)[NL], const int (&tot)[NL], Lane& L) {
-        const int T = a.T;
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
-            const FwdLayer& y = a.ly[l];
-            int* row = y.steptab + ((size_t)b * T + n) * SNN_STEP_ROW;
+            int* row = L.tab[l] + n * SNN_STEP_ROW;
             if (tid == 0 && g == 0) {
                 // internal record indices never pass the capacity (the
                 // caller's count stays exact)
-                y.rec_idx[(size_t)b * (T + 1) + n] = min(cnt0[l], a.cap);
+                L.idx[l][n] = min(cnt0[l], a.cap);
                 row[0] = tot[l];
                 row[1] = min(cnt0[l], a.cap);
             }
@@ -395,12 +415,11 @@ struct FwdCore {
                 if (rank[l] < SNN_STEP_IDS) row[2 + rank[l]] = j;
                 const int pos = cnt0[l] + rank[l];
                 if (pos < a.cap) {
-                    const size_t r = (size_t)b * a.cap + pos;
-                    y.rec_n[r] = j;
-                    y.rec_s[r] = n;
-                    y.rec_I[r] = L.I[l];
-                    y.out_step[r] = n;
-                    y.out_neuron[r] = j;
+                    L.rn[l][pos] = j;
+                    L.rs[l][pos] = n;
+                    L.rI[l][pos] = L.I[l];
+                    L.os[l][pos] = n;
+                    L.on[l][pos] = j;
                 }
             }
             if (tid == 0 && cnt0[l] + tot[l] > a.cap) a.st->overflow = 1;
@@ -437,7 +456,7 @@ struct FwdCore {
             scatter_rest(a, b, l, tid, tid, n, mw[l], masks + (size_t)(par * NL + l) * NW, 0, tot[l]);
         N.ain = a.A_in[((size_t)b * T + min(n + 1, T - 1)) * a.n1 + min(tid, a.n1 - 1)];
 
-        records(a, b, 0, tid, tid, n, spk, rank, cnt0, tot, L);
+        records(a, 0, tid, tid, n, spk, rank, cnt0, tot, L);
         arrivals(a, b, tid, tid, n, P, L);
     }
 
@@ -514,7 +533,7 @@ struct FwdCore {
         unsigned long long mw[NL][NWM];
         int tot[NL], rank[NL], cnt0[NL];
         counts(a, masks + (size_t)par * NL * NW, g, mine, mw, tot, rank, cnt0, L);
-        records(a, b, g, lane, j, n, spk, rank, cnt0, tot, L);
+        records(a, g, lane, j, n, spk, rank, cnt0, tot, L);
         lds_barrier();                                   // every ring holds step n's arrivals
         arrivals(a, b, lane, j, n, P, L);
         return true;
@@ -574,6 +593,7 @@ struct FwdCore {
             L.cnt[l] = 0;
             L.own[l] = 0;
         }
+        record_ptrs(a, b, L);
         Pre A, B;
         A.ain = a.A_in[(size_t)b * a.T * a.n1 + min(j, a.n1 - 1)];
         int n = 0;
@@ -632,6 +652,7 @@ struct FwdCore {
             L.cnt[l] = 0;
             L.own[l] = 0;
         }
+        record_ptrs(a, b, L);
         if constexpr (RO) {
             if ((tid >> 6) == a.NW) {
                 // the readout wave: its ring's columns, rows 0 .. S (row S:
