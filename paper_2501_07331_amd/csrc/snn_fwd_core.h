@@ -61,9 +61,14 @@ struct FwdCore {
         // step uses, they are spilled and reloaded lane by lane every step)
         int *rn[NL], *rs[NL], *on[NL], *os[NL], *tab[NL], *idx[NL];
         float* rI[NL];
+        const float* ain;                     // this lane's column of the input arrivals [T][n_1]
+        DevStatus* st;
     };
 
-    static __device__ __forceinline__ void record_ptrs(const CoreFwdArgs& a, int b, Lane& L) {
+    static __device__ __forceinline__ void record_ptrs(const CoreFwdArgs& a, int b, int j, Lane& L) {
+        L.ain = a.A_in + (size_t)b * a.T * a.n1 + min(j, a.n1 - 1);
+        L.st = a.st;
+        asm volatile("" : "+v"(L.ain), "+v"(L.st));
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
             const FwdLayer& y = a.ly[l];
@@ -422,7 +427,7 @@ struct FwdCore {
                     L.on[l][pos] = j;
                 }
             }
-            if (tid == 0 && cnt0[l] + tot[l] > a.cap) a.st->overflow = 1;
+            if (tid == 0 && cnt0[l] + tot[l] > a.cap) L.st->overflow = 1;
         }
     }
 
@@ -454,7 +459,7 @@ struct FwdCore {
 #pragma unroll
         for (int l = 0; l < NL; ++l)
             scatter_rest(a, b, l, tid, tid, n, mw[l], masks + (size_t)(par * NL + l) * NW, 0, tot[l]);
-        N.ain = a.A_in[((size_t)b * T + min(n + 1, T - 1)) * a.n1 + min(tid, a.n1 - 1)];
+        N.ain = L.ain[min(n + 1, T - 1) * a.n1];
 
         records(a, 0, tid, tid, n, spk, rank, cnt0, tot, L);
         arrivals(a, b, tid, tid, n, P, L);
@@ -462,7 +467,7 @@ struct FwdCore {
 
     static __device__ __forceinline__ void run_steps(const CoreFwdArgs& a, int b, int tid, Lane& L) {
         Pre A, B;
-        A.ain = a.A_in[(size_t)b * a.T * a.n1 + min(tid, a.n1 - 1)];
+        A.ain = L.ain[0];
         int n = 0;
         for (; n + 1 < a.T; n += 2) {
             step(a, b, tid, n, A, B, L);
@@ -526,7 +531,7 @@ struct FwdCore {
         // the next step's input arrival goes out right after the exchange,
         // so that no load of this wave is in flight when the next exchange
         // waits for its own (a wait covers every older access)
-        N.ain = a.A_in[((size_t)b * T + min(n + 1, T - 1)) * a.n1 + min(j, a.n1 - 1)];
+        N.ain = L.ain[min(n + 1, T - 1) * a.n1];
         if (!ok && lane == 0) *cl_flag(a) = 1;
         lds_barrier();                                   // the masks of step n are in
         if (!ok) return false;
@@ -593,9 +598,9 @@ struct FwdCore {
             L.cnt[l] = 0;
             L.own[l] = 0;
         }
-        record_ptrs(a, b, L);
+        record_ptrs(a, b, j, L);
         Pre A, B;
-        A.ain = a.A_in[(size_t)b * a.T * a.n1 + min(j, a.n1 - 1)];
+        A.ain = L.ain[0];
         int n = 0;
         for (; n + 1 < a.T; n += 2) {
             if (!step_cl(a, b, c, g, lane, n, A, B, L)) return;
@@ -652,7 +657,7 @@ struct FwdCore {
             L.cnt[l] = 0;
             L.own[l] = 0;
         }
-        record_ptrs(a, b, L);
+        record_ptrs(a, b, tid, L);
         if constexpr (RO) {
             if ((tid >> 6) == a.NW) {
                 // the readout wave: its ring's columns, rows 0 .. S (row S:
