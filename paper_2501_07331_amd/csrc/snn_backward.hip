@@ -191,17 +191,41 @@ struct BwdCore {
     static constexpr int ROW4 = (2 + KP + 3) / 4;      // int4 loads of a spike-table row
     typedef BwdState<NL, KP, NPA> State;
 
+    // The sample's arrays: uniform, but held in vector registers (in scalar
+    // ones, beside the kernel arguments the step uses, they are spilled and
+    // reloaded lane by lane every step).
+    struct Ptrs {
+        double2* tr[NL];               // this lane's trajectory column (stride lif_total)
+        const int* tab[NL];            // step table [T][SNN_STEP_ROW]
+        const float* recI[NL];         // records [cap]
+        const double* A2[NL];          // [cap], or NULL
+        const int* recn[NL];
+    };
+
+    static __device__ __forceinline__ void make_ptrs(const CoreBwdArgs& a, int b, int tid, Ptrs& P) {
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            const BwdLayer& y = a.ly[l];
+            const size_t r0 = (size_t)b * a.cap;
+            P.tr[l] = a.traj + (size_t)b * a.T * a.lif_total + y.lif_off + tid;
+            P.tab[l] = y.steptab + (size_t)b * a.T * SNN_STEP_ROW;
+            P.recI[l] = y.recI + r0;
+            P.A2[l] = y.A2 ? y.A2 + r0 : nullptr;
+            P.recn[l] = y.recn + r0;
+            asm volatile("" : "+v"(P.tr[l]), "+v"(P.tab[l]), "+v"(P.recI[l]), "+v"(P.A2[l]), "+v"(P.recn[l]));
+        }
+    }
+
     // Spike-table row of step x: count, record index, first KP neurons.  The
     // row is the same for every lane, but its address carries a per-lane zero
     // that the compiler cannot see through: a load it knows to be uniform has
     // its result moved to scalar registers right where it lands, which would
     // wait for it there; these values are made scalar a step later, at use.
-    static __device__ __forceinline__ void load_row(const BwdLayer& y, int b, int T, int x, int& cnt,
-                                                    int& ri, int (&ids)[KP]) {
+    static __device__ __forceinline__ void load_row(const int* tab, int x, int& cnt, int& ri,
+                                                    int (&ids)[KP]) {
         int zero;
         asm volatile("v_mov_b32 %0, 0" : "=v"(zero));
-        const int4* rp =
-            reinterpret_cast<const int4*>(y.steptab + ((size_t)b * T + x) * SNN_STEP_ROW) + zero;
+        const int4* rp = reinterpret_cast<const int4*>(tab + x * SNN_STEP_ROW) + zero;
         int v[ROW4 * 4];
 #pragma unroll
         for (int k = 0; k < ROW4; ++k) {
@@ -221,10 +245,10 @@ struct BwdCore {
     // (valid for q < cnt; record index of ids[0] is ri + r0).  Only the
     // chunks of 4 that hold spikes are loaded; ids are made uniform so that
     // a row's address is scalar and the lane adds its column.
-    static __device__ __forceinline__ void load_step(const CoreBwdArgs& a, int b, int tid, int l,
-                                                     int ri, int cnt, const int (&ids)[KP], int r0,
-                                                     uint2 (&ws)[NPA][KP], int& mine, float& I,
-                                                     double& A2) {
+    static __device__ __forceinline__ void load_step(const CoreBwdArgs& a, const float* recI,
+                                                     const double* A2p, int tid, int l, int ri, int cnt,
+                                                     const int (&ids)[KP], int r0, uint2 (&ws)[NPA][KP],
+                                                     int& mine, float& I, double& A2) {
         const BwdLayer& y = a.ly[l];
         // (the ids stay in vector registers: held in scalar ones, the 16 ids
         // and their row offsets overflow the scalar register file).  Entries
@@ -259,24 +283,24 @@ struct BwdCore {
                 if (q < cnt && idc[q] == tid) mine = q + 1;
         }
         if (mine) {
-            const size_t r = (size_t)b * a.cap + (ri + r0 + mine - 1);
-            I = y.recI[r];
-            A2 = y.A2 ? y.A2[r] : 0.0;
+            const int r = ri + r0 + mine - 1;
+            I = recI[r];
+            A2 = A2p ? A2p[r] : 0.0;
         }
     }
 
     // Issue the loads of B from A (processing step n).
-    static __device__ __forceinline__ void advance(const CoreBwdArgs& a, int b, int tid, int n,
+    static __device__ __forceinline__ void advance(const CoreBwdArgs& a, const Ptrs& P, int tid, int n,
                                                    const State& A, State& B) {
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
-            load_row(a.ly[l], b, a.T, max(n - 2, 0), B.cnt2[l], B.ri2[l], B.id2[l]);
+            load_row(P.tab[l], max(n - 2, 0), B.cnt2[l], B.ri2[l], B.id2[l]);
             B.cnt3[l] = __builtin_amdgcn_readfirstlane(A.cnt2[l]);
             B.ri3[l] = __builtin_amdgcn_readfirstlane(A.ri2[l]);
 #pragma unroll
             for (int q = 0; q < KP; ++q) B.id3[l][q] = A.id2[l][q];
-            load_step(a, b, tid, l, B.ri3[l], B.cnt3[l], A.id2[l], 0, B.ws[l], B.mine[l], B.I[l],
-                      B.A2[l]);
+            load_step(a, P.recI[l], P.A2[l], tid, l, B.ri3[l], B.cnt3[l], A.id2[l], 0, B.ws[l], B.mine[l],
+                      B.I[l], B.A2[l]);
         }
     }
 
@@ -392,7 +416,7 @@ struct BwdCore {
     };
 
     // One reverse-time step n with the loads of A, issuing those of B.
-    static __device__ __forceinline__ void step(const CoreBwdArgs& a, int b, int tid, int n,
+    static __device__ __forceinline__ void step(const CoreBwdArgs& a, const Ptrs& P, int b, int tid, int n,
                                                 const State& A, State& B, Lane& L) {
         const int T = a.T, LT = a.lif_total;
         double* part = reinterpret_cast<double*>(smem + a.part_off);   // [2][NL][KP][4 NW]
@@ -406,7 +430,7 @@ struct BwdCore {
         // the loads issued one step ago (A) have landed: wait for them once,
         // here, so that no later use waits for this step's loads
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
-        advance(a, b, tid, n, A, B);
+        advance(a, P, tid, n, A, B);
 
         // ---- adjoint free dynamics, trajectory, adjoint ring
 #pragma unroll
@@ -419,7 +443,7 @@ struct BwdCore {
                 L.lv[l] = __dmul_rn(a.alpha, v);
             }
             const double d = __dsub_rn(L.lI[l], L.lv[l]);
-            a.traj[((size_t)b * T + n) * LT + y.lif_off + tid] = make_double2(L.lI[l], d);
+            P.tr[l][(size_t)n * LT] = make_double2(L.lI[l], d);
             if (y.ring_lds == -2) continue;
             const int n_own = n % y.S;
             if (RL)
@@ -464,10 +488,9 @@ struct BwdCore {
                 int ids[KP];
                 const int capm = max(a.cap - 1, 0);
 #pragma unroll
-                for (int q = 0; q < KP; ++q)
-                    ids[q] = y.recn[(size_t)b * a.cap + min(max(A.ri3[l] + r * KP + q, 0), capm)];
+                for (int q = 0; q < KP; ++q) ids[q] = P.recn[l][min(max(A.ri3[l] + r * KP + q, 0), capm)];
                 uint2 ws[NPA][KP];
-                load_step(a, b, tid, l, A.ri3[l], cnt, ids, r * KP, ws, mine[l], I[l], A2[l]);
+                load_step(a, P.recI[l], P.A2[l], tid, l, A.ri3[l], cnt, ids, r * KP, ws, mine[l], I[l], A2[l]);
                 double* part_l = part + (size_t)(pb * NL + l) * KP * (4 * a.NW);
                 if (NP > 0) gather(a, b, tid, n, nm[l], l, cnt, ids, ws, part_l);
             }
@@ -492,23 +515,25 @@ struct BwdCore {
         }
         L.deg = 0;
         L.rnd = 0;
+        Ptrs P;
+        make_ptrs(a, b, tid, P);
         State A, B;
         // step T - 1's data and step T - 2's table row, before the loop
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
-            load_row(a.ly[l], b, T, T - 1, A.cnt3[l], A.ri3[l], A.id3[l]);
-            load_row(a.ly[l], b, T, max(T - 2, 0), A.cnt2[l], A.ri2[l], A.id2[l]);
+            load_row(P.tab[l], T - 1, A.cnt3[l], A.ri3[l], A.id3[l]);
+            load_row(P.tab[l], max(T - 2, 0), A.cnt2[l], A.ri2[l], A.id2[l]);
             A.cnt3[l] = __builtin_amdgcn_readfirstlane(A.cnt3[l]);
             A.ri3[l] = __builtin_amdgcn_readfirstlane(A.ri3[l]);
-            load_step(a, b, tid, l, A.ri3[l], A.cnt3[l], A.id3[l], 0, A.ws[l], A.mine[l], A.I[l],
-                      A.A2[l]);
+            load_step(a, P.recI[l], P.A2[l], tid, l, A.ri3[l], A.cnt3[l], A.id3[l], 0, A.ws[l], A.mine[l],
+                      A.I[l], A.A2[l]);
         }
         int n = T - 1;
         for (; n >= 1; n -= 2) {
-            step(a, b, tid, n, A, B, L);
-            step(a, b, tid, n - 1, B, A, L);
+            step(a, P, b, tid, n, A, B, L);
+            step(a, P, b, tid, n - 1, B, A, L);
         }
-        if (n == 0) step(a, b, tid, 0, A, B, L);
+        if (n == 0) step(a, P, b, tid, 0, A, B, L);
         if (L.deg) atomicAdd(&a.st->degenerate, L.deg);
     }
 };
