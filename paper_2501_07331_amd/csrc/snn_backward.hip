@@ -594,21 +594,47 @@ struct BwdCluster {
         asm volatile("" ::: "memory");
     }
 
+    // The sample's arrays: uniform, but held in vector registers (in scalar
+    // ones, beside the kernel arguments, they are spilled and reloaded lane
+    // by lane every step).
+    struct Ptrs {
+        const int* tab[NL];            // step table [T][SNN_STEP_ROW]
+        const int* recn[NL];           // records [cap]
+        const float* recI[NL];
+        const double* A2[NL];          // or NULL
+        double2* tr[NL];               // this lane's trajectory column (stride lif_total)
+    };
+
+    static __device__ __forceinline__ void make_ptrs(const CoreBwdArgs& a, int b, int j, Ptrs& P) {
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+            const BwdLayer& y = a.ly[l];
+            const size_t r0 = (size_t)b * a.cap;
+            P.tab[l] = y.steptab + (size_t)b * a.T * SNN_STEP_ROW;
+            P.recn[l] = y.recn + r0;
+            P.recI[l] = y.recI + r0;
+            P.A2[l] = y.A2 ? y.A2 + r0 : nullptr;
+            P.tr[l] = a.traj + (size_t)b * a.T * a.lif_total + y.lif_off + j;
+            asm volatile("" : "+v"(P.tab[l]), "+v"(P.recn[l]), "+v"(P.recI[l]), "+v"(P.A2[l]), "+v"(P.tr[l]));
+        }
+    }
+
     // Spike count and first record index of layer l at step x (a per-lane
     // zero in the address keeps the compiler from making the load scalar and
     // waiting for it where it lands).
-    static __device__ __forceinline__ int2 load_cr(const CoreBwdArgs& a, int b, int l, int x) {
+    static __device__ __forceinline__ int2 load_cr(const Ptrs& P, int l, int x) {
         int zero;
         asm volatile("v_mov_b32 %0, 0" : "=v"(zero));
-        return reinterpret_cast<const int2*>(a.ly[l].steptab + ((size_t)b * a.T + x) * SNN_STEP_ROW)[zero];
+        return reinterpret_cast<const int2*>(P.tab[l] + x * SNN_STEP_ROW)[zero];
     }
 
     // Lane q: the neuron of spike q0 + q of a step with records [ri, ri +
     // cnt) (clamped into them; -1 for a step without spikes).
-    static __device__ __forceinline__ int load_id(const CoreBwdArgs& a, int b, int l, int ri, int cnt, int q0) {
+    static __device__ __forceinline__ int load_id(const CoreBwdArgs& a, const Ptrs& P, int l, int ri, int cnt,
+                                                  int q0) {
         const int q = min(q0 + (int)(threadIdx.x & 63), max(cnt - 1, 0));
         const int idx = min(max(ri + q, 0), max(a.cap - 1, 0));
-        return (cnt > 0 && a.cap > 0) ? a.ly[l].recn[(size_t)b * a.cap + idx] : -1;
+        return (cnt > 0 && a.cap > 0) ? P.recn[l][idx] : -1;
     }
 
     // Weights and slots of spikes q < KC (ids in lanes q of `ids`) for post
@@ -650,8 +676,8 @@ struct BwdCluster {
 
     // Step n with this step's weights wc (landed); issues step n - 1's into
     // wn.  false: the cluster gave up (the flag was raised).
-    static __device__ __forceinline__ bool gstep(const CoreBwdArgs& a, int b, int g, int r, int l, int pp,
-                                                 int n, GState& st, uint2 (&wc)[KC], uint2 (&wn)[KC]) {
+    static __device__ __forceinline__ bool gstep(const CoreBwdArgs& a, const Ptrs& P, int g, int r, int l,
+                                                 int pp, int n, GState& st, uint2 (&wc)[KC], uint2 (&wn)[KC]) {
         const int lane = threadIdx.x & 63, j = g * 64 + lane, T = a.T;
         const BwdLayer& y = a.ly[l];
         const int nq = y.nq[pp], S = y.qS[pp];
@@ -673,7 +699,7 @@ struct BwdCluster {
             const int q0 = rd * KC, nr = min(max(cnt - q0, 0), KC);
             if (rd > 0 && nr > 0) {
                 // spikes past the prefetched ones: ids, then weights, now
-                const int idr = load_id(a, b, l, ri, cnt, q0);
+                const int idr = load_id(a, P, l, ri, cnt, q0);
                 load_ws(a, l, pp, j, idr, wc);
             }
             // (unrolled over the KC slots, so that the weights stay in
@@ -709,12 +735,12 @@ struct BwdCluster {
         // steps ahead, ids two, weights one
         int2 c3[NL];
 #pragma unroll
-        for (int m = 0; m < NL; ++m) c3[m] = load_cr(a, b, m, max(n - 3, 0));
+        for (int m = 0; m < NL; ++m) c3[m] = load_cr(P, m, max(n - 3, 0));
         int i2 = 0;
 #pragma unroll
         for (int m = 0; m < NL; ++m)
             if (m == l)
-                i2 = load_id(a, b, l, __builtin_amdgcn_readfirstlane(st.c2[m].y),
+                i2 = load_id(a, P, l, __builtin_amdgcn_readfirstlane(st.c2[m].y),
                              __builtin_amdgcn_readfirstlane(st.c2[m].x), 0);
         if (n > 0) load_ws(a, l, pp, j, st.i1, wn);
 #pragma unroll
@@ -730,13 +756,15 @@ struct BwdCluster {
 
     static __device__ void gather_wave(const CoreBwdArgs& a, int b, int g, int r, int l, int pp) {
         const int j = g * 64 + (int)(threadIdx.x & 63), T = a.T;
+        Ptrs P;
+        make_ptrs(a, b, j, P);
         GState st;
         int2 c0[NL];
 #pragma unroll
         for (int m = 0; m < NL; ++m) {
-            c0[m] = load_cr(a, b, m, T - 1);
-            st.c1[m] = load_cr(a, b, m, max(T - 2, 0));
-            st.c2[m] = load_cr(a, b, m, max(T - 3, 0));
+            c0[m] = load_cr(P, m, T - 1);
+            st.c1[m] = load_cr(P, m, max(T - 2, 0));
+            st.c2[m] = load_cr(P, m, max(T - 3, 0));
         }
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
         int i0 = 0;
@@ -745,8 +773,8 @@ struct BwdCluster {
             st.cn[m] = __builtin_amdgcn_readfirstlane(c0[m].x);
             st.rn[m] = __builtin_amdgcn_readfirstlane(c0[m].y);
             if (m == l) {
-                i0 = load_id(a, b, l, st.rn[m], st.cn[m], 0);
-                st.i1 = load_id(a, b, l, __builtin_amdgcn_readfirstlane(st.c1[m].y),
+                i0 = load_id(a, P, l, st.rn[m], st.cn[m], 0);
+                st.i1 = load_id(a, P, l, __builtin_amdgcn_readfirstlane(st.c1[m].y),
                                 __builtin_amdgcn_readfirstlane(st.c1[m].x), 0);
             }
         }
@@ -755,10 +783,10 @@ struct BwdCluster {
         load_ws(a, l, pp, j, i0, wa);
         int n = T - 1;
         for (; n >= 1; n -= 2) {
-            if (!gstep(a, b, g, r, l, pp, n, st, wa, wb)) return;
-            if (!gstep(a, b, g, r, l, pp, n - 1, st, wb, wa)) return;
+            if (!gstep(a, P, g, r, l, pp, n, st, wa, wb)) return;
+            if (!gstep(a, P, g, r, l, pp, n - 1, st, wb, wa)) return;
         }
-        if (n == 0) gstep(a, b, g, r, l, pp, 0, st, wa, wb);
+        if (n == 0) gstep(a, P, g, r, l, pp, 0, st, wa, wb);
     }
 
     // ---- the neuron wave
@@ -865,13 +893,15 @@ struct BwdCluster {
         }
         int* pos = positions(a);
         const double* tot = totals(a);
+        Ptrs P;
+        make_ptrs(a, b, j, P);
         // pipeline: (count, first record) of steps n, n - 1; ids of n
         int2 c0[NL], c1[NL];
         int id0[NL];
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
-            c0[l] = load_cr(a, b, l, T - 1);
-            c1[l] = load_cr(a, b, l, max(T - 2, 0));
+            c0[l] = load_cr(P, l, T - 1);
+            c1[l] = load_cr(P, l, max(T - 2, 0));
         }
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
         int cnt0[NL], ri0[NL];
@@ -879,7 +909,7 @@ struct BwdCluster {
         for (int l = 0; l < NL; ++l) {
             cnt0[l] = __builtin_amdgcn_readfirstlane(c0[l].x);
             ri0[l] = __builtin_amdgcn_readfirstlane(c0[l].y);
-            id0[l] = load_id(a, b, l, ri0[l], cnt0[l], 0);
+            id0[l] = load_id(a, P, l, ri0[l], cnt0[l], 0);
         }
         for (int n = T - 1; n >= 0; --n) {
             __builtin_amdgcn_s_waitcnt(kWaitVm0);
@@ -888,8 +918,8 @@ struct BwdCluster {
             for (int l = 0; l < NL; ++l) {
                 cnt1[l] = __builtin_amdgcn_readfirstlane(c1[l].x);
                 ri1[l] = __builtin_amdgcn_readfirstlane(c1[l].y);
-                c1[l] = load_cr(a, b, l, max(n - 2, 0));
-                id1[l] = load_id(a, b, l, ri1[l], cnt1[l], 0);
+                c1[l] = load_cr(P, l, max(n - 2, 0));
+                id1[l] = load_id(a, P, l, ri1[l], cnt1[l], 0);
             }
             // ---- adjoint free dynamics, trajectory, adjoint ring
 #pragma unroll
@@ -902,7 +932,7 @@ struct BwdCluster {
                     lv[l] = __dmul_rn(a.alpha, v);
                 }
                 const double d = __dsub_rn(lI[l], lv[l]);
-                a.traj[((size_t)b * T + n) * LT + y.lif_off + j] = make_double2(lI[l], d);
+                P.tr[l][(size_t)n * LT] = make_double2(lI[l], d);
                 if (y.ring_lds >= 0) ((lds_f64*)(smem + y.ring_lds))[(n % y.S) * 64 + lane] = d;
             }
             const int rounds = rounds_of(cnt0);
@@ -919,7 +949,7 @@ struct BwdCluster {
                     nr[l] = min(max(cnt0[l] - q0, 0), KC);
                     off[l] = K;
                     K += nr[l];
-                    const int id = (rd == 0) ? id0[l] : load_id(a, b, l, ri0[l], cnt0[l], q0);
+                    const int id = (rd == 0) ? id0[l] : load_id(a, P, l, ri0[l], cnt0[l], q0);
                     pos[l * 64 + lane] = 0;
                     const int o = id - g * 64;
                     if ((int)lane < nr[l] && o >= 0 && o < 64) pos[l * 64 + o] = lane + 1;
@@ -931,9 +961,9 @@ struct BwdCluster {
                     I[l] = 0.0f;
                     A2[l] = 0.0;
                     if (mine[l]) {
-                        const size_t rr = (size_t)b * a.cap + (ri0[l] + q0 + mine[l] - 1);
-                        I[l] = a.ly[l].recI[rr];
-                        A2[l] = a.ly[l].A2 ? a.ly[l].A2[rr] : 0.0;
+                        const int rr = ri0[l] + q0 + mine[l] - 1;
+                        I[l] = P.recI[l][rr];
+                        A2[l] = P.A2[l] ? P.A2[l][rr] : 0.0;
                     }
                 }
                 lds_barrier();                                   // ring rows in, shares free
