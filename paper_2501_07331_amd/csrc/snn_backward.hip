@@ -4,9 +4,10 @@
 // delayed postsynaptic adjoints and the weight and delay gradients).
 //
 //  readout_adjoint  one workgroup per sample: the LI adjoints over reverse time
-//                   (loss source only), their trajectories, then the readout
-//                   part of the jump sum of every spike of the feeding layer,
-//                   computed in parallel over the spikes.
+//                   (loss source only; a linear recursion, run in chunks of
+//                   steps in three passes), their trajectories, then the
+//                   readout part of the jump sum of every spike of the
+//                   feeding layer, computed in parallel over the spikes.
 //  backward_core    one workgroup per sample runs the LIF adjoints in reverse
 //                   time.  The spikes of every step are known from the
 //                   forward's per-step masks, so the weights and slots of a
@@ -14,12 +15,14 @@
 //                   loaded one step ahead; the per-step chain is then LDS and
 //                   ALU work only: free dynamics, trajectory row, adjoint
 //                   ring, delayed postsynaptic sums, one barrier, jumps.
-//  group            spikes of every sample grouped by presynaptic neuron.
+//  group            spikes of every sample grouped by presynaptic neuron
+//                   (counting sort and per-neuron sort in LDS).
 //  gradients        workgroup = (post layer, block of J posts, block of
 //                   samples): lanes over the presynaptic neurons of every
 //                   projection into the layer; per sample the J post
-//                   trajectories are staged in LDS and each lane sums, over
-//                   its spikes in step order, lambda_I and lambda_I -
+//                   trajectories, the spike-list offsets and the spike steps
+//                   are staged in LDS by direct loads, and each lane sums,
+//                   over its spikes in step order, lambda_I and lambda_I -
 //                   lambda_V at the delayed arrivals.  Sample blocks are
 //                   reduced in a fixed order: no atomics, deterministic.
 //
