@@ -1127,7 +1127,6 @@ __global__ void __launch_bounds__(1024) group_kernel(GroupArgs a) {
 // Workgroups come in units of four J-post blocks that share lines of the
 // [B][T][N] trajectories; a unit's four blocks have indices 8 apart, so with
 // round-robin dispatch over the 8 XCDs they run on one XCD and share its L2.
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 // n dwords from src to dst in LDS (both 4-byte aligned) as direct loads into
 // LDS: wave w of nw takes the 64-dword chunks w, w + nw, ...; the caller

@@ -29,6 +29,19 @@ typedef __attribute__((address_space(1))) float global_f32;
 typedef __attribute__((address_space(3))) float lds_f32;
 typedef __attribute__((address_space(1))) double global_f64;
 typedef __attribute__((address_space(3))) double lds_f64;
+// destination of a direct load into LDS (wave-uniform base; lane k's data
+// lands at base + k * size)
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+// A device-memory pointer typed as such.  Pointers that a kernel keeps in
+// vector registers (made opaque by an empty asm) need it: a generic pointer
+// there loses its address space, and its accesses become flat ones, which
+// also count on the LDS counter, so that every later wait for an LDS access
+// waits for them too.
+template <typename T>
+using gptr = __attribute__((address_space(1))) T*;
+// two doubles as one 16-byte access (a plain vector type: HIP's double2
+// has no assignment into an address-space-qualified object)
+typedef double dvec2 __attribute__((ext_vector_type(2)));
 
 // x of the lane given by the DPP control CTRL (within 16-lane rows), fp64 as
 // two 32-bit moves.
@@ -159,6 +172,8 @@ __device__ __forceinline__ void word_ids(const unsigned long long (&m)[NWM],
 
 // s_waitcnt vmcnt(0), expcnt and lgkmcnt left at their maximum (gfx9 encoding)
 constexpr int kWaitVm0 = 0x0F70;
+// s_waitcnt vmcnt(k), 0 <= k < 64 (bits 3:0 and 15:14), the others at their maximum
+constexpr int wait_vm(int k) { return kWaitVm0 | (k & 15) | ((k >> 4) << 14); }
 
 // ------------------------------------------------------------------ cluster exchange
 
