@@ -375,15 +375,11 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
             if (t.pre[p] == l && t.kind[t.post[p]] == SNN_LIF) ++k;
         net->cl_np = std::max(net->cl_np, k);
     }
-    // forward core: with at most 256 core threads the input-arrival FIFO
-    // [SNN_PF_ROWS][SNN_PF_COLS] first, the delay rings [S+1][n_post] of the
-    // LIF->LIF projections (row S: dummy), all in LDS or all in HBM, then the
-    // ballot masks [3][NL][NW]
+    // forward core: the delay rings [S+1][n_post] of the LIF->LIF projections
+    // (row S: dummy), all in LDS or all in HBM, then the ballot masks [3][NL][NW]
     {
         const size_t masks = align16((size_t)3 * std::max(t.n_lif, 1) * nwaves * sizeof(unsigned long long));
-        const size_t fifo =
-            net->core_threads <= SNN_PF_COLS ? (size_t)SNN_PF_ROWS * SNN_PF_COLS * sizeof(float) : 0;
-        size_t used = fifo;
+        size_t used = 0;
         for (int p = 0; p < t.P; ++p) {
             if (t.pre[p] == 0 || t.kind[t.post[p]] != SNN_LIF) continue;
             t.fring[p] = (int)(used / sizeof(float));
@@ -391,7 +387,7 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
         }
         const bool rings_lds = !(hbm || used + masks > kLds);
         if (!rings_lds) {
-            used = fifo;
+            used = 0;
             for (int p = 0; p < t.P; ++p) t.fring[p] = -1;
         }
         net->mask_off = (int)align16(used);
@@ -928,11 +924,8 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
         if (net->cl_f)
             TIMED(net, K_CORE, launch_forward_clusters(net, a, s));
         else
-            TIMED(net, K_CORE,
-                  launch_forward_core(a, t.n_lif,
-                                      net->core_threads + (net->ro_fused ? 64 : 0) +
-                                          (net->core_threads <= SNN_PF_COLS ? 64 : 0),
-                                      net->lds_core_f, s));
+            TIMED(net, K_CORE, launch_forward_core(a, t.n_lif, net->core_threads + (net->ro_fused ? 64 : 0),
+                                                   net->lds_core_f, s));
     }
     if (net->reg_on) {
         RegArgs ra{};

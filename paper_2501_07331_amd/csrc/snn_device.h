@@ -39,9 +39,6 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 // waits for them too.
 template <typename T>
 using gptr = __attribute__((address_space(1))) T*;
-// two doubles as one 16-byte access (a plain vector type: HIP's double2
-// has no assignment into an address-space-qualified object)
-typedef double dvec2 __attribute__((ext_vector_type(2)));
 
 // x of the lane given by the DPP control CTRL (within 16-lane rows), fp64 as
 // two 32-bit moves.
@@ -172,8 +169,6 @@ __device__ __forceinline__ void word_ids(const unsigned long long (&m)[NWM],
 
 // s_waitcnt vmcnt(0), expcnt and lgkmcnt left at their maximum (gfx9 encoding)
 constexpr int kWaitVm0 = 0x0F70;
-// s_waitcnt vmcnt(k), 0 <= k < 64 (bits 3:0 and 15:14), the others at their maximum
-constexpr int wait_vm(int k) { return kWaitVm0 | (k & 15) | ((k >> 4) << 14); }
 
 // ------------------------------------------------------------------ cluster exchange
 

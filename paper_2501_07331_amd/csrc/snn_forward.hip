@@ -617,22 +617,11 @@ hipError_t set_forward_lds_limits(size_t bytes, int* bad) {
 
 hipError_t launch_forward_core(const CoreFwdArgs& a, int n_lif, int threads, size_t lds,
                                hipStream_t s) {
-    // the core waves, one more for a fused readout and, with cores of up to
-    // 256 threads, one more for the input-arrival FIFO at LDS offset 0
+    // the core waves, and one more for a fused readout (cores of up to 256 threads)
     const int core = 64 * a.NW;
-    const bool pf = core <= SNN_PF_COLS;
-    const int fifo = SNN_PF_ROWS * SNN_PF_COLS * 4;
-    if (n_lif < 1 || n_lif > SNN_MAX_LIF || threads != core + (a.ro_C > 0 ? 64 : 0) + (pf ? 64 : 0) ||
+    if (n_lif < 1 || n_lif > SNN_MAX_LIF || threads != core + (a.ro_C > 0 ? 64 : 0) ||
         (a.ro_C > 0 && (core > 256 || a.ro_C > 64 || a.ro_feed < 0 || a.ro_feed >= n_lif)))
         return hipErrorInvalidValue;
-    if (pf) {
-        bool ok = a.n1 >= 1 && a.n1 <= SNN_PF_COLS && lds >= (size_t)fifo && a.mask_off >= fifo &&
-                  (a.ro_C == 0 || a.ro_off >= fifo);
-        for (int l = 0; l < n_lif; ++l)
-            for (int pp = 0; pp < a.ly[l].npost; ++pp)
-                ok = ok && (a.ly[l].ring_lds[pp] < 0 || a.ly[l].ring_lds[pp] >= fifo / 4);
-        if (!ok) return hipErrorInvalidValue;
-    }
     int np = 0;
     bool rl = true;
     for (int l = 0; l < n_lif; ++l) {

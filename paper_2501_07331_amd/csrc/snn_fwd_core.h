@@ -27,14 +27,12 @@
 // of a step loaded a step ahead, was slower: 1.41 against 1.33 ms on the
 // 700-256rec-20 step.)
 //
-// With at most 256 core threads, one more wave stages the input
-// projection's arrivals in an LDS FIFO several steps ahead (pf_run); the
-// core reads row n of it instead of loading its own arrival a step ahead.
-//
 // The sample's record arrays are held in vector registers as device-memory
 // pointers (gptr): as generic pointers their stores were flat ones, which
-// count on the LDS counter too, so the next LDS wait of the step waited for
-// their write acknowledgements (1.23 against 1.19 ms with the FIFO).
+// count on the LDS counter too, so that the next LDS wait of the step waited
+// for their write acknowledgements (1.23 against 1.16 ms).  (One more wave
+// that staged the input arrivals in an LDS FIFO several steps ahead, so that
+// the core never waited for their loads, was slower: 1.18 ms.)
 #pragma once
 
 #include <type_traits>
@@ -55,15 +53,8 @@ struct FwdCore {
     // so does a cluster's step, whose weight loads all go out together (a
     // lone wave has the registers)
     static constexpr int KI = CL ? (NL <= 2 ? 32 : 16) : (RL || MAXT <= 256) ? KB : 16;
-    // the input-arrival wave (workgroups of at most 256 core threads): an
-    // LDS FIFO of kPF rows of SNN_PF_COLS floats at LDS offset 0, kPR direct
-    // loads a row
-    static constexpr bool PF = !CL && MAXT <= SNN_PF_COLS;
-    static constexpr int kPF = SNN_PF_ROWS, kPR = SNN_PF_COLS / 64;
-    static_assert(kPR * (kPF - 2) < 64, "the FIFO's loads in flight fit the vector memory counter");
 
-    // Load in flight for the next step: its input arrival (cores without
-    // the input-arrival wave).
+    // Load in flight for the next step: its input arrival.
     struct Pre {
         float ain;
     };
@@ -193,15 +184,13 @@ struct FwdCore {
         }
     }
 
-    // All spikes of layer l at step e (mask words m), in chunks of KI with
-    // their weights loaded now.  (Finding a chunk's ids by scalar bit scans
-    // instead of lane by lane took fewer vector instructions but more scalar
-    // branches and spills, and was slower: 1.34 against 1.19 ms.)
+    // All spikes of layer l at step e (mask words m), from position `from` on,
+    // in chunks of KB with their weights loaded now.
     static __device__ __forceinline__ void scatter_rest(const CoreFwdArgs& a, int b, int l, int tid,
                                                         int j, int e, const unsigned long long (&m)[NWM],
-                                                        const unsigned long long* row, int total) {
+                                                        const unsigned long long* row, int from, int total) {
         const FwdLayer& y = a.ly[l];
-        for (int q0 = 0; q0 < total; q0 += KI) {
+        for (int q0 = from; q0 < total; q0 += KI) {
             int ids[KI];
             word_ids<NWM, KI, CL>(m, row, a.NW, q0, ids);
 #pragma unroll
@@ -387,9 +376,8 @@ struct FwdCore {
     }
 
     // Arrivals at step n: per projection into the layer, in projection order
-    // (the input projection's: FIFO row n % kPF with the input-arrival wave,
-    // else P.ain, loaded a step ahead); the lane's ring column is tid, 64
-    // wide in cluster mode.
+    // (P.ain: the input projection's, loaded a step ahead); the lane's ring
+    // column is tid, 64 wide in cluster mode.
     static __device__ __forceinline__ void arrivals(const CoreFwdArgs& a, int b, int tid, int j, int n,
                                                     const Pre& P, Lane& L) {
 #pragma unroll
@@ -402,10 +390,7 @@ struct FwdCore {
                 float add;
                 const int sl = y.in_l[e];
                 if (sl < 0) {
-                    if constexpr (PF)
-                        add = ((const lds_f32*)smem)[(n % kPF) * SNN_PF_COLS + j];
-                    else
-                        add = P.ain;
+                    add = P.ain;
                 } else {
                     const int S = y.in_S[e], n_mod = n % S;
                     RingPtr rc;
@@ -475,13 +460,13 @@ struct FwdCore {
         counts(a, masks + (size_t)par * NL * NW, wave, mine, mw, tot, rank, cnt0, L);
 
         // the input arrival loaded a step ago (P) has landed
-        if constexpr (!PF) __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
 
         // ---- this step's spikes into the rings (all delays)
 #pragma unroll
         for (int l = 0; l < NL; ++l)
-            scatter_rest(a, b, l, tid, tid, n, mw[l], masks + (size_t)(par * NL + l) * NW, tot[l]);
-        if constexpr (!PF) N.ain = L.ain[min(n + 1, T - 1) * a.n1];
+            scatter_rest(a, b, l, tid, tid, n, mw[l], masks + (size_t)(par * NL + l) * NW, 0, tot[l]);
+        N.ain = L.ain[min(n + 1, T - 1) * a.n1];
 
         records(a, 0, tid, tid, n, spk, rank, cnt0, tot, L);
         arrivals(a, b, tid, tid, n, P, L);
@@ -489,52 +474,13 @@ struct FwdCore {
 
     static __device__ __forceinline__ void run_steps(const CoreFwdArgs& a, int b, int tid, Lane& L) {
         Pre A, B;
-        A.ain = PF ? 0.0f : L.ain[0];
+        A.ain = L.ain[0];
         int n = 0;
         for (; n + 1 < a.T; n += 2) {
             step(a, b, tid, n, A, B, L);
             step(a, b, tid, n + 1, B, A, L);
         }
         if (n < a.T) step(a, b, tid, n, A, B, L);
-    }
-
-    // ---- the input-arrival wave.  A load that a core wave issues is waited
-    // for at that wave's next wait for any later access (the vector memory
-    // counter retires in issue order), so a row loaded by the core a step
-    // ahead leaves part of the HBM latency in every step.  This wave loads
-    // the sample's A_in rows into an LDS FIFO of kPF rows by direct loads,
-    // kPF - 1 steps ahead of their use; only it waits for them, before the
-    // barrier after which the core reads the row.  Row r lives in slot
-    // r % kPF: the core reads row n between the barriers of steps n and
-    // n + 1, so the slot of row n - 1 is refilled (with row n + kPF - 1) after
-    // the barrier of step n.  Columns past n_1 repeat the last one (never
-    // read).
-    static __device__ __forceinline__ void pf_row(const CoreFwdArgs& a, const float* src, int lane, int r) {
-        const float* row = src + (size_t)r * a.n1;
-        lds_f32* dst = (lds_f32*)smem + (r % kPF) * SNN_PF_COLS;
-#pragma unroll
-        for (int i = 0; i < kPR; ++i)
-            __builtin_amdgcn_global_load_lds(row + min(i * 64 + lane, a.n1 - 1), (lds_ptr_t)(dst + i * 64), 4,
-                                             0, 0);
-    }
-
-    static __device__ __forceinline__ void pf_run(const CoreFwdArgs& a, int b, int lane) {
-        const int T = a.T;
-        const float* src = a.A_in + (size_t)b * T * a.n1;
-        for (int r = 0; r < min(kPF - 1, T); ++r) pf_row(a, src, lane, r);
-        asm volatile("" ::: "memory");
-        __builtin_amdgcn_s_barrier();                    // the rings are zeroed
-        asm volatile("" ::: "memory");
-        for (int n = 0; n < T; ++n) {
-            // row n is in; rows n + 1 .. n + kPF - 2 may still be in flight
-            if (n + kPF - 2 < T)
-                __builtin_amdgcn_s_waitcnt(wait_vm(kPR * (kPF - 2)));
-            else
-                __builtin_amdgcn_s_waitcnt(kWaitVm0);
-            __builtin_amdgcn_s_barrier();                // the masks of step n are in
-            asm volatile("" ::: "memory");
-            if (n + kPF - 1 < T) pf_row(a, src, lane, n + kPF - 1);
-        }
     }
 
     // ---- cluster mode: wave 0 of a workgroup runs its 64 neurons of every
@@ -699,12 +645,6 @@ struct FwdCore {
             return;
         }
         const int b = blockIdx.x, tid = threadIdx.x;
-        if constexpr (PF) {
-            if ((tid >> 6) == a.NW + (RO ? 1 : 0)) {
-                pf_run(a, b, tid & 63);
-                return;
-            }
-        }
         // ---- zero the ring columns this lane owns (rows 0 .. S, row S: dummy)
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
@@ -748,11 +688,10 @@ struct FwdCore {
 };
 
 // MAXT: the most LIF neurons per layer (threads of the core waves); with RO
-// the workgroup has one more wave, and at MAXT <= 256 (the input-arrival
-// wave) one more.  CL: cluster mode (MAXT = 64: the neuron wave, then one
-// wave per ring).
+// the workgroup has one more wave.  CL: cluster mode (MAXT = 64: the neuron
+// wave, then one wave per ring).
 template <int MAXT, int NL, int NP, bool RL, bool RO, bool CL = false>
-__global__ void __launch_bounds__(CL ? 64 * (1 + NL * NP) : MAXT + (RO ? 64 : 0) + (MAXT <= 256 ? 64 : 0))
+__global__ void __launch_bounds__(CL ? 64 * (1 + NL * NP) : MAXT + (RO ? 64 : 0))
     forward_core_kernel(CoreFwdArgs a) {
     FwdCore<MAXT, NL, NP, RL, RO, CL>::run(a);
 }

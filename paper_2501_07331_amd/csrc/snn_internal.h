@@ -15,12 +15,6 @@
 #define SNN_STEP_IDS 16
 #define SNN_STEP_ROW 20
 
-// LDS FIFO of the input-arrival wave of forward cores of at most 256 threads,
-// at LDS offset 0: rows of 256 floats (the input projection's arrivals of a
-// step), read 7 steps after their loads go out
-#define SNN_PF_ROWS 8
-#define SNN_PF_COLS 256
-
 // Device status word, one per handle.
 struct DevStatus {
     int bad_input;                   // input spike list or labels failed validation
