@@ -67,7 +67,7 @@ struct snn_net {
     int ro_fused, ro_off;       // the LI readout runs as one more wave of the forward core
     int read_threads;           // readout workgroup size
     size_t lds_core_f, lds_core_b, lds_scan, lds_read, lds_grad, lds_radj;
-    int mask_off, scan_tb, table_lds;
+    int mask_off, ids_off, scan_tb, table_lds;
     int bpart_off;              // backward-core LDS plan
     int bring_mode[SNN_MAX_LAYERS];   // adjoint ring of a LIF layer: -2 none, -1 HBM, >= 0 LDS
                                       // byte offset
@@ -378,7 +378,8 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
     // forward core: the delay rings [S+1][n_post] of the LIF->LIF projections
     // (row S: dummy), all in LDS or all in HBM, then the ballot masks [3][NL][NW]
     {
-        const size_t masks = align16((size_t)3 * std::max(t.n_lif, 1) * nwaves * sizeof(unsigned long long));
+        const size_t masks = align16((size_t)3 * std::max(t.n_lif, 1) * nwaves * sizeof(unsigned long long)) +
+                             align16((size_t)std::max(t.n_lif, 1) * net->core_threads * sizeof(int));
         size_t used = 0;
         for (int p = 0; p < t.P; ++p) {
             if (t.pre[p] == 0 || t.kind[t.post[p]] != SNN_LIF) continue;
@@ -391,6 +392,8 @@ extern "C" int snn_create(const snn_layer* layers, int32_t n_layers, float tau_m
             for (int p = 0; p < t.P; ++p) t.fring[p] = -1;
         }
         net->mask_off = (int)align16(used);
+        net->ids_off = net->mask_off +
+                       (int)align16((size_t)3 * std::max(t.n_lif, 1) * nwaves * sizeof(unsigned long long));
         net->lds_core_f = net->mask_off + masks;
         // cluster mode where the rings do not fit (or on request): each
         // workgroup holds 64 columns of every ring, the masks of all G
@@ -909,6 +912,7 @@ extern "C" int snn_forward(snn_net* net, const snn_spikes_in* in, const float* c
         a.If = net->If;
         a.st = net->st;
         a.mask_off = net->mask_off;
+        a.ids_off = net->ids_off;
         if (net->ro_fused) {
             a.ro_C = C;
             a.ro_feed = t.lif[t.pre[t.out_p]];

@@ -184,15 +184,35 @@ struct FwdCore {
         }
     }
 
-    // All spikes of layer l at step e (mask words m), from position `from` on,
-    // in chunks of KB with their weights loaded now.
+    // Ids of spikes q0 .. q0 + N of layer l's list of the step in LDS (one
+    // workgroup per sample), uniform; -1 past the step's count.  Reading them
+    // costs one LDS round trip where finding them lane by lane in the mask
+    // words costs about sixty vector instructions a chunk.
+    template <int N>
+    static __device__ __forceinline__ void list_ids(const CoreFwdArgs& a, int l, int q0, int total,
+                                                    int (&ids)[N]) {
+        const int* list = reinterpret_cast<const int*>(smem + a.ids_off) + l * a.NW * 64;
+        const int last = a.NW * 64 - 1;
+#pragma unroll
+        for (int k = 0; k < N; ++k) {
+            const int v = __builtin_amdgcn_readfirstlane(list[min(q0 + k, last)]);
+            ids[k] = (q0 + k < total) ? v : -1;
+        }
+    }
+
+    // All spikes of layer l at step e (mask words m), in chunks of KI with
+    // their weights loaded now; outside cluster mode the chunk's ids come
+    // from the step's list in LDS.
     static __device__ __forceinline__ void scatter_rest(const CoreFwdArgs& a, int b, int l, int tid,
                                                         int j, int e, const unsigned long long (&m)[NWM],
-                                                        const unsigned long long* row, int from, int total) {
+                                                        const unsigned long long* row, int total) {
         const FwdLayer& y = a.ly[l];
-        for (int q0 = from; q0 < total; q0 += KI) {
+        for (int q0 = 0; q0 < total; q0 += KI) {
             int ids[KI];
-            word_ids<NWM, KI, CL>(m, row, a.NW, q0, ids);
+            if constexpr (CL)
+                word_ids<NWM, KI, CL>(m, row, a.NW, q0, ids);
+            else
+                list_ids<KI>(a, l, q0, total, ids);
 #pragma unroll
             for (int pp = 0; pp < NP; ++pp) {
                 if (pp >= y.npost) continue;
@@ -293,7 +313,7 @@ struct FwdCore {
         lds_f32* col = ro_col(a, lane, stride);
         for (int q0 = 0; q0 < total; q0 += KB) {
             int ids[KB];
-            word_ids<NWM, KB>(mw, row, a.NW, q0, ids);
+            list_ids<KB>(a, a.ro_feed, q0, total, ids);
             uint2 w[KB];
             ro_load(a, lane, ids, w);
             ro_add(a, e, total - q0, w, col, stride);
@@ -317,6 +337,7 @@ struct FwdCore {
         LiState q{};
         for (int n = 0; n < a.T; ++n) {
             __syncthreads();
+            __syncthreads();                             // the step's spike lists are in
             ro_step<SUM>(a, lane, n, masks + (size_t)((n % 3) * NL + a.ro_feed) * a.NW, q);
         }
         ro_finish(a, b, lane, q);
@@ -458,6 +479,13 @@ struct FwdCore {
         unsigned long long mw[NL][NWM];
         int tot[NL], rank[NL], cnt0[NL];
         counts(a, masks + (size_t)par * NL * NW, wave, mine, mw, tot, rank, cnt0, L);
+        // every spike's neuron at its rank in its layer's list of the step,
+        // which all waves read after one more barrier
+        int* lists = reinterpret_cast<int*>(smem + a.ids_off);
+#pragma unroll
+        for (int l = 0; l < NL; ++l)
+            if (spk[l]) lists[l * NW * 64 + rank[l]] = tid;
+        __syncthreads();
 
         // the input arrival loaded a step ago (P) has landed
         __builtin_amdgcn_s_waitcnt(kWaitVm0);
@@ -465,7 +493,7 @@ struct FwdCore {
         // ---- this step's spikes into the rings (all delays)
 #pragma unroll
         for (int l = 0; l < NL; ++l)
-            scatter_rest(a, b, l, tid, tid, n, mw[l], masks + (size_t)(par * NL + l) * NW, 0, tot[l]);
+            scatter_rest(a, b, l, tid, tid, n, mw[l], masks + (size_t)(par * NL + l) * NW, tot[l]);
         N.ain = L.ain[min(n + 1, T - 1) * a.n1];
 
         records(a, 0, tid, tid, n, spk, rank, cnt0, tot, L);

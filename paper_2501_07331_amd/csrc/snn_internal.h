@@ -132,6 +132,7 @@ struct CoreFwdArgs {
     float* If;
     DevStatus* st;
     int mask_off;                      // byte offset of the ballot masks [3][NL][NW] in LDS
+    int ids_off;                       // byte offset of the step's spike lists [NL][64 NW] in LDS
     // the LI readout fused into the core as one extra wave (ro_C > 0): lane
     // k < ro_C owns output k; arrivals in an LDS ring [ro_S + 1][ro_C] (row
     // ro_S: dummy) at byte offset ro_off
