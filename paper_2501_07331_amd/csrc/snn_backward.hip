@@ -276,7 +276,7 @@ struct BwdCore {
 #pragma unroll
                 for (int q = q0; q < q0 + 4; ++q) {
                     // (unsigned: a stale entry's offset wraps instead of overflowing)
-                    const unsigned off = (unsigned)col8 + (unsigned)idc[q] * (unsigned)(nq * 8);
+                    const unsigned off = (unsigned)col8 + __umul24((unsigned)idc[q], (unsigned)(nq * 8));
                     const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, (int)off, 0, 0);
                     ws[pp][q] = make_uint2((unsigned)v[0], (unsigned)v[1]);
                 }
@@ -343,7 +343,7 @@ struct BwdCore {
                 // (in LDS the row is always in the ring and the column is
                 // clamped into it, so the read needs no mask; its value does)
                 if (RL)
-                    d[k][pp] = ((lds_f64*)(smem + y.qring_lds[pp]))[row * nq + min(tid, nq - 1)];
+                    d[k][pp] = ((lds_f64*)(smem + y.qring_lds[pp]))[__umul24(row, nq) + min(tid, nq - 1)];
                 else   // (masked reads share one line of device memory)
                     d[k][pp] = ((global_f64*)(y.qring[pp] +
                                               ((size_t)b * S + (ok[k][pp] ? row : 0)) * nq))[ok[k][pp] ? tid : 0];
