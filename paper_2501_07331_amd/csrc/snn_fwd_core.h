@@ -4,11 +4,13 @@
 // current jumps).  Lane j owns neuron j of every LIF layer and column j of
 // every delay ring into that layer.
 //
-// Per step n: free dynamics, threshold and reset, wave ballots into LDS, one
-// barrier, the delayed scatter of the spikes into the rings of the LIF-post
-// projections, the spike records, and the arrivals (ring row n, projection
-// by projection in projection order).  A ring cell sums its weights in emission
-// order (step, then presynaptic neuron).
+// Per step n: free dynamics, threshold and reset, wave ballots into LDS, a
+// barrier, every spike's neuron into the step's spike list in LDS at its
+// rank, a second barrier, the delayed scatter of the spikes (ids from the
+// list) into the rings of the LIF-post projections, the spike records, and
+// the arrivals (ring row n, projection by projection in projection order).
+// A ring cell sums its weights in emission order (step, then presynaptic
+// neuron).
 //
 // The scatter of a step's spikes is immediate: in chunks, their weight rows
 // are loaded and added to the ring cells of their arrivals (delay 0
@@ -18,8 +20,8 @@
 // gone.)
 //
 // With RO, one more wave runs the leaky-integrator readout fed by a LIF
-// layer, in its own loop with one barrier per step like the core waves:
-// after the barrier of step n it reads that layer's spike masks of step n,
+// layer, in its own loop with the core waves' two barriers per step: after
+// the barriers of step n it reads that layer's spike list of step n,
 // adds the spikes' readout weights to the ring cells of their arrivals (an
 // LDS ring of S_out + 1 rows, emission order per cell) and runs the LI step
 // n.  Its work overlaps the core waves' own scatter instead of following the
@@ -297,9 +299,10 @@ struct FwdCore {
         column_add(col, stride, rw, wv);
     }
 
-    // Step e of the readout (after the step's barrier): the feeding layer's
-    // spikes of step e (masks row `row`) into the ring, chunk by chunk, then
-    // the LI step with the arrivals of row e.
+    // Step e of the readout (after the step's barriers): the feeding layer's
+    // spikes of step e (their count from the masks row `row`, their ids from
+    // the step's list) into the ring, chunk by chunk, then the LI step with
+    // the arrivals of row e.
     template <bool SUM>
     static __device__ __forceinline__ void ro_step(const CoreFwdArgs& a, int lane, int e,
                                                    const unsigned long long* row, LiState& q) {
@@ -328,7 +331,7 @@ struct FwdCore {
         li_update<SUM>(a.alpha, a.beta, a.gamma, e, x, q);
     }
 
-    // The readout wave's loop: one barrier per step, as the core waves' steps
+    // The readout wave's loop: two barriers per step, as the core waves' steps
     // (the branch is per wave, so every wave reaches every barrier); then the
     // results.
     template <bool SUM>
