@@ -342,3 +342,43 @@ def test_parity_fine_dt_long_T():
     assert_forward_bitexact(gpu, orc, wl)
     assert np.allclose(gpu["loss"], orc["loss"], rtol=1e-6, atol=1e-7)
     assert_backward_close(gpu, orc)
+
+
+def test_parity_synchronous_bursts():
+    """Input spikes that drive every hidden neuron over threshold within a
+    step or two: steps with up to all 256 neurons spiking at once, so the
+    step's spike list is filled by every wave and read in many chunks by the
+    scatter and the readout wave (the 700-256rec-20 network, B = 2)."""
+    import dataclasses
+
+    from workloads import Workload
+    from workloads.configs import CONFIGS
+    from workloads.generators import labels
+
+    cfg = dataclasses.replace(CONFIGS[4], name="bursts-700-256rec-20")
+    B, T = 2, 200
+    rng = np.random.default_rng(2024)
+    steps, neurons, off = [], [], [0]
+    for b in range(B):
+        t = np.sort(rng.choice(np.arange(5, T - 20), size=6, replace=False))
+        steps.append(t)
+        neurons.append(rng.integers(0, 700, size=t.size))
+        off.append(off[-1] + t.size)
+    st = np.concatenate(steps).astype(np.int32)
+    ne = np.concatenate(neurons).astype(np.int32)
+    off = np.array(off, dtype=np.int32)
+    W = [rng.uniform(9.5, 10.5, size=(700, 256)).astype(np.float32),
+         rng.normal(0.0, 0.02, size=(256, 256)).astype(np.float32),
+         rng.normal(0.0, 0.1, size=(256, 20)).astype(np.float32)]
+    D = [np.zeros((700, 256), dtype=np.float32),
+         rng.uniform(0.0, 50.0, size=(256, 256)).astype(np.float32),
+         rng.uniform(0.0, 150.0, size=(256, 20)).astype(np.float32)]
+    wl = Workload(cfg, B, T, off, st, ne, W, D, labels(cfg, B))
+    gpu, orc = _parity(wl)
+    f = orc["fwd"]
+    most = 0
+    for b in range(B):
+        c = int(f.count[0, b])
+        most = max(most, int(np.bincount(f.step[0, b, :c], minlength=T).max()))
+    print(f"[bursts] most spikes in one step of a sample: {most}", flush=True)
+    assert most >= 200
